@@ -1,0 +1,12 @@
+"""fp64 CPU oracle of the LionMuon step (test infrastructure only; see
+``oracle.lionmuon_oracle``)."""
+from .lionmuon_oracle import (CUBIC, NS_EPS, NS_STEPS, QUINTIC, SCALE_NONE,
+                              SCALE_RMS02, elementwise_sign, is_muon_step,
+                              lionmuon_step, lionmuon_update, newton_schulz,
+                              ns_output_scale, stable_rank_estimate)
+
+__all__ = [
+    "CUBIC", "NS_EPS", "NS_STEPS", "QUINTIC", "SCALE_NONE", "SCALE_RMS02",
+    "elementwise_sign", "is_muon_step", "lionmuon_step", "lionmuon_update",
+    "newton_schulz", "ns_output_scale", "stable_rank_estimate",
+]

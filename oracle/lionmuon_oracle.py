@@ -1,0 +1,179 @@
+"""Plain fp64 CPU oracle of the LionMuon optimizer step.
+
+TEST INFRASTRUCTURE ONLY. Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this module. The GPU product
+path (``paper_2605_19811_amd``) never imports it and shares no code, header,
+constant table or helper with it.
+
+Every function follows the paper (arXiv 2605.19811, "LionMuon: Alternating
+Spectral and Sign Descent for Efficient Training"):
+
+* Algorithm 1 (Section 3, "LionMuon and SignMuon"): the per-matrix update
+  rule -- Lion interpolation, the ``t mod P`` branch between a Muon step and a
+  Lion step, decoupled weight decay on both branches, and the momentum update
+  done after the branch, every step.
+* Section 2 (Related works, "Spectral methods" and "Approximating the matrix
+  sign"): the Muon direction is msign(X) = U V^T approximated by K steps of an
+  odd-polynomial Newton-Schulz iteration.
+* Section 3, "Implementation notes": one momentum buffer per parameter; 1-D
+  parameters do not take the spectral branch.
+* Table 4 (Appendix, full experimental setup): K_NS = 5 and the optional NS
+  output scaling 0.2*sqrt(max(m, n)).
+
+Readings where the paper is silent (each listed in the design doc):
+
+* The quintic coefficients (a, b, c) = (3.4445, -4.7750, 2.0315) are the ones
+  published with Muon (the paper cites it as the source of the NS step); the
+  paper prints none.
+* Frobenius pre-normalisation X0 = Ghat / (||Ghat||_F + eps), eps = 1e-7.
+* A tall matrix (m > n) is iterated in transposed form; in exact arithmetic
+  NS(X^T) = NS(X)^T, so this changes cost, not the result.
+* sign(0) = 0.
+
+All arithmetic is float64 numpy: a plain, obviously-correct restatement with
+no blocking, no symmetry tricks and no batching. Pinned by
+``tests/test_oracle.py`` against SVD closed forms, the textbook cubic
+iteration's limit (the polar factor), brute force on tiny inputs and the
+invariants the paper states.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+# Odd quintic p(x) = a*x + b*x^3 + c*x^5 of the Muon Newton-Schulz step
+# (coefficients published with Muon; reading, the paper prints none).
+QUINTIC = (3.4445, -4.7750, 2.0315)
+# Classical cubic Newton-Schulz p(x) = 1.5*x - 0.5*x^3 (converges to U V^T).
+CUBIC = (1.5, -0.5, 0.0)
+
+NS_STEPS = 5          # K_NS, Table 4
+NS_EPS = 1e-7         # Frobenius pre-normalisation guard (reading)
+
+SCALE_NONE = 0        # Algorithm 1 uses NS output as is
+SCALE_RMS02 = 1       # Table 4: NS output times 0.2*sqrt(max(m, n))
+
+
+def is_muon_step(t: int, P: int) -> bool:
+    """Branch rule of Algorithm 1: the Muon branch is taken iff t mod P == 0.
+
+    P = 0 encodes P = infinity (the Muon branch is never taken).
+    """
+    if P < 0 or t < 0:
+        raise ValueError("t and P must be non-negative")
+    if P == 0:
+        return False
+    return t % P == 0
+
+
+def elementwise_sign(x: np.ndarray) -> np.ndarray:
+    """sign(x) with sign(0) = 0: the LMO of the max-norm (Section 2, notation)."""
+    return np.sign(np.asarray(x, dtype=np.float64))
+
+
+def ns_output_scale(m: int, n: int, scale_mode: int) -> float:
+    """Optional NS output scaling of Table 4 (0.2*sqrt(max(m, n)))."""
+    if scale_mode == SCALE_NONE:
+        return 1.0
+    if scale_mode == SCALE_RMS02:
+        return 0.2 * math.sqrt(max(m, n))
+    raise ValueError(f"unknown scale mode {scale_mode}")
+
+
+def newton_schulz(G: np.ndarray, steps: int = NS_STEPS, coeffs=QUINTIC,
+                  eps: float = NS_EPS) -> np.ndarray:
+    """NS_K(G): K Newton-Schulz steps towards msign(G) = U V^T (Section 2).
+
+    X0 = G / (||G||_F + eps), oriented so that X has no more rows than
+    columns; each step forms A = X X^T, B = b*A + c*A A and X <- a*X + B X;
+    the result is turned back to G's orientation.
+    """
+    a, b, c = (float(v) for v in coeffs)
+    X = np.array(G, dtype=np.float64, copy=True)
+    if X.ndim != 2:
+        raise ValueError("Newton-Schulz needs a 2-D matrix")
+    transposed = X.shape[0] > X.shape[1]
+    if transposed:
+        X = X.T
+    X = X / (np.linalg.norm(X, "fro") + eps)
+    for _ in range(steps):
+        A = X @ X.T
+        B = b * A + c * (A @ A)
+        X = a * X + B @ X
+    if transposed:
+        X = X.T
+    return X
+
+
+def lionmuon_update(W, G, M, t, P, beta1, beta2, lr_muon, lr_lion, wd, *,
+                    lion_only=False, ns_steps=NS_STEPS, coeffs=QUINTIC,
+                    eps=NS_EPS, scale_mode=SCALE_NONE):
+    """One step of Algorithm 1 for one parameter tensor, in float64.
+
+    Ghat = beta1*M + (1-beta1)*G (interpolation with the PRE-update buffer);
+    Muon branch (t mod P == 0, 2-D, not lion_only):
+        W' = W - lr_muon * (kappa*NS_K(Ghat) + wd*W)
+    Lion branch otherwise:
+        W' = W - lr_lion * (sign(Ghat) + wd*W)
+    then M' = beta2*M + (1-beta2)*G.  Returns (W', M').
+    """
+    W = np.asarray(W, dtype=np.float64)
+    G = np.asarray(G, dtype=np.float64)
+    M = np.asarray(M, dtype=np.float64)
+    if not (W.shape == G.shape == M.shape):
+        raise ValueError("W, G, M must have one shape")
+    Ghat = beta1 * M + (1.0 - beta1) * G
+    spectral = (W.ndim == 2 and min(W.shape) > 1 and not lion_only
+                and is_muon_step(t, P))
+    if spectral:
+        kappa = ns_output_scale(W.shape[0], W.shape[1], scale_mode)
+        direction = kappa * newton_schulz(Ghat, ns_steps, coeffs, eps)
+        W_new = W - lr_muon * (direction + wd * W)
+    else:
+        W_new = W - lr_lion * (elementwise_sign(Ghat) + wd * W)
+    M_new = beta2 * M + (1.0 - beta2) * G
+    return W_new, M_new
+
+
+def lionmuon_step(params, grads, moms, t, P, beta1, beta2, lr_muon, lr_lion,
+                  wd, *, lion_only=None, **ns_kwargs):
+    """Algorithm 1 applied to every tensor of a parameter list.
+
+    ``lion_only`` is an optional per-tensor flag list; 1-D tensors never take
+    the spectral branch (Section 3, implementation notes). Returns the lists
+    (W', M') in float64.
+    """
+    n = len(params)
+    if lion_only is None:
+        lion_only = [False] * n
+    out_w, out_m = [], []
+    for W, G, M, lo in zip(params, grads, moms, lion_only):
+        w, m = lionmuon_update(W, G, M, t, P, beta1, beta2, lr_muon, lr_lion,
+                               wd, lion_only=lo, **ns_kwargs)
+        out_w.append(w)
+        out_m.append(m)
+    return out_w, out_m
+
+
+def stable_rank_estimate(M: np.ndarray, power_steps: int = 10,
+                         v0: np.ndarray | None = None) -> float:
+    """r_hat(M) = ||M||_F^2 / sigma_hat_1(M)^2 (Appendix G, adaptive rule).
+
+    sigma_hat_1 is taken from ``power_steps`` power-iteration steps on M^T M
+    started from ``v0`` (all-ones when not given).
+    """
+    M = np.asarray(M, dtype=np.float64)
+    n = M.shape[1]
+    v = np.ones(n) if v0 is None else np.asarray(v0, dtype=np.float64)
+    v = v / np.linalg.norm(v)
+    for _ in range(power_steps):
+        w = M.T @ (M @ v)
+        nw = np.linalg.norm(w)
+        if nw == 0.0:
+            return 0.0
+        v = w / nw
+    sigma1 = np.linalg.norm(M @ v)
+    if sigma1 == 0.0:
+        return 0.0
+    return float(np.linalg.norm(M, "fro") ** 2 / sigma1 ** 2)
