@@ -1,0 +1,249 @@
+"""Benchmark of the LionMuon optimizer step on one MI355X.
+
+One step = one pass of Algorithm 1 over the whole matrix set (the Lion branch
+kernel on Lion steps; preparation, Frobenius norm and five Newton-Schulz
+iterations on Muon steps, every P-th step). Reported: amortised ms/step over
+K timed steps (K a multiple of P), Lion GB/s (20 bytes per element) and
+Newton-Schulz TFLOP/s (symmetric algorithmic flops), with the roofline of the
+dominant kernel measured by the library's per-launch HIP events on the launch
+stream, and the fp64 CPU oracle timed on a bounded sample as a baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workloads  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0            # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2516.6         # dense MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
+FP32_MFMA_PEAK_TFLOPS = 157.3
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2605_19811_amd", "csrc", "kernels.hip")
+TRAFFIC_DIR = os.path.join(ROOT, "profiles")
+
+
+def kernel_hash():
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(workload, kernel):
+    """HBM traffic (bytes per launch) from the committed rocprofv3 counter
+    summary, or None when absent or taken from another kernel source."""
+    path = os.path.join(TRAFFIC_DIR, f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("kernel_source_sha256_16") != kernel_hash():
+        return None
+    k = d.get("kernels", {}).get(kernel)
+    return None if k is None else k.get("bytes_per_launch")
+
+
+def ns_flops_per_launch(wl):
+    gram = poly = apply = 0.0
+    for t in wl.tensors:
+        if t.lion_only or t.rows == 1:
+            continue
+        s, l = min(t.rows, t.cols), max(t.rows, t.cols)
+        gram += s * (s + 1) * l
+        poly += s * s * (s + 1)
+        apply += 2.0 * s * s * l
+    return {"gram": gram, "poly": poly, "apply": apply}
+
+
+def cpu_baseline(wl, P):
+    """fp64 oracle on a bounded sample: one Lion step and one Muon step on one
+    tensor of every distinct shape, scaled to the whole set by element count
+    (Lion) and by Newton-Schulz flops (Muon), amortised over P."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = len(os.sched_getaffinity(0))
+    seen, sample = {}, []
+    for i, t in enumerate(wl.tensors):
+        key = (t.rows, t.cols, t.lion_only)
+        seen[key] = seen.get(key, 0) + 1
+        if seen[key] == 1:
+            sample.append(i)
+    count = {k: v for k, v in seen.items()}
+    t_lion = t_muon = 0.0
+    rng = np.random.default_rng(0)
+    for i in sample:
+        t = wl.tensors[i]
+        reps = count[(t.rows, t.cols, t.lion_only)]
+        W = rng.standard_normal(t.shape).astype(np.float32) * 0.02
+        M = rng.standard_normal(t.shape).astype(np.float32) * wl.grad_std
+        G = rng.standard_normal(t.shape).astype(np.float32) * wl.grad_std
+        t0 = time.perf_counter()
+        oracle.lionmuon_update(W, G, M, 1, P, wl.beta1, wl.beta2, wl.lr_muon, wl.lr_lion,
+                               wl.wd, lion_only=True)
+        t1 = time.perf_counter()
+        oracle.lionmuon_update(W, G, M, 0, 1, wl.beta1, wl.beta2, wl.lr_muon, wl.lr_lion,
+                               wl.wd, lion_only=t.lion_only)
+        t2 = time.perf_counter()
+        t_lion += (t1 - t0) * reps
+        t_muon += (t2 - t1) * reps
+    if P == 0:
+        amort = t_lion
+    else:
+        amort = ((P - 1) * t_lion + t_muon) / P
+    return {"value": round(amort * 1e3, 1), "unit": "ms/step", "cores": int(cores),
+            "kind": "oracle",
+            "sample": (f"one Lion and one Muon fp64 oracle step on one tensor of each of the "
+                       f"{len(sample)} distinct shapes of {wl.name}, scaled by tensor count; "
+                       f"Lion {t_lion * 1e3:.0f} ms/step, Muon {t_muon * 1e3:.0f} ms/step, "
+                       f"amortised over P={P}")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="gpt2-124m", choices=sorted(workloads.WORKLOADS))
+    ap.add_argument("--P", type=int, default=2, help="period; 0 = pure Lion")
+    ap.add_argument("--pure-muon", action="store_true", help="P=1 with beta1=beta2=0.9")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true",
+                    help="time without per-launch events (no roofline object)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
+              f"layout is a design, not a build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2605_19811_amd import lionmuon as lm
+
+    wl = workloads.get(args.workload)
+    P = 1 if args.pure_muon else args.P
+    beta1, beta2 = (0.9, 0.9) if args.pure_muon else (wl.beta1, wl.beta2)
+    steps = args.steps
+    if P > 1 and steps % P:
+        steps += P - steps % P                 # whole periods only
+    dev = torch.device("cuda:0")
+    params, moms, grad_sets = workloads.device_state(torch, wl, dev, seed=7, warm=True, n_grad=2)
+    lion_only = [t.lion_only for t in wl.tensors]
+    lists = [lm.TensorList(params, g, moms, lion_only) for g in grad_sets]
+    cfg = lm.config(ns_precision=wl.ns_precision, lr_muon=wl.lr_muon, lr_lion=wl.lr_lion)
+    specs = [(t.rows, t.cols, t.lion_only) for t in wl.tensors]
+    info_muon = lm.lionmuon_plan_info(specs, 0, 1, cfg)
+    info_lion = lm.lionmuon_plan_info(specs, 1, 2, cfg)
+    stream = torch.cuda.current_stream()
+
+    def run(t0, n):
+        for k in range(n):
+            t = t0 + k
+            lm.lionmuon_step_ex(None, None, None, t, P, beta1, beta2, wl.wd, cfg,
+                                stream=stream, tensors=lists[t % 2])
+
+    run(1, args.warmup)
+    torch.cuda.synchronize()
+    t_start = 1 + args.warmup
+    t_start += (-t_start) % max(P, 1)         # timed region starts on a Muon step
+    profile = not args.no_profile
+    if profile:
+        lm.lionmuon_profiling_reset()
+        lm.lionmuon_profiling_enable(True)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    run(t_start, steps)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = e0.elapsed_time(e1)
+    ms_step = total_ms / steps
+    phases = None
+    if profile:
+        phases = lm.lionmuon_profiling_read()
+        lm.lionmuon_profiling_enable(False)
+
+    n_muon_steps = sum(1 for k in range(steps) if P >= 1 and (t_start + k) % P == 0)
+    n_lion_steps = steps - n_muon_steps
+    out = {
+        "metric": "amortised optimizer-step ms per period P (LionMuon step, 1 GPU)",
+        "value": round(ms_step, 4),
+        "unit": "ms/step",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.ns_precision == "bf16" else "f32",
+        "data": "synthetic (seeded gradients of the workload's shapes; random-init weights)",
+        "config": {"workload": wl.name, "P": P, "beta1": beta1, "beta2": beta2,
+                   "n_tensors": len(wl.tensors), "elements": wl.numel,
+                   "muon_elements": info_muon["muon_elements"],
+                   "ns_precision": wl.ns_precision, "ns_steps": 5,
+                   "state": "fp32 W, M, G; bf16 MFMA Newton-Schulz with fp32 accumulation"},
+    }
+    if phases is not None:
+        flops = ns_flops_per_launch(wl)
+        ph = {}
+        for name, v in phases.items():
+            if v["launches"] == 0:
+                continue
+            avg = v["ms"] / v["launches"]
+            entry = {"launches": v["launches"], "avg_ms": round(avg, 5)}
+            if name in flops:
+                entry["tflops"] = round(flops[name] / (avg * 1e-3) / 1e12, 1)
+                entry["frac_bf16_peak"] = round(entry["tflops"] / BF16_PEAK_TFLOPS, 4)
+            if name == "lion":
+                # Lion steps update every tensor; Muon steps only the Lion-only ones
+                lion_elems = n_lion_steps * info_lion["lion_elements"]
+                if n_muon_steps and info_muon["lion_elements"]:
+                    lion_elems += n_muon_steps * info_muon["lion_elements"]
+                bytes_launch = 20.0 * lion_elems / v["launches"]
+                entry["gbps"] = round(bytes_launch / (avg * 1e-3) / 1e9, 1)
+                entry["frac_hbm_peak"] = round(entry["gbps"] / HBM_PEAK_GBPS, 4)
+            ph[name] = entry
+        out["phases"] = ph
+        ns_ms = sum(phases[p]["ms"] for p in ("gram", "poly", "apply"))
+        if n_muon_steps:
+            out["ns_tflops"] = round(info_muon["ns_flops"] * n_muon_steps / (ns_ms * 1e-3) / 1e12, 1)
+            out["ns_frac_bf16_peak"] = round(out["ns_tflops"] / BF16_PEAK_TFLOPS, 4)
+            out["ns_ms_per_muon_step"] = round(ns_ms / n_muon_steps, 4)
+        if "lion" in ph:
+            out["lion_gbps"] = ph["lion"]["gbps"]
+            out["lion_frac_hbm_peak"] = ph["lion"]["frac_hbm_peak"]
+        # dominant kernel: most total time in the timed region
+        dom = max((p for p in phases if phases[p]["launches"]), key=lambda p: phases[p]["ms"])
+        d = ph[dom]
+        kernel_names = {"lion": "lion_kernel", "prep": "prep_kernel", "norm": "norm_kernel",
+                        "gram": "gemm_kernel<bf16, Gram>", "poly": "gemm_kernel<bf16, Poly>",
+                        "apply": "gemm_kernel<bf16, Apply>"}
+        if dom in flops:
+            roof = {"kernel": kernel_names[dom], "bound": "mfma", "achieved": d["tflops"],
+                    "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": d["frac_bf16_peak"]}
+        elif dom == "lion":
+            roof = {"kernel": kernel_names[dom], "bound": "hbm", "achieved": d["gbps"],
+                    "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": d["frac_hbm_peak"]}
+        else:
+            roof = {"kernel": kernel_names[dom], "bound": "hbm", "achieved": None,
+                    "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": None}
+        roof["avg_launch_ms"] = d["avg_ms"]
+        roof["traffic"] = load_traffic(wl.name, dom)
+        out["roofline"] = roof
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, P)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

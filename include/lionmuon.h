@@ -1,0 +1,205 @@
+/*
+ * lionmuon.h -- C ABI of the MI355X (gfx950) LionMuon optimizer step.
+ *
+ * The operation is Algorithm 1 of "LionMuon: Alternating Spectral and Sign
+ * Descent for Efficient Training" (arXiv 2605.19811, Section 3), applied to a
+ * list of fp32 parameter tensors that each own one momentum buffer
+ * (Section 3, implementation notes):
+ *
+ *   Ghat = beta1*M + (1-beta1)*G                 Lion interpolation, with the
+ *                                                buffer BEFORE this step's update
+ *   if t mod P == 0 (Muon step, 2-D tensors that are not Lion-only):
+ *       W <- W - lr_muon * (kappa*NS_K(Ghat) + wd*W)
+ *   else (Lion step):
+ *       W <- W - lr_lion * (sign(Ghat) + wd*W)   sign(0) = 0
+ *   M <- beta2*M + (1-beta2)*G                   every step, every tensor
+ *
+ * NS_K is K steps of the odd quintic Newton-Schulz iteration towards the
+ * matrix sign msign(X) = U V^T (Section 2, "Spectral methods" and
+ * "Approximating the matrix sign"; K_NS = 5 in Table 4):
+ *   X0 = Ghat / (||Ghat||_F + eps), iterated in the orientation with
+ *   rows <= cols; each step A = X X^T, B = b*A + c*A A, X <- a*X + B X.
+ * kappa is 1 (Algorithm 1) or 0.2*sqrt(max(m, n)) (Table 4 "NS scaling").
+ *
+ * Conventions shared by every entry point:
+ *  - Pointer arrays (params, grads, momentum, shapes) live in HOST memory;
+ *    the pointers they hold are DEVICE pointers to fp32, contiguous,
+ *    row-major tensors owned by the caller. 1-D tensors use rows = 1.
+ *  - params and momentum are updated in place; grads are read only. The
+ *    three buffers of one tensor must not overlap (checked).
+ *  - Every call is asynchronous on `stream` (0 = the null stream) and returns
+ *    once all work is enqueued; no host synchronisation is performed.
+ *  - Validation happens before anything is enqueued: an invalid call returns
+ *    an error and modifies nothing. A HIP failure after enqueueing started
+ *    returns LM_ERR_HIP; tensors may then be partly updated.
+ *  - lionmuon_last_error() gives a thread-local message for the last failure.
+ *  - Calls that use the library-owned workspace are serialised by a mutex;
+ *    calls with caller workspaces may run concurrently on distinct streams.
+ */
+#ifndef LIONMUON_H
+#define LIONMUON_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LIONMUON_ABI_VERSION 1
+
+typedef enum lm_status {
+  LM_OK = 0,
+  LM_ERR_INVALID_ARGUMENT = 1,   /* null pointer, bad size, beta outside [0,1), ... */
+  LM_ERR_UNSUPPORTED = 2,        /* valid request the library does not implement     */
+  LM_ERR_OUT_OF_MEMORY = 3,      /* library-owned workspace or plan allocation failed */
+  LM_ERR_WORKSPACE_TOO_SMALL = 4,/* caller workspace below lionmuon_workspace_bytes   */
+  LM_ERR_HIP = 5                 /* a HIP runtime call or kernel launch failed        */
+} lm_status;
+
+/* Per-tensor flag: never take the Muon branch (Lion update on every step).
+ * A tensor with rows == 1 or cols == 1 is always treated as Lion-only
+ * (1-D parameters do not take the spectral step, Section 3). */
+enum { LM_TENSOR_LION_ONLY = 1u };
+
+/* Precision of the Newton-Schulz matrix products. */
+enum { LM_NS_BF16 = 0,   /* bf16 operands on MFMA, fp32 accumulation, for every
+                            matrix whose short side is >= ns_bf16_min_side;
+                            smaller matrices use the fp32 path              */
+       LM_NS_FP32 = 1 }; /* fp32 operands on MFMA, fp32 accumulation        */
+
+/* Output scaling kappa of the Muon direction. */
+enum { LM_NS_SCALE_NONE = 0,    /* kappa = 1 (Algorithm 1)                        */
+       LM_NS_SCALE_RMS02 = 1 }; /* kappa = 0.2*sqrt(max(rows, cols)) (Table 4)    */
+
+/* Shape of one tensor: rows x cols, row-major; rows = 1 for a vector.
+ * rows = 0 or cols = 0 is an empty tensor (skipped). */
+typedef struct lm_shape {
+  int64_t rows;
+  int64_t cols;
+  uint32_t flags;      /* LM_TENSOR_* bits */
+  uint32_t reserved;   /* must be 0 */
+} lm_shape;
+
+/* Step configuration. Initialise with lionmuon_config_default().
+ * Hyper-parameters are passed in double; the kernels compute in fp32 with
+ * constants rounded once from the double values (1 - beta is formed in
+ * double before rounding). */
+typedef struct lm_config {
+  uint32_t struct_size;     /* sizeof(lm_config)                                 */
+  int32_t ns_steps;         /* K_NS in [1, 64], default 5 (Table 4)              */
+  double ns_a, ns_b, ns_c;  /* odd polynomial a x + b x^3 + c x^5,
+                               default (3.4445, -4.7750, 2.0315)                  */
+  double ns_eps;            /* Frobenius guard eps >= 0, default 1e-7            */
+  int32_t ns_precision;     /* LM_NS_BF16 (default) or LM_NS_FP32                */
+  int32_t ns_scale_mode;    /* LM_NS_SCALE_NONE (default) or LM_NS_SCALE_RMS02   */
+  double lr_muon;           /* eta_M >= 0 of the Muon branch (Algorithm 1)       */
+  double lr_lion;           /* eta_L >= 0 of the Lion branch (Algorithm 1)       */
+  int32_t ns_bf16_min_side; /* LM_NS_BF16 only: matrices with a shorter short
+                               side run the fp32 path; default 64, >= 0          */
+  int32_t reserved;         /* must be 0                                          */
+} lm_config;
+
+/* Fill *cfg with the defaults listed above; lr_muon = lr_lion = 0. */
+void lionmuon_config_default(lm_config* cfg);
+
+/*
+ * One LionMuon step (Algorithm 1) over n_tensors tensors with
+ * eta_M = eta_L = lr, bf16 Newton-Schulz and the other defaults.
+ *   params[i], grads[i], momentum[i]: device fp32, shapes[i].rows*cols values.
+ *   t >= 0: step index; the Muon branch fires iff P >= 1 and t mod P == 0.
+ *   P >= 0: period; P = 0 encodes P = infinity (pure Lion).
+ *   beta1, beta2 in [0, 1); lr >= 0; wd >= 0 (decoupled weight decay).
+ * Uses a library-owned device workspace, allocated on first Muon step and
+ * grown as needed (freed by lionmuon_release).
+ */
+lm_status lionmuon_step(float* const* params, const float* const* grads,
+                        float* const* momentum, const lm_shape* shapes,
+                        int32_t n_tensors, int64_t t, int32_t P, double beta1,
+                        double beta2, double lr, double wd, hipStream_t stream);
+
+/*
+ * lionmuon_step with an explicit configuration (two learning rates, fp32 or
+ * bf16 Newton-Schulz, coefficients, eps, output scaling) and an optional
+ * caller-owned device workspace. workspace == NULL with workspace_bytes == 0
+ * selects the library-owned workspace; otherwise workspace must hold at least
+ * lionmuon_workspace_bytes(...) bytes, be 256-byte aligned, stay valid until
+ * the enqueued work finishes, and must not be used by a concurrent call.
+ */
+lm_status lionmuon_step_ex(float* const* params, const float* const* grads,
+                           float* const* momentum, const lm_shape* shapes,
+                           int32_t n_tensors, int64_t t, int32_t P, double beta1,
+                           double beta2, double wd, const lm_config* cfg,
+                           void* workspace, size_t workspace_bytes,
+                           hipStream_t stream);
+
+/* Device workspace (bytes) a Muon step over these tensors needs with cfg
+ * (NULL = defaults). A Lion step needs none. Host-only; no HIP call. */
+lm_status lionmuon_workspace_bytes(const lm_shape* shapes, int32_t n_tensors,
+                                   const lm_config* cfg, size_t* out_bytes);
+
+/*
+ * Newton-Schulz hook (Section 2): O[b] = kappa * NS_K(X[b]) for a batch of
+ * `batch` same-shape rows x cols fp32 device matrices stored back to back
+ * (X and O each hold batch*rows*cols values; they must not overlap).
+ * Uses the same kernels as the Muon branch of lionmuon_step_ex.
+ * workspace/workspace_bytes as in lionmuon_step_ex, sized by
+ * lionmuon_workspace_bytes for `batch` tensors of this shape.
+ */
+lm_status lionmuon_ns(const float* X, float* O, int64_t rows, int64_t cols,
+                      int32_t batch, const lm_config* cfg, void* workspace,
+                      size_t workspace_bytes, hipStream_t stream);
+
+/* Host-side description of the work one step would enqueue (no HIP call). */
+typedef struct lm_plan_info {
+  int32_t n_tensors;        /* non-empty tensors                               */
+  int32_t n_lion;           /* tensors updated by the Lion branch this step    */
+  int32_t n_muon;           /* matrices updated by the Muon branch this step   */
+  int32_t n_shape_classes;  /* distinct (short side, long side) Muon shapes    */
+  int64_t lion_elements;    /* elements on the Lion branch                     */
+  int64_t muon_elements;    /* elements on the Muon branch                     */
+  int64_t gram_tiles, poly_tiles, apply_tiles; /* MFMA output tiles per NS step */
+  double ns_flops;          /* algorithmic NS flops, symmetric products counted
+                               once: K * sum s(s+1)l + s^2(s+1) + 2 s^2 l       */
+  double ns_flops_dense;    /* dense convention K * sum 4 s^2 l + 2 s^3        */
+  double lion_bytes;        /* 20 bytes per Lion-branch element                 */
+  size_t workspace_bytes;   /* device workspace this step needs                */
+} lm_plan_info;
+
+lm_status lionmuon_plan_info(const lm_shape* shapes, int32_t n_tensors,
+                             int64_t t, int32_t P, const lm_config* cfg,
+                             lm_plan_info* out);
+
+/*
+ * Phase timing. When enabled, every call records HIP events around each
+ * kernel it enqueues, on the call's stream; lionmuon_profiling_read waits for
+ * the recorded events and returns per-phase sums (ms) and launch counts since
+ * the last reset. Disabled by default; enabling costs one event pair per
+ * launch.
+ */
+enum { LM_PHASE_LION = 0, LM_PHASE_PREP = 1, LM_PHASE_NORM = 2,
+       LM_PHASE_GRAM = 3, LM_PHASE_POLY = 4, LM_PHASE_APPLY = 5,
+       LM_PHASE_COUNT = 6 };
+typedef struct lm_phase_times {
+  double ms[LM_PHASE_COUNT];
+  int64_t launches[LM_PHASE_COUNT];
+} lm_phase_times;
+lm_status lionmuon_profiling_enable(int32_t enable);
+lm_status lionmuon_profiling_read(lm_phase_times* out);
+lm_status lionmuon_profiling_reset(void);
+
+/* Free the library-owned workspace and cached plans (device memory). Must not
+ * be called while work enqueued by this library is still running. */
+void lionmuon_release(void);
+
+const char* lionmuon_status_string(lm_status status);
+const char* lionmuon_last_error(void);
+int32_t lionmuon_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIONMUON_H */

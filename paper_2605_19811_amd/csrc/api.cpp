@@ -1,0 +1,623 @@
+// C ABI of the LionMuon step (declared in include/lionmuon.h): validation,
+// the cache of uploaded plans, the library-owned workspace, phase timing and
+// the launch sequence of Algorithm 1 on one stream.
+#include <hip/hip_runtime_api.h>
+
+#include <cmath>
+#include <cstring>
+#include <list>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "lionmuon.h"
+#include "plan.h"
+
+namespace {
+
+using lm::Plan;
+using lm::Status;
+using lm::TensorIn;
+
+thread_local std::string g_last_error;
+
+lm_status fail(lm_status st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+lm_status to_c(Status s) { return static_cast<lm_status>(static_cast<int>(s)); }
+
+lm_status hip_fail(hipError_t e, const char* what) {
+  return fail(LM_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// ---------------------------------------------------------------------------
+// Uploaded plans
+// ---------------------------------------------------------------------------
+// One plan per (device, tensor list, step kind, NS element size, scaling).
+// Its descriptor tables live in one device allocation, filled once from a
+// pinned host copy on the stream of the call that created the plan.
+struct DevicePlan {
+  Plan plan;
+  int device = -1;
+  std::vector<uint8_t> key;
+  void* dev = nullptr;
+  void* host = nullptr;             // pinned staging copy (kept for the plan's life)
+  hipEvent_t uploaded = nullptr;
+  hipStream_t upload_stream = nullptr;
+  lm::LionTensor* d_lion = nullptr;
+  int32_t* d_lion_start = nullptr;
+  lm::MuonMat* d_mats = nullptr;
+  int32_t* d_prep_start = nullptr;
+  lm::GemmTask* d_tasks[2][3] = {};   // [precision][gram, poly, apply]
+  lm::XcdSplit* d_splits = nullptr;   // [precision * 3 + stage]
+
+  ~DevicePlan() {
+    if (uploaded) (void)hipEventDestroy(uploaded);
+    if (dev) (void)hipFree(dev);
+    if (host) (void)hipHostFree(host);
+  }
+};
+
+constexpr size_t kMaxPlans = 16;
+std::mutex g_mu;                                      // plans, workspace, profiling
+std::list<std::shared_ptr<DevicePlan>> g_plans;       // most recent first
+
+struct OwnedWorkspace {
+  int device = -1;
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+std::vector<OwnedWorkspace> g_ws;
+
+// Phase timing
+bool g_prof = false;
+struct PendingEvent {
+  int phase;
+  hipEvent_t start, stop;
+};
+std::vector<PendingEvent> g_pending;
+std::vector<hipEvent_t> g_event_pool;
+lm_phase_times g_times{};
+
+hipError_t get_event(hipEvent_t* e) {
+  if (!g_event_pool.empty()) {
+    *e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreate(e);
+}
+
+void append_key(std::vector<uint8_t>* k, const void* p, size_t n) {
+  const uint8_t* b = static_cast<const uint8_t*>(p);
+  k->insert(k->end(), b, b + n);
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+template <typename T>
+void place(std::vector<T>& v, size_t* off, std::vector<std::pair<size_t, std::pair<const void*, size_t>>>* parts) {
+  parts->push_back({*off, {v.data(), v.size() * sizeof(T)}});
+  *off = align256(*off + v.size() * sizeof(T));
+}
+
+lm_status get_plan(const TensorIn* x, int32_t n, bool muon, lm::NsPrecision prec, bool rms02,
+                   hipStream_t stream, std::shared_ptr<DevicePlan>* out) {
+  int device = 0;
+  hipError_t e = hipGetDevice(&device);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::vector<uint8_t> key;
+  key.reserve(size_t(n) * sizeof(TensorIn) + 16);
+  const int32_t hdr[5] = {device, muon ? 1 : 0, prec.all_fp32 ? 1 : 0, prec.bf16_min_side,
+                          rms02 ? 1 : 0};
+  append_key(&key, hdr, sizeof(hdr));
+  append_key(&key, x, size_t(n) * sizeof(TensorIn));
+  for (auto it = g_plans.begin(); it != g_plans.end(); ++it) {
+    if ((*it)->key == key) {
+      g_plans.splice(g_plans.begin(), g_plans, it);
+      *out = g_plans.front();
+      if ((*out)->upload_stream != stream) {
+        e = hipStreamWaitEvent(stream, (*out)->uploaded, 0);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+      }
+      return LM_OK;
+    }
+  }
+  auto dp = std::make_shared<DevicePlan>();
+  dp->device = device;
+  dp->key = std::move(key);
+  std::string err;
+  Status st = lm::build_plan(x, n, muon, prec, rms02, &dp->plan, &err);
+  if (st != Status::kOk) return fail(to_c(st), err);
+  Plan& p = dp->plan;
+  std::vector<std::pair<size_t, std::pair<const void*, size_t>>> parts;
+  size_t off = 0;
+  const size_t o_lion = off;       place(p.lion, &off, &parts);
+  const size_t o_lion_start = off; place(p.lion_block_start, &off, &parts);
+  const size_t o_mats = off;       place(p.mats, &off, &parts);
+  const size_t o_prep = off;       place(p.prep_start, &off, &parts);
+  size_t o_tasks[2][3];
+  std::vector<lm::XcdSplit> splits;
+  for (int pr = 0; pr < 2; ++pr) {
+    o_tasks[pr][0] = off; place(p.gram[pr], &off, &parts);
+    o_tasks[pr][1] = off; place(p.poly[pr], &off, &parts);
+    o_tasks[pr][2] = off; place(p.apply[pr], &off, &parts);
+    splits.push_back(p.gram_split[pr]);
+    splits.push_back(p.poly_split[pr]);
+    splits.push_back(p.apply_split[pr]);
+  }
+  const size_t o_splits = off;     place(splits, &off, &parts);
+  const size_t total = std::max<size_t>(off, 256);
+  e = hipMalloc(&dp->dev, total);
+  if (e != hipSuccess) return fail(LM_ERR_OUT_OF_MEMORY, "plan tables: hipMalloc failed");
+  e = hipHostMalloc(&dp->host, total, hipHostMallocDefault);
+  if (e != hipSuccess) return fail(LM_ERR_OUT_OF_MEMORY, "plan tables: hipHostMalloc failed");
+  std::memset(dp->host, 0, total);
+  for (const auto& part : parts)
+    if (part.second.second) std::memcpy(static_cast<uint8_t*>(dp->host) + part.first,
+                                        part.second.first, part.second.second);
+  e = hipMemcpyAsync(dp->dev, dp->host, total, hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "plan tables: hipMemcpyAsync");
+  e = hipEventCreateWithFlags(&dp->uploaded, hipEventDisableTiming);
+  if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+  e = hipEventRecord(dp->uploaded, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+  dp->upload_stream = stream;
+  uint8_t* base = static_cast<uint8_t*>(dp->dev);
+  dp->d_lion = reinterpret_cast<lm::LionTensor*>(base + o_lion);
+  dp->d_lion_start = reinterpret_cast<int32_t*>(base + o_lion_start);
+  dp->d_mats = reinterpret_cast<lm::MuonMat*>(base + o_mats);
+  dp->d_prep_start = reinterpret_cast<int32_t*>(base + o_prep);
+  for (int pr = 0; pr < 2; ++pr)
+    for (int st3 = 0; st3 < 3; ++st3)
+      dp->d_tasks[pr][st3] = reinterpret_cast<lm::GemmTask*>(base + o_tasks[pr][st3]);
+  dp->d_splits = reinterpret_cast<lm::XcdSplit*>(base + o_splits);
+  g_plans.push_front(dp);
+  while (g_plans.size() > kMaxPlans) g_plans.pop_back();   // hipFree waits for the device
+  *out = dp;
+  return LM_OK;
+}
+
+lm_status owned_workspace(size_t bytes, void** ptr) {
+  int device = 0;
+  hipError_t e = hipGetDevice(&device);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  for (auto& w : g_ws) {
+    if (w.device != device) continue;
+    if (w.bytes >= bytes) {
+      *ptr = w.ptr;
+      return LM_OK;
+    }
+    (void)hipFree(w.ptr);          // waits for outstanding work on the device
+    w.ptr = nullptr;
+    w.bytes = 0;
+    e = hipMalloc(&w.ptr, bytes);
+    if (e != hipSuccess) return fail(LM_ERR_OUT_OF_MEMORY, "workspace: hipMalloc failed");
+    w.bytes = bytes;
+    *ptr = w.ptr;
+    return LM_OK;
+  }
+  OwnedWorkspace w;
+  w.device = device;
+  e = hipMalloc(&w.ptr, bytes);
+  if (e != hipSuccess) return fail(LM_ERR_OUT_OF_MEMORY, "workspace: hipMalloc failed");
+  w.bytes = bytes;
+  g_ws.push_back(w);
+  *ptr = w.ptr;
+  return LM_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Launch sequence
+// ---------------------------------------------------------------------------
+struct Timer {
+  hipStream_t stream;
+  int phase;
+  hipEvent_t start = nullptr, stop = nullptr;
+  Timer(hipStream_t s, int ph) : stream(s), phase(ph) {
+    if (!g_prof) return;
+    if (get_event(&start) != hipSuccess || get_event(&stop) != hipSuccess ||
+        hipEventRecord(start, stream) != hipSuccess) {
+      start = stop = nullptr;
+    }
+  }
+  void done() {
+    if (!start) return;
+    if (hipEventRecord(stop, stream) == hipSuccess) g_pending.push_back({phase, start, stop});
+    start = nullptr;
+  }
+};
+
+lm::StepConsts step_consts(double beta1, double beta2, double wd, double lr_muon,
+                           double lr_lion, double eps) {
+  lm::StepConsts k;
+  k.beta1 = float(beta1);
+  k.one_minus_beta1 = float(1.0 - beta1);
+  k.beta2 = float(beta2);
+  k.one_minus_beta2 = float(1.0 - beta2);
+  k.lr_lion = float(lr_lion);
+  k.lr_muon = float(lr_muon);
+  k.wd = float(wd);
+  k.eps = float(eps);
+  return k;
+}
+
+lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config& cfg, void* ws,
+                  bool store_o, hipStream_t stream) {
+  const Plan& p = dp.plan;
+  hipError_t e;
+  if (!p.lion.empty()) {
+    lm::LionLaunch l;
+    l.tensors = dp.d_lion;
+    l.block_start = dp.d_lion_start;
+    l.n_tensors = int32_t(p.lion.size());
+    l.n_blocks = p.lion_block_start.back();
+    l.k = k;
+    Timer t(stream, LM_PHASE_LION);
+    e = lm::launch_lion(l, stream);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "lion kernel launch");
+  }
+  if (p.mats.empty()) return LM_OK;
+  uint8_t* wsb = static_cast<uint8_t*>(ws);
+  float* partials = reinterpret_cast<float*>(wsb + p.ws_partials_off);
+  float* rscale = reinterpret_cast<float*>(wsb + p.ws_rscale_off);
+  lm::PrepLaunch pl;
+  pl.mats = dp.d_mats;
+  pl.prep_start = dp.d_prep_start;
+  pl.n_mats = int32_t(p.mats.size());
+  pl.n_tiles = p.prep_start.back();
+  pl.ws = ws;
+  pl.partials = partials;
+  pl.rscale = rscale;
+  pl.k = k;
+  {
+    Timer t(stream, LM_PHASE_PREP);
+    e = lm::launch_prep(pl, stream);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "prep kernel launch");
+  }
+  {
+    Timer t(stream, LM_PHASE_NORM);
+    e = lm::launch_norm(pl, stream);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "norm kernel launch");
+  }
+  lm::GemmLaunch gl;
+  gl.mats = dp.d_mats;
+  gl.ws = ws;
+  gl.rscale = rscale;
+  gl.store_o = store_o ? 1 : 0;
+  gl.a = float(cfg.ns_a);
+  gl.b = float(cfg.ns_b);
+  gl.c = float(cfg.ns_c);
+  gl.lr = k.lr_muon;
+  gl.wd = k.wd;
+  const lm::GemmMode modes[3] = {lm::kGram, lm::kPoly, lm::kApply};
+  const int phases[3] = {LM_PHASE_GRAM, LM_PHASE_POLY, LM_PHASE_APPLY};
+  for (int it = 0; it < cfg.ns_steps; ++it) {
+    gl.src = it & 1;
+    gl.first = it == 0;
+    gl.last = it == cfg.ns_steps - 1;
+    for (int st3 = 0; st3 < 3; ++st3) {
+      Timer t(stream, phases[st3]);
+      for (int pr = 0; pr < 2; ++pr) {   // bf16 matrices, then fp32 matrices
+        const lm::XcdSplit& sp = st3 == 0 ? p.gram_split[pr] : (st3 == 1 ? p.poly_split[pr]
+                                                                          : p.apply_split[pr]);
+        if (sp.max_count == 0) continue;
+        gl.tasks = dp.d_tasks[pr][st3];
+        gl.split = dp.d_splits + pr * 3 + st3;
+        gl.max_count = sp.max_count;
+        gl.fp32 = pr;
+        e = lm::launch_gemm(modes[st3], gl, stream);
+        if (e != hipSuccess) return hip_fail(e, "Newton-Schulz kernel launch");
+      }
+      t.done();
+    }
+  }
+  return LM_OK;
+}
+
+lm_status check_config(const lm_config* cfg) {
+  if (cfg->struct_size != sizeof(lm_config)) return fail(LM_ERR_INVALID_ARGUMENT, "lm_config.struct_size mismatch");
+  if (cfg->ns_steps < 1 || cfg->ns_steps > 64) return fail(LM_ERR_INVALID_ARGUMENT, "ns_steps must lie in [1, 64]");
+  if (!std::isfinite(cfg->ns_a) || !std::isfinite(cfg->ns_b) || !std::isfinite(cfg->ns_c))
+    return fail(LM_ERR_INVALID_ARGUMENT, "Newton-Schulz coefficients must be finite");
+  if (!(cfg->ns_eps >= 0.0f) || !std::isfinite(cfg->ns_eps)) return fail(LM_ERR_INVALID_ARGUMENT, "ns_eps must be finite and >= 0");
+  if (cfg->ns_precision != LM_NS_BF16 && cfg->ns_precision != LM_NS_FP32)
+    return fail(LM_ERR_INVALID_ARGUMENT, "unknown ns_precision");
+  if (cfg->ns_scale_mode != LM_NS_SCALE_NONE && cfg->ns_scale_mode != LM_NS_SCALE_RMS02)
+    return fail(LM_ERR_INVALID_ARGUMENT, "unknown ns_scale_mode");
+  if (cfg->ns_bf16_min_side < 0) return fail(LM_ERR_INVALID_ARGUMENT, "ns_bf16_min_side must be >= 0");
+  if (cfg->reserved != 0) return fail(LM_ERR_INVALID_ARGUMENT, "lm_config.reserved must be 0");
+  return LM_OK;
+}
+
+lm::NsPrecision precision_of(const lm_config& cfg) {
+  lm::NsPrecision p;
+  p.all_fp32 = cfg.ns_precision == LM_NS_FP32;
+  p.bf16_min_side = cfg.ns_bf16_min_side;
+  return p;
+}
+
+std::vector<TensorIn> gather(float* const* params, const float* const* grads, float* const* momentum,
+                             const lm_shape* shapes, int32_t n) {
+  std::vector<TensorIn> v(size_t(n > 0 ? n : 0));
+  for (int32_t i = 0; i < n; ++i) {
+    v[i].w = params[i];
+    v[i].g = grads[i];
+    v[i].m = momentum[i];
+    v[i].rows = shapes[i].rows;
+    v[i].cols = shapes[i].cols;
+    v[i].flags = shapes[i].flags;
+    v[i].reserved = shapes[i].reserved;
+  }
+  return v;
+}
+
+lm_status step_impl(float* const* params, const float* const* grads, float* const* momentum,
+                    const lm_shape* shapes, int32_t n, int64_t t, int32_t P, double beta1,
+                    double beta2, double wd, const lm_config* cfg, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream) {
+  if (cfg == nullptr) return fail(LM_ERR_INVALID_ARGUMENT, "null config");
+  lm_status cs = check_config(cfg);
+  if (cs != LM_OK) return cs;
+  std::string err;
+  Status st = lm::validate_scalars(t, P, beta1, beta2, wd, cfg->lr_muon, cfg->lr_lion, &err);
+  if (st != Status::kOk) return fail(to_c(st), err);
+  if (n < 0) return fail(LM_ERR_INVALID_ARGUMENT, "n_tensors must be >= 0");
+  if (n == 0) return LM_OK;
+  if (!params || !grads || !momentum || !shapes) return fail(LM_ERR_INVALID_ARGUMENT, "null tensor array");
+  if ((workspace == nullptr) != (workspace_bytes == 0))
+    return fail(LM_ERR_INVALID_ARGUMENT, "workspace and workspace_bytes must both be set or both be 0");
+  if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u))
+    return fail(LM_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  std::vector<TensorIn> x = gather(params, grads, momentum, shapes, n);
+  st = lm::validate_tensors(x.data(), n, &err);
+  if (st != Status::kOk) return fail(to_c(st), err);
+  bool any = false;
+  for (const TensorIn& ti : x) any = any || (ti.rows > 0 && ti.cols > 0);
+  if (!any) return LM_OK;                          // only empty tensors: nothing to do
+  const bool muon = lm::is_muon_step(t, P);
+  const bool rms02 = cfg->ns_scale_mode == LM_NS_SCALE_RMS02;
+
+  std::lock_guard<std::mutex> lock(g_mu);
+  std::shared_ptr<DevicePlan> dp;
+  lm_status s = get_plan(x.data(), n, muon, precision_of(*cfg), rms02, stream, &dp);
+  if (s != LM_OK) return s;
+  void* ws = workspace;
+  if (dp->plan.ws_bytes > 0) {
+    if (workspace) {
+      if (workspace_bytes < dp->plan.ws_bytes)
+        return fail(LM_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than lionmuon_workspace_bytes");
+    } else {
+      s = owned_workspace(dp->plan.ws_bytes, &ws);
+      if (s != LM_OK) return s;
+    }
+  }
+  return enqueue(*dp, step_consts(beta1, beta2, wd, cfg->lr_muon, cfg->lr_lion, cfg->ns_eps),
+                 *cfg, ws, false, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+void lionmuon_config_default(lm_config* cfg) {
+  if (!cfg) return;
+  std::memset(cfg, 0, sizeof(*cfg));
+  cfg->struct_size = sizeof(lm_config);
+  cfg->ns_steps = 5;
+  cfg->ns_a = 3.4445;
+  cfg->ns_b = -4.7750;
+  cfg->ns_c = 2.0315;
+  cfg->ns_eps = 1e-7;
+  cfg->ns_precision = LM_NS_BF16;
+  cfg->ns_scale_mode = LM_NS_SCALE_NONE;
+  cfg->lr_muon = 0.0;
+  cfg->lr_lion = 0.0;
+  cfg->ns_bf16_min_side = 64;
+  cfg->reserved = 0;
+}
+
+lm_status lionmuon_step(float* const* params, const float* const* grads, float* const* momentum,
+                        const lm_shape* shapes, int32_t n_tensors, int64_t t, int32_t P,
+                        double beta1, double beta2, double lr, double wd, hipStream_t stream) {
+  lm_config cfg;
+  lionmuon_config_default(&cfg);
+  cfg.lr_muon = lr;
+  cfg.lr_lion = lr;
+  return step_impl(params, grads, momentum, shapes, n_tensors, t, P, beta1, beta2, wd, &cfg,
+                   nullptr, 0, stream);
+}
+
+lm_status lionmuon_step_ex(float* const* params, const float* const* grads, float* const* momentum,
+                           const lm_shape* shapes, int32_t n_tensors, int64_t t, int32_t P,
+                           double beta1, double beta2, double wd, const lm_config* cfg,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return step_impl(params, grads, momentum, shapes, n_tensors, t, P, beta1, beta2, wd, cfg,
+                   workspace, workspace_bytes, stream);
+}
+
+lm_status lionmuon_workspace_bytes(const lm_shape* shapes, int32_t n_tensors, const lm_config* cfg,
+                                   size_t* out_bytes) {
+  lm_plan_info info;
+  lm_status s = lionmuon_plan_info(shapes, n_tensors, 0, 1, cfg, &info);
+  if (s != LM_OK) return s;
+  if (!out_bytes) return fail(LM_ERR_INVALID_ARGUMENT, "null out_bytes");
+  *out_bytes = info.workspace_bytes;
+  return LM_OK;
+}
+
+lm_status lionmuon_plan_info(const lm_shape* shapes, int32_t n, int64_t t, int32_t P,
+                             const lm_config* cfg, lm_plan_info* out) {
+  if (!out) return fail(LM_ERR_INVALID_ARGUMENT, "null output");
+  lm_config def;
+  lionmuon_config_default(&def);
+  if (!cfg) cfg = &def;
+  lm_status cs = check_config(cfg);
+  if (cs != LM_OK) return cs;
+  if (n < 0) return fail(LM_ERR_INVALID_ARGUMENT, "n_tensors must be >= 0");
+  if (n > 0 && !shapes) return fail(LM_ERR_INVALID_ARGUMENT, "null shapes");
+  if (t < 0 || P < 0) return fail(LM_ERR_INVALID_ARGUMENT, "t and P must be >= 0");
+  // Synthetic, distinct, 16-byte aligned addresses: only shapes matter here.
+  std::vector<TensorIn> x(static_cast<size_t>(n));
+  uintptr_t addr = 4096;
+  for (int32_t i = 0; i < n; ++i) {
+    x[i].rows = shapes[i].rows;
+    x[i].cols = shapes[i].cols;
+    x[i].flags = shapes[i].flags;
+    x[i].reserved = shapes[i].reserved;
+    if (x[i].rows < 0 || x[i].cols < 0) continue;    // rejected by validate_tensors
+    const uintptr_t bytes = (uintptr_t(x[i].rows) * uintptr_t(x[i].cols) * 4u + 15u) & ~uintptr_t(15);
+    x[i].w = reinterpret_cast<float*>(addr); addr += bytes + 16;
+    x[i].g = reinterpret_cast<const float*>(addr); addr += bytes + 16;
+    x[i].m = reinterpret_cast<float*>(addr); addr += bytes + 16;
+  }
+  std::string err;
+  Status st = lm::validate_tensors(x.data(), n, &err);
+  if (st != Status::kOk) return fail(to_c(st), err);
+  Plan p;
+  st = lm::build_plan(x.data(), n, lm::is_muon_step(t, P), precision_of(*cfg),
+                      cfg->ns_scale_mode == LM_NS_SCALE_RMS02, &p, &err);
+  if (st != Status::kOk) return fail(to_c(st), err);
+  std::memset(out, 0, sizeof(*out));
+  out->n_tensors = p.n_tensors;
+  out->n_lion = int32_t(p.lion.size());
+  out->n_muon = int32_t(p.mats.size());
+  out->n_shape_classes = p.n_shape_classes;
+  out->lion_elements = p.lion_elements;
+  out->muon_elements = p.muon_elements;
+  out->gram_tiles = int64_t(p.gram[0].size() + p.gram[1].size());
+  out->poly_tiles = int64_t(p.poly[0].size() + p.poly[1].size());
+  out->apply_tiles = int64_t(p.apply[0].size() + p.apply[1].size());
+  out->ns_flops = lm::ns_flops_symmetric(p, cfg->ns_steps);
+  out->ns_flops_dense = lm::ns_flops_dense(p, cfg->ns_steps);
+  out->lion_bytes = 20.0 * double(p.lion_elements);
+  out->workspace_bytes = p.ws_bytes;
+  return LM_OK;
+}
+
+lm_status lionmuon_ns(const float* X, float* O, int64_t rows, int64_t cols, int32_t batch,
+                      const lm_config* cfg, void* workspace, size_t workspace_bytes,
+                      hipStream_t stream) {
+  lm_config def;
+  lionmuon_config_default(&def);
+  if (!cfg) cfg = &def;
+  lm_status cs = check_config(cfg);
+  if (cs != LM_OK) return cs;
+  if (batch < 0 || rows < 0 || cols < 0) return fail(LM_ERR_INVALID_ARGUMENT, "negative size");
+  if (batch == 0 || rows == 0 || cols == 0) return LM_OK;
+  if (!X || !O) return fail(LM_ERR_INVALID_ARGUMENT, "null X or O");
+  if (rows < 2 || cols < 2) return fail(LM_ERR_UNSUPPORTED, "Newton-Schulz hook needs rows, cols >= 2");
+  if ((workspace == nullptr) != (workspace_bytes == 0))
+    return fail(LM_ERR_INVALID_ARGUMENT, "workspace and workspace_bytes must both be set or both be 0");
+  if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u))
+    return fail(LM_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  const int64_t numel = rows * cols;
+  const uintptr_t xb = reinterpret_cast<uintptr_t>(X), ob = reinterpret_cast<uintptr_t>(O);
+  const uintptr_t bytes = uintptr_t(numel) * uintptr_t(batch) * 4u;
+  if (xb < ob + bytes && ob < xb + bytes) return fail(LM_ERR_INVALID_ARGUMENT, "X and O overlap");
+  if ((xb | ob) & 3u) return fail(LM_ERR_INVALID_ARGUMENT, "X and O must be 4-byte aligned");
+  // Each matrix is a Muon tensor with G = X, no momentum (beta1 = 0) and an
+  // output epilogue that stores kappa * NS_K(X) into O.
+  std::vector<TensorIn> x(static_cast<size_t>(batch));
+  for (int32_t b = 0; b < batch; ++b) {
+    x[b].w = O + b * numel;
+    x[b].g = X + b * numel;
+    x[b].m = nullptr;
+    x[b].rows = rows;
+    x[b].cols = cols;
+    x[b].flags = 0;
+    x[b].reserved = 0;
+  }
+  const bool rms02 = cfg->ns_scale_mode == LM_NS_SCALE_RMS02;
+  std::lock_guard<std::mutex> lock(g_mu);
+  std::shared_ptr<DevicePlan> dp;
+  lm_status s = get_plan(x.data(), batch, true, precision_of(*cfg), rms02, stream, &dp);
+  if (s != LM_OK) return s;
+  void* ws = workspace;
+  if (workspace) {
+    if (workspace_bytes < dp->plan.ws_bytes)
+      return fail(LM_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than lionmuon_workspace_bytes");
+  } else {
+    s = owned_workspace(dp->plan.ws_bytes, &ws);
+    if (s != LM_OK) return s;
+  }
+  return enqueue(*dp, step_consts(0.0, 0.0, 0.0, 0.0, 0.0, cfg->ns_eps), *cfg, ws, true, stream);
+}
+
+lm_status lionmuon_profiling_enable(int32_t enable) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  g_prof = enable != 0;
+  return LM_OK;
+}
+
+lm_status lionmuon_profiling_read(lm_phase_times* out) {
+  if (!out) return fail(LM_ERR_INVALID_ARGUMENT, "null output");
+  std::lock_guard<std::mutex> lock(g_mu);
+  for (const PendingEvent& pe : g_pending) {
+    hipError_t e = hipEventSynchronize(pe.stop);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    float ms = 0.0f;
+    e = hipEventElapsedTime(&ms, pe.start, pe.stop);
+    if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+    g_times.ms[pe.phase] += ms;
+    g_times.launches[pe.phase] += 1;
+    g_event_pool.push_back(pe.start);
+    g_event_pool.push_back(pe.stop);
+  }
+  g_pending.clear();
+  *out = g_times;
+  return LM_OK;
+}
+
+lm_status lionmuon_profiling_reset(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  for (const PendingEvent& pe : g_pending) {
+    (void)hipEventSynchronize(pe.stop);
+    g_event_pool.push_back(pe.start);
+    g_event_pool.push_back(pe.stop);
+  }
+  g_pending.clear();
+  std::memset(&g_times, 0, sizeof(g_times));
+  return LM_OK;
+}
+
+void lionmuon_release(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  g_plans.clear();
+  for (auto& w : g_ws)
+    if (w.ptr) (void)hipFree(w.ptr);
+  g_ws.clear();
+  for (const PendingEvent& pe : g_pending) {
+    (void)hipEventSynchronize(pe.stop);
+    g_event_pool.push_back(pe.start);
+    g_event_pool.push_back(pe.stop);
+  }
+  g_pending.clear();
+  for (hipEvent_t e : g_event_pool) (void)hipEventDestroy(e);
+  g_event_pool.clear();
+}
+
+const char* lionmuon_status_string(lm_status s) {
+  switch (s) {
+    case LM_OK: return "LM_OK";
+    case LM_ERR_INVALID_ARGUMENT: return "LM_ERR_INVALID_ARGUMENT";
+    case LM_ERR_UNSUPPORTED: return "LM_ERR_UNSUPPORTED";
+    case LM_ERR_OUT_OF_MEMORY: return "LM_ERR_OUT_OF_MEMORY";
+    case LM_ERR_WORKSPACE_TOO_SMALL: return "LM_ERR_WORKSPACE_TOO_SMALL";
+    case LM_ERR_HIP: return "LM_ERR_HIP";
+  }
+  return "unknown lm_status";
+}
+
+const char* lionmuon_last_error(void) { return g_last_error.c_str(); }
+
+int32_t lionmuon_abi_version(void) { return LIONMUON_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,61 @@
+// Launchers of the gfx950 kernels of the LionMuon step. Each returns the
+// hipError_t of its launch; all work is enqueued on `stream`.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include "lm_desc.h"
+
+namespace lm {
+
+// fp32 constants of one step, each rounded once from the double
+// hyper-parameters (one_minus_beta* formed in double).
+struct StepConsts {
+  float beta1, one_minus_beta1, beta2, one_minus_beta2;
+  float lr_lion, lr_muon, wd, eps;
+};
+
+struct LionLaunch {
+  const LionTensor* tensors;     // device
+  const int32_t* block_start;    // device, n_tensors + 1
+  int32_t n_tensors;
+  int32_t n_blocks;
+  StepConsts k;
+};
+hipError_t launch_lion(const LionLaunch& a, hipStream_t stream);
+
+struct PrepLaunch {
+  const MuonMat* mats;           // device
+  const int32_t* prep_start;     // device, n_mats + 1
+  int32_t n_mats;
+  int32_t n_tiles;
+  void* ws;                      // workspace base
+  float* partials;               // one float per preparation tile
+  float* rscale;                 // one float per matrix
+  StepConsts k;
+};
+// Interpolation, momentum update, X0 / X0^T store and Frobenius partials,
+// then the per-matrix 1/(||Ghat||_F + eps).
+hipError_t launch_prep(const PrepLaunch& a, hipStream_t stream);
+hipError_t launch_norm(const PrepLaunch& a, hipStream_t stream);
+
+enum GemmMode { kGram = 0, kPoly = 1, kApply = 2 };
+
+struct GemmLaunch {
+  const MuonMat* mats;           // device
+  const GemmTask* tasks;         // device, grouped by XCD segment
+  const XcdSplit* split;         // device: one segment of `tasks` per XCD
+  int32_t max_count;             // largest segment (host copy): grid = 8 x max_count
+  void* ws;
+  const float* rscale;
+  int32_t src;                   // ping-pong index of the current X, X^T
+  int32_t first;                 // first NS step: apply 1/(||Ghat||_F + eps)
+  int32_t last;                  // last NS step: write W (or O)
+  int32_t store_o;               // last step stores kappa*X_K instead of a W update
+  float a, b, c;                 // odd polynomial coefficients
+  float lr, wd;                  // eta_M and lambda of the W update
+  int32_t fp32;                  // element type of the matrices in `tasks`
+};
+hipError_t launch_gemm(GemmMode mode, const GemmLaunch& a, hipStream_t stream);
+
+}  // namespace lm

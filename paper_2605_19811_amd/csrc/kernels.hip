@@ -1,0 +1,533 @@
+// gfx950 kernels of the LionMuon step (Algorithm 1 of arXiv 2605.19811).
+//
+//  lion_kernel   Lion branch: Ghat = b1*M + (1-b1)*G; W -= lr*(sign(Ghat) + wd*W);
+//                M = b2*M + (1-b2)*G. Multi-tensor, 16-byte vectors, HBM bound.
+//  prep_kernel   Muon branch, first pass: the same interpolation and momentum
+//                update, Ghat stored in the NS element type in both the
+//                iteration orientation X (rows <= cols) and its transpose, and
+//                a per-tile partial sum of Ghat^2 (wave shuffles + LDS).
+//  norm_kernel   fixed-order reduction of the partials -> 1/(||Ghat||_F + eps).
+//  gemm_kernel   the Newton-Schulz products on MFMA with fp32 accumulation:
+//                Gram A = X X^T and polynomial B = b A + c A A on the lower
+//                triangle of tiles (mirrored on store), apply X' = a X + B X
+//                with the W update fused into the last step's epilogue.
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+namespace lm {
+
+namespace {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// sign with sign(+-0) = 0 and NaN propagated.
+__device__ __forceinline__ float sign_f(float x) {
+  return x > 0.0f ? 1.0f : (x < 0.0f ? -1.0f : x);
+}
+
+// Largest i in [0, n) with start[i] <= b (start is non-decreasing, start[0] = 0).
+__device__ __forceinline__ int find_segment(const int32_t* start, int n, int b) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (start[mid] <= b) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// Lion branch
+// ---------------------------------------------------------------------------
+struct LionArgs {
+  const LionTensor* tensors;
+  const int32_t* block_start;
+  int32_t n_tensors;
+  float b1, omb1, b2, omb2, lr, wd;
+};
+
+__device__ __forceinline__ void lion_elem(float& w, float g, float& m, const LionArgs& a) {
+  const float c = fmaf(a.b1, m, a.omb1 * g);
+  w = fmaf(-a.lr, fmaf(a.wd, w, sign_f(c)), w);
+  m = fmaf(a.b2, m, a.omb2 * g);
+}
+
+constexpr int kLionUnroll = kLionBlockElems / (256 * 4);
+
+__global__ __launch_bounds__(256) void lion_kernel(LionArgs a) {
+  const int b = blockIdx.x;
+  const int ti = find_segment(a.block_start, a.n_tensors, b);
+  const LionTensor t = a.tensors[ti];
+  const int64_t base = int64_t(b - a.block_start[ti]) * kLionBlockElems;
+  const int tid = threadIdx.x;
+  if (t.vec_ok && base + kLionBlockElems <= t.numel) {
+    f32x4* w4 = reinterpret_cast<f32x4*>(t.w + base);
+    const f32x4* g4 = reinterpret_cast<const f32x4*>(t.g + base);
+    f32x4* m4 = reinterpret_cast<f32x4*>(t.m + base);
+    f32x4 w[kLionUnroll], g[kLionUnroll], m[kLionUnroll];
+#pragma unroll
+    for (int u = 0; u < kLionUnroll; ++u) {
+      const int i = tid + 256 * u;
+      w[u] = w4[i];
+      g[u] = __builtin_nontemporal_load(&g4[i]);
+      m[u] = m4[i];
+    }
+#pragma unroll
+    for (int u = 0; u < kLionUnroll; ++u) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float we = w[u][e], me = m[u][e];
+        lion_elem(we, g[u][e], me, a);
+        w[u][e] = we;
+        m[u][e] = me;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kLionUnroll; ++u) {
+      const int i = tid + 256 * u;
+      __builtin_nontemporal_store(w[u], &w4[i]);
+      __builtin_nontemporal_store(m[u], &m4[i]);
+    }
+  } else {
+    const int64_t end = min(base + int64_t(kLionBlockElems), t.numel);
+    for (int64_t i = base + tid; i < end; i += 256) {
+      float w = t.w[i], m = t.m[i];
+      lion_elem(w, t.g[i], m, a);
+      t.w[i] = w;
+      t.m[i] = m;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Muon branch: preparation and norm
+// ---------------------------------------------------------------------------
+struct PrepArgs {
+  const MuonMat* mats;
+  const int32_t* prep_start;
+  int32_t n_mats;
+  void* ws;
+  float* partials;
+  float* rscale;
+  float b1, omb1, b2, omb2, eps;
+};
+
+template <typename T> __device__ __forceinline__ T to_elem(float v);
+template <> __device__ __forceinline__ float to_elem<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 to_elem<bf16>(float v) { return bf16(v); }
+
+// Store four consecutive elements (8 bytes for bf16, 16 for fp32; aligned).
+__device__ __forceinline__ void store4(bf16* p, const float v[4]) {
+  bf16x4 x = {bf16(v[0]), bf16(v[1]), bf16(v[2]), bf16(v[3])};
+  *reinterpret_cast<bf16x4*>(p) = x;
+}
+__device__ __forceinline__ void store4(float* p, const float v[4]) {
+  const f32x4 x = {v[0], v[1], v[2], v[3]};
+  *reinterpret_cast<f32x4*>(p) = x;
+}
+__device__ __forceinline__ void load4(const bf16* p, float v[4]) {
+  const bf16x4 x = *reinterpret_cast<const bf16x4*>(p);
+  v[0] = float(x[0]); v[1] = float(x[1]); v[2] = float(x[2]); v[3] = float(x[3]);
+}
+__device__ __forceinline__ void load4(const float* p, float v[4]) {
+  const f32x4 x = *reinterpret_cast<const f32x4*>(p);
+  v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3];
+}
+
+template <typename T>
+__device__ __forceinline__ void prep_tile(const PrepArgs& a, const MuonMat& mm, int b) {
+  constexpr int kPad = 4 / sizeof(T) + 1;        // odd word stride per LDS row
+  __shared__ T tile[kPrepTile][kPrepTile + kPad];
+  __shared__ float red[4];
+  const int local = b - mm.prep_first;
+  const int ti = local / mm.prep_tiles_n, tj = local - ti * mm.prep_tiles_n;
+  const int64_t rows_pad = mm.transposed ? mm.l_pad : mm.s_pad;
+  const int64_t cols_pad = mm.transposed ? mm.s_pad : mm.l_pad;
+  char* ws = static_cast<char*>(a.ws);
+  T* S = reinterpret_cast<T*>(ws + (mm.transposed ? mm.off_xt[0] : mm.off_x[0]));   // rows_pad x cols_pad
+  T* Tt = reinterpret_cast<T*>(ws + (mm.transposed ? mm.off_x[0] : mm.off_xt[0]));  // cols_pad x rows_pad
+  const int tid = threadIdx.x, r0 = tid >> 4, c4 = (tid & 15) * 4;
+  float ss = 0.0f;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int r = r0 + 16 * u;
+    const int64_t p = int64_t(ti) * kPrepTile + r;
+    const int64_t q = int64_t(tj) * kPrepTile + c4;
+    float gv[4] = {0.f, 0.f, 0.f, 0.f}, mv[4] = {0.f, 0.f, 0.f, 0.f};
+    const bool row_in = p < mm.rows;
+    const bool vec = row_in && mm.vec_ok && q + 3 < mm.cols;
+    const int64_t idx = p * mm.cols + q;
+    if (vec) {
+      const f32x4 g = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(mm.g + idx));
+      gv[0] = g[0]; gv[1] = g[1]; gv[2] = g[2]; gv[3] = g[3];
+      if (mm.m) {
+        const f32x4 m = *reinterpret_cast<const f32x4*>(mm.m + idx);
+        mv[0] = m[0]; mv[1] = m[1]; mv[2] = m[2]; mv[3] = m[3];
+      }
+    } else if (row_in) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (q + e < mm.cols) {
+          gv[e] = mm.g[idx + e];
+          if (mm.m) mv[e] = mm.m[idx + e];
+        }
+      }
+    }
+    float c[4], mn[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      c[e] = fmaf(a.b1, mv[e], a.omb1 * gv[e]);
+      mn[e] = fmaf(a.b2, mv[e], a.omb2 * gv[e]);
+      ss = fmaf(c[e], c[e], ss);
+    }
+    if (mm.m) {
+      if (vec) {
+        const f32x4 mv4 = {mn[0], mn[1], mn[2], mn[3]};
+        *reinterpret_cast<f32x4*>(mm.m + idx) = mv4;
+      } else if (row_in) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (q + e < mm.cols) mm.m[idx + e] = mn[e];
+      }
+    }
+    store4(S + p * cols_pad + q, c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) tile[r][c4 + e] = to_elem<T>(c[e]);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int qq = r0 + 16 * u;          // column of the source tile
+    float v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = float(tile[c4 + e][qq]);
+    store4(Tt + (int64_t(tj) * kPrepTile + qq) * rows_pad + int64_t(ti) * kPrepTile + c4, v);
+  }
+  ss = wave_sum(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  if (tid == 0) a.partials[mm.prep_first + local] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+__global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
+  const int b = blockIdx.x;
+  const MuonMat& mm = a.mats[find_segment(a.prep_start, a.n_mats, b)];
+  if (mm.fp32)
+    prep_tile<float>(a, mm, b);
+  else
+    prep_tile<bf16>(a, mm, b);
+}
+
+__global__ __launch_bounds__(256) void norm_kernel(PrepArgs a) {
+  __shared__ float red[4];
+  const MuonMat mm = a.mats[blockIdx.x];
+  const float* p = a.partials + mm.prep_first;
+  float s = 0.0f;
+  for (int i = threadIdx.x; i < mm.prep_count; i += 256) s += p[i];
+  s = wave_sum(s);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const float total = (red[0] + red[1]) + (red[2] + red[3]);
+    a.rscale[blockIdx.x] = 1.0f / (sqrtf(total) + a.eps);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Newton-Schulz GEMMs
+// ---------------------------------------------------------------------------
+// C[128 x 128] = sum_k Aop[row0 + i][k] * Bop[col0 + j][k]: both operands are
+// K-contiguous ("NT"), staged through LDS 128 bytes of K per row per stage,
+// double buffered via registers. 4 waves, each a 64 x 64 sub-tile of 2 x 2
+// MFMA 32x32 blocks. Accumulator element r of block (mi, ni) sits at
+// row wm + 32 mi + 8 (r / 4) + 4 (lane / 32) + r % 4, col wn + 32 ni + lane % 32.
+template <typename T> struct Mfma;
+
+template <> struct Mfma<bf16> {
+  static constexpr int kBK = 64;      // K per stage (128 bytes)
+  static constexpr int kKStep = 16;   // K per MFMA
+  typedef bf16x8 Frag;
+  __device__ static __forceinline__ Frag load(const bf16* row, int lk) {
+    return *reinterpret_cast<const bf16x8*>(row + lk * 8);
+  }
+  __device__ static __forceinline__ f32x16 mma(Frag a, Frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <> struct Mfma<float> {
+  static constexpr int kBK = 32;
+  static constexpr int kKStep = 2;
+  typedef float Frag;
+  __device__ static __forceinline__ Frag load(const float* row, int lk) { return row[lk]; }
+  __device__ static __forceinline__ f32x16 mma(Frag a, Frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+};
+
+struct GemmArgs {
+  const MuonMat* mats;
+  const GemmTask* tasks;
+  const XcdSplit* split;
+  void* ws;
+  const float* rscale;
+  int32_t src, first, last, store_o;
+  float a, b, c, lr, wd;
+};
+
+template <typename T, int MODE>
+__global__ __launch_bounds__(256, 2) void gemm_kernel(GemmArgs g) {
+  using M = Mfma<T>;
+  constexpr int kBK = M::kBK;
+  constexpr int kEpc = 16 / sizeof(T);           // elements per 16-byte chunk
+  constexpr int kLd = kBK + kEpc;                // LDS row stride: 144 bytes
+  __shared__ __attribute__((aligned(16))) T sA[2][kTile][kLd];
+  __shared__ __attribute__((aligned(16))) T sB[2][kTile][kLd];
+
+  const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
+  if (slot >= g.split->count[xcd]) return;
+  const GemmTask task = g.tasks[g.split->start[xcd] + slot];
+  const MuonMat& mm = g.mats[task.mat];
+  char* wsb = static_cast<char*>(g.ws);
+  auto at = [&](int64_t off) { return reinterpret_cast<T*>(wsb + off); };
+  // ping-pong buffers chosen without indexing (keeps descriptors out of scratch)
+  const int64_t off_x_cur = g.src ? mm.off_x[1] : mm.off_x[0];
+  const int64_t off_x_nxt = g.src ? mm.off_x[0] : mm.off_x[1];
+  const int64_t off_xt_cur = g.src ? mm.off_xt[1] : mm.off_xt[0];
+  const int64_t off_xt_nxt = g.src ? mm.off_xt[0] : mm.off_xt[1];
+  const T* Aop;
+  const T* Bop;
+  int64_t lda, ldb;
+  int K;
+  if (MODE == kGram) {
+    Aop = Bop = at(off_x_cur);
+    lda = ldb = mm.l_pad;
+    K = mm.l_pad;
+  } else if (MODE == kPoly) {
+    Aop = Bop = at(mm.off_a);
+    lda = ldb = mm.s_pad;
+    K = mm.s_pad;
+  } else {
+    Aop = at(mm.off_b);
+    Bop = at(off_xt_cur);
+    lda = ldb = mm.s_pad;
+    K = mm.s_pad;
+  }
+  const int row0 = task.tm * kTile, col0 = task.tn * kTile;
+  Aop += row0 * lda;
+  Bop += col0 * ldb;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 31, lk = lane >> 5;
+  const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;
+  const int ld_row = tid >> 3, ld_ch = (tid & 7) * kEpc;
+
+  u32x4 ra[4], rb[4];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int row = ld_row + 32 * q;
+      ra[q] = *reinterpret_cast<const u32x4*>(Aop + row * lda + k0 + ld_ch);
+      rb[q] = *reinterpret_cast<const u32x4*>(Bop + row * ldb + k0 + ld_ch);
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int row = ld_row + 32 * q;
+      *reinterpret_cast<u32x4*>(&sA[buf][row][ld_ch]) = ra[q];
+      *reinterpret_cast<u32x4*>(&sB[buf][row][ld_ch]) = rb[q];
+    }
+  };
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  const int nk = K / kBK;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) gload((kt + 1) * kBK);
+#pragma unroll
+    for (int kk = 0; kk < kBK / M::kKStep; ++kk) {
+      const int kc = kk * M::kKStep;
+      const typename M::Frag a0 = M::load(&sA[buf][wm + lr][kc], lk);
+      const typename M::Frag a1 = M::load(&sA[buf][wm + 32 + lr][kc], lk);
+      const typename M::Frag b0 = M::load(&sB[buf][wn + lr][kc], lk);
+      const typename M::Frag b1 = M::load(&sB[buf][wn + 32 + lr][kc], lk);
+      acc[0][0] = M::mma(a0, b0, acc[0][0]);
+      acc[0][1] = M::mma(a0, b1, acc[0][1]);
+      acc[1][0] = M::mma(a1, b0, acc[1][0]);
+      acc[1][1] = M::mma(a1, b1, acc[1][1]);
+    }
+    if (kt + 1 < nk) sstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  // ---- epilogues -----------------------------------------------------------
+  const int64_t s_pad = mm.s_pad, l_pad = mm.l_pad;
+  if (MODE == kGram || MODE == kPoly) {
+    float alpha = 1.0f;
+    if (MODE == kGram && g.first) {
+      const float r = g.rscale[task.mat];
+      alpha = r * r;
+    }
+    T* out = at(MODE == kGram ? mm.off_a : mm.off_b);
+    const T* aold = at(mm.off_a);
+    const bool mirror = task.tm != task.tn;
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int64_t R = row0 + wm + 32 * mi + 8 * q + 4 * lk;   // 4 rows R..R+3
+          const int64_t C = col0 + wn + 32 * ni + lr;
+          float v[4];
+          if (MODE == kGram) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = alpha * acc[mi][ni][4 * q + e];
+          } else {
+            float old[4];
+            load4(aold + C * s_pad + R, old);        // A is symmetric
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = fmaf(g.b, old[e], g.c * acc[mi][ni][4 * q + e]);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) out[(R + e) * s_pad + C] = to_elem<T>(v[e]);
+          if (mirror) store4(out + C * s_pad + R, v);
+        }
+  } else {
+    const float alpha = g.first ? g.rscale[task.mat] : 1.0f;
+    const T* xt_cur = at(off_xt_cur);
+    T* x_dst = at(off_x_nxt);
+    T* xt_dst = at(off_xt_nxt);
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int64_t R = row0 + wm + 32 * mi + 8 * q + 4 * lk;   // short side
+          const int64_t C = col0 + wn + 32 * ni + lr;               // long side
+          float x[4], v[4];
+          load4(xt_cur + C * s_pad + R, x);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = alpha * fmaf(g.a, x[e], acc[mi][ni][4 * q + e]);
+          if (!g.last) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x_dst[(R + e) * l_pad + C] = to_elem<T>(v[e]);
+            store4(xt_dst + C * s_pad + R, v);
+          } else if (C < mm.l) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              if (R + e >= mm.s) break;
+              const int64_t widx = mm.transposed ? C * mm.cols + (R + e) : (R + e) * mm.cols + C;
+              const float o = mm.kappa * v[e];
+              if (g.store_o) {
+                mm.w[widx] = o;
+              } else {
+                const float w = mm.w[widx];
+                mm.w[widx] = fmaf(-g.lr, fmaf(g.wd, w, o), w);
+              }
+            }
+          }
+        }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_lion(const LionLaunch& l, hipStream_t stream) {
+  if (l.n_blocks == 0) return hipSuccess;
+  LionArgs a;
+  a.tensors = l.tensors;
+  a.block_start = l.block_start;
+  a.n_tensors = l.n_tensors;
+  a.b1 = l.k.beta1;
+  a.omb1 = l.k.one_minus_beta1;
+  a.b2 = l.k.beta2;
+  a.omb2 = l.k.one_minus_beta2;
+  a.lr = l.k.lr_lion;
+  a.wd = l.k.wd;
+  hipLaunchKernelGGL(lion_kernel, dim3(l.n_blocks), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+static PrepArgs prep_args(const PrepLaunch& l) {
+  PrepArgs a;
+  a.mats = l.mats;
+  a.prep_start = l.prep_start;
+  a.n_mats = l.n_mats;
+  a.ws = l.ws;
+  a.partials = l.partials;
+  a.rscale = l.rscale;
+  a.b1 = l.k.beta1;
+  a.omb1 = l.k.one_minus_beta1;
+  a.b2 = l.k.beta2;
+  a.omb2 = l.k.one_minus_beta2;
+  a.eps = l.k.eps;
+  return a;
+}
+
+hipError_t launch_prep(const PrepLaunch& l, hipStream_t stream) {
+  if (l.n_tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL(prep_kernel, dim3(l.n_tiles), dim3(256), 0, stream, prep_args(l));
+  return hipGetLastError();
+}
+
+hipError_t launch_norm(const PrepLaunch& l, hipStream_t stream) {
+  if (l.n_mats == 0) return hipSuccess;
+  hipLaunchKernelGGL(norm_kernel, dim3(l.n_mats), dim3(256), 0, stream, prep_args(l));
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
+  if (l.max_count == 0) return hipSuccess;
+  GemmArgs a;
+  a.mats = l.mats;
+  a.tasks = l.tasks;
+  a.split = l.split;
+  a.ws = l.ws;
+  a.rscale = l.rscale;
+  a.src = l.src;
+  a.first = l.first;
+  a.last = l.last;
+  a.store_o = l.store_o;
+  a.a = l.a;
+  a.b = l.b;
+  a.c = l.c;
+  a.lr = l.lr;
+  a.wd = l.wd;
+  const dim3 grid(unsigned(l.max_count) * kXcds), block(256);
+  if (l.fp32) {
+    if (mode == kGram) hipLaunchKernelGGL((gemm_kernel<float, kGram>), grid, block, 0, stream, a);
+    else if (mode == kPoly) hipLaunchKernelGGL((gemm_kernel<float, kPoly>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((gemm_kernel<float, kApply>), grid, block, 0, stream, a);
+  } else {
+    if (mode == kGram) hipLaunchKernelGGL((gemm_kernel<bf16, kGram>), grid, block, 0, stream, a);
+    else if (mode == kPoly) hipLaunchKernelGGL((gemm_kernel<bf16, kPoly>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((gemm_kernel<bf16, kApply>), grid, block, 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace lm

@@ -1,0 +1,64 @@
+// Plain-old-data descriptors shared by the host planner and the gfx950
+// kernels of the LionMuon step. Only integer and pointer fields: the planner
+// fills them on the host, uploads them once per tensor-list signature, and the
+// kernels read them from device memory.
+#pragma once
+
+#include <stdint.h>
+
+namespace lm {
+
+// Tile sizes of the Newton-Schulz GEMMs and of the Muon preparation pass.
+constexpr int kTile = 128;       // MFMA output tile (both dims); buffers padded to it
+constexpr int kPrepTile = 64;    // square tile of the preparation / transpose pass
+constexpr int kLionBlockElems = 4096;  // elements per Lion workgroup (256 x float4 x 4)
+constexpr int kXcds = 8;         // accelerator complex dies of one MI355X
+
+// One tensor on the Lion branch.
+struct LionTensor {
+  float* w;
+  const float* g;
+  float* m;
+  int64_t numel;
+  int32_t vec_ok;   // w, g, m are all 16-byte aligned
+  int32_t pad_;
+};
+
+// One matrix on the Muon branch. Workspace offsets are in BYTES from the
+// workspace base; the Newton-Schulz buffers of the matrix hold bf16 or fp32
+// elements (`fp32`).
+struct MuonMat {
+  float* w;          // W (m x n, row-major); the output O for the NS hook
+  const float* g;    // G
+  float* m;          // M, or null (NS hook: no momentum)
+  int64_t rows, cols;      // m, n of the original tensor
+  int32_t s, l;            // short and long side
+  int32_t s_pad, l_pad;    // padded to kTile
+  int32_t transposed;      // rows > cols: iterate on G^T
+  int32_t vec_ok;          // 16-byte vector access legal on w, g, m rows
+  int32_t fp32;            // 1: fp32 Newton-Schulz buffers, 0: bf16
+  int32_t pad_;
+  int64_t off_x[2];        // X  (s_pad x l_pad), ping-pong
+  int64_t off_xt[2];       // X^T (l_pad x s_pad), ping-pong
+  int64_t off_a;           // A = X X^T (s_pad x s_pad)
+  int64_t off_b;           // B = b A + c A A (s_pad x s_pad)
+  int32_t prep_first;      // first preparation tile of this matrix
+  int32_t prep_tiles_n;    // preparation tiles along the original columns
+  int32_t prep_count;      // preparation tiles of this matrix
+  float kappa;             // output scale
+};
+
+// One output tile of one Newton-Schulz GEMM.
+struct GemmTask {
+  int32_t mat;
+  int16_t tm, tn;          // tile row / column (units of kTile)
+};
+
+// Per-launch partition of a task list into one contiguous segment per XCD.
+struct XcdSplit {
+  int32_t start[kXcds];
+  int32_t count[kXcds];
+  int32_t max_count;
+};
+
+}  // namespace lm

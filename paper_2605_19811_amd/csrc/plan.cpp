@@ -1,0 +1,262 @@
+// Host planner of the LionMuon step (see plan.h). No HIP calls.
+#include "plan.h"
+
+#include <algorithm>
+#include <cmath>
+#include <map>
+#include <numeric>
+#include <utility>
+
+namespace lm {
+
+namespace {
+
+int64_t round_up(int64_t x, int64_t q) { return (x + q - 1) / q * q; }
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+bool finite_nonneg(double v) { return std::isfinite(v) && v >= 0.0; }
+
+}  // namespace
+
+bool is_muon_step(int64_t t, int32_t P) { return P >= 1 && t % P == 0; }
+
+bool is_matrix(const TensorIn& x) {
+  return x.rows > 1 && x.cols > 1 && !(x.flags & 1u);
+}
+
+Status validate_scalars(int64_t t, int32_t P, double beta1, double beta2, double wd,
+                        double lr_muon, double lr_lion, std::string* err) {
+  if (t < 0) { *err = "t must be >= 0"; return Status::kInvalid; }
+  if (P < 0) { *err = "P must be >= 0 (0 encodes P = infinity)"; return Status::kInvalid; }
+  if (!(beta1 >= 0.0 && beta1 < 1.0)) { *err = "beta1 must lie in [0, 1)"; return Status::kInvalid; }
+  if (!(beta2 >= 0.0 && beta2 < 1.0)) { *err = "beta2 must lie in [0, 1)"; return Status::kInvalid; }
+  if (!finite_nonneg(wd)) { *err = "wd must be finite and >= 0"; return Status::kInvalid; }
+  if (!finite_nonneg(lr_muon) || !finite_nonneg(lr_lion)) {
+    *err = "learning rates must be finite and >= 0";
+    return Status::kInvalid;
+  }
+  return Status::kOk;
+}
+
+Status validate_tensors(const TensorIn* x, int32_t n, std::string* err) {
+  if (n < 0) { *err = "n_tensors must be >= 0"; return Status::kInvalid; }
+  if (n > 0 && x == nullptr) { *err = "null tensor list"; return Status::kInvalid; }
+  // [begin, end) byte ranges: writable (W, M) and read-only (G).
+  std::vector<std::pair<uintptr_t, uintptr_t>> wr, rd;
+  wr.reserve(2 * size_t(n));
+  rd.reserve(size_t(n));
+  for (int32_t i = 0; i < n; ++i) {
+    const TensorIn& t = x[i];
+    if (t.rows < 0 || t.cols < 0) {
+      *err = "tensor " + std::to_string(i) + ": negative dimension";
+      return Status::kInvalid;
+    }
+    if (t.reserved != 0 || (t.flags & ~1u)) {
+      *err = "tensor " + std::to_string(i) + ": unknown flag bits or reserved field set";
+      return Status::kInvalid;
+    }
+    if (t.rows == 0 || t.cols == 0) continue;
+    if (t.rows > (int64_t(1) << 40) / t.cols) {
+      *err = "tensor " + std::to_string(i) + ": too many elements";
+      return Status::kInvalid;
+    }
+    if (!t.w || !t.g || !t.m) {
+      *err = "tensor " + std::to_string(i) + ": null params, grads or momentum pointer";
+      return Status::kInvalid;
+    }
+    auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; };
+    if (!al(t.w) || !al(t.g) || !al(t.m)) {
+      *err = "tensor " + std::to_string(i) + ": pointers must be 4-byte aligned fp32";
+      return Status::kInvalid;
+    }
+    const uintptr_t bytes = uintptr_t(t.rows * t.cols) * 4u;
+    wr.push_back({reinterpret_cast<uintptr_t>(t.w), reinterpret_cast<uintptr_t>(t.w) + bytes});
+    wr.push_back({reinterpret_cast<uintptr_t>(t.m), reinterpret_cast<uintptr_t>(t.m) + bytes});
+    rd.push_back({reinterpret_cast<uintptr_t>(t.g), reinterpret_cast<uintptr_t>(t.g) + bytes});
+  }
+  std::sort(wr.begin(), wr.end());
+  for (size_t i = 1; i < wr.size(); ++i) {
+    if (wr[i].first < wr[i - 1].second) {
+      *err = "params / momentum buffers overlap";
+      return Status::kInvalid;
+    }
+  }
+  // every read-only range must be disjoint from every writable range
+  for (const auto& r : rd) {
+    auto it = std::upper_bound(wr.begin(), wr.end(), std::make_pair(r.first, ~uintptr_t(0)));
+    if (it != wr.end() && it->first < r.second) {
+      *err = "a gradient buffer overlaps params or momentum";
+      return Status::kInvalid;
+    }
+    if (it != wr.begin() && std::prev(it)->second > r.first) {
+      *err = "a gradient buffer overlaps params or momentum";
+      return Status::kInvalid;
+    }
+  }
+  return Status::kOk;
+}
+
+void split_by_xcd(std::vector<GemmTask>* tasks, const std::vector<int64_t>& cost,
+                  XcdSplit* split) {
+  const size_t n = tasks->size();
+  const int64_t total = std::accumulate(cost.begin(), cost.end(), int64_t(0));
+  // cut points: segment x ends once the running cost reaches (x+1)/8 of total
+  std::vector<size_t> cut(kXcds + 1, 0);
+  size_t pos = 0;
+  int64_t run = 0;
+  for (int x = 0; x < kXcds; ++x) {
+    cut[x] = pos;
+    const int64_t goal = (total * (x + 1) + kXcds - 1) / kXcds;
+    while (pos < n && (run < goal || x == kXcds - 1)) {
+      run += cost[pos];
+      ++pos;
+    }
+  }
+  cut[kXcds] = n;
+  std::vector<GemmTask> out;
+  out.reserve(n);
+  split->max_count = 0;
+  for (int x = 0; x < kXcds; ++x) {
+    std::vector<size_t> idx(cut[x + 1] - cut[x]);
+    std::iota(idx.begin(), idx.end(), cut[x]);
+    std::stable_sort(idx.begin(), idx.end(),
+                     [&](size_t a, size_t b) { return cost[a] > cost[b]; });
+    split->start[x] = int32_t(out.size());
+    split->count[x] = int32_t(idx.size());
+    split->max_count = std::max(split->max_count, split->count[x]);
+    for (size_t i : idx) out.push_back((*tasks)[i]);
+  }
+  tasks->swap(out);
+}
+
+Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec,
+                  bool kappa_rms02, Plan* p, std::string* err) {
+  *p = Plan();
+  p->muon_step = muon_step;
+  p->lion_block_start.push_back(0);
+  p->prep_start.push_back(0);
+  std::map<std::pair<int64_t, int64_t>, int> classes;
+  int64_t ns_off = 0;   // bytes
+  for (int32_t i = 0; i < n; ++i) {
+    const TensorIn& t = x[i];
+    if (t.rows == 0 || t.cols == 0) continue;
+    ++p->n_tensors;
+    const bool vec_ok = ((reinterpret_cast<uintptr_t>(t.w) | reinterpret_cast<uintptr_t>(t.g) |
+                          reinterpret_cast<uintptr_t>(t.m)) & 15u) == 0;
+    if (!(muon_step && is_matrix(t))) {
+      LionTensor lt{};
+      lt.w = t.w;
+      lt.g = t.g;
+      lt.m = t.m;
+      lt.numel = t.rows * t.cols;
+      lt.vec_ok = vec_ok ? 1 : 0;
+      const int64_t blocks = (lt.numel + kLionBlockElems - 1) / kLionBlockElems;
+      if (int64_t(p->lion_block_start.back()) + blocks > INT32_MAX) {
+        *err = "too many elements on the Lion branch";
+        return Status::kUnsupported;
+      }
+      p->lion.push_back(lt);
+      p->lion_block_start.push_back(p->lion_block_start.back() + int32_t(blocks));
+      p->lion_elements += lt.numel;
+      continue;
+    }
+    MuonMat mm{};
+    mm.w = t.w;
+    mm.g = t.g;
+    mm.m = t.m;
+    mm.rows = t.rows;
+    mm.cols = t.cols;
+    mm.transposed = t.rows > t.cols ? 1 : 0;
+    const int64_t s = std::min(t.rows, t.cols), l = std::max(t.rows, t.cols);
+    if (s > kMaxShortSide || round_up(s, kTile) * round_up(l, kTile) > kMaxMatrixElems) {
+      *err = "tensor " + std::to_string(i) + ": matrix too large for the Newton-Schulz kernels";
+      return Status::kUnsupported;
+    }
+    mm.s = int32_t(s);
+    mm.l = int32_t(l);
+    mm.s_pad = int32_t(round_up(s, kTile));
+    mm.l_pad = int32_t(round_up(l, kTile));
+    // vector path on the original rows needs 16-byte aligned rows
+    mm.vec_ok = (vec_ok && (t.cols % 4) == 0) ? 1 : 0;
+    mm.fp32 = prec.fp32_for(s) ? 1 : 0;
+    const int64_t eb = mm.fp32 ? 4 : 2;
+    const int64_t sl = int64_t(mm.s_pad) * mm.l_pad * eb, ss = int64_t(mm.s_pad) * mm.s_pad * eb;
+    mm.off_x[0] = ns_off;  ns_off += sl;
+    mm.off_x[1] = ns_off;  ns_off += sl;
+    mm.off_xt[0] = ns_off; ns_off += sl;
+    mm.off_xt[1] = ns_off; ns_off += sl;
+    mm.off_a = ns_off;     ns_off += ss;
+    mm.off_b = ns_off;     ns_off += ss;
+    const int64_t rows_pad = mm.transposed ? mm.l_pad : mm.s_pad;
+    const int64_t cols_pad = mm.transposed ? mm.s_pad : mm.l_pad;
+    mm.prep_tiles_n = int32_t(cols_pad / kPrepTile);
+    mm.prep_count = int32_t((rows_pad / kPrepTile) * (cols_pad / kPrepTile));
+    mm.prep_first = p->prep_start.back();
+    if (int64_t(mm.prep_first) + mm.prep_count > INT32_MAX) {
+      *err = "too many elements on the Muon branch";
+      return Status::kUnsupported;
+    }
+    mm.kappa = kappa_rms02 ? float(0.2 * std::sqrt(double(l))) : 1.0f;
+    p->prep_start.push_back(mm.prep_first + mm.prep_count);
+    p->mats.push_back(mm);
+    p->muon_elements += t.rows * t.cols;
+    classes[{s, l}] += 1;
+  }
+  p->n_shape_classes = int32_t(classes.size());
+
+  // GEMM work lists in canonical order (matrix, then tiles), cost = inner
+  // dimension, one list per Newton-Schulz precision.
+  for (int pr = 0; pr < 2; ++pr) {
+    std::vector<int64_t> cg, cp, ca;
+    for (int32_t mi = 0; mi < int32_t(p->mats.size()); ++mi) {
+      const MuonMat& mm = p->mats[mi];
+      if (mm.fp32 != pr) continue;
+      const int ts = mm.s_pad / kTile, tl = mm.l_pad / kTile;
+      for (int tm = 0; tm < ts; ++tm) {
+        for (int tn = 0; tn <= tm; ++tn) {      // symmetric: lower triangle
+          p->gram[pr].push_back({mi, int16_t(tm), int16_t(tn)});
+          cg.push_back(mm.l_pad);
+          p->poly[pr].push_back({mi, int16_t(tm), int16_t(tn)});
+          cp.push_back(mm.s_pad);
+        }
+      }
+      for (int tn = 0; tn < tl; ++tn) {
+        for (int tm = 0; tm < ts; ++tm) {
+          p->apply[pr].push_back({mi, int16_t(tm), int16_t(tn)});
+          ca.push_back(mm.s_pad);
+        }
+      }
+    }
+    split_by_xcd(&p->gram[pr], cg, &p->gram_split[pr]);
+    split_by_xcd(&p->poly[pr], cp, &p->poly_split[pr]);
+    split_by_xcd(&p->apply[pr], ca, &p->apply_split[pr]);
+  }
+
+  size_t off = align256(size_t(ns_off));
+  p->ws_partials_off = off;
+  off = align256(off + size_t(p->prep_start.back()) * sizeof(float));
+  p->ws_rscale_off = off;
+  off = align256(off + p->mats.size() * sizeof(float));
+  p->ws_bytes = p->mats.empty() ? 0 : off;
+  return Status::kOk;
+}
+
+double ns_flops_symmetric(const Plan& p, int k) {
+  double f = 0.0;
+  for (const MuonMat& m : p.mats) {
+    const double s = m.s, l = m.l;
+    f += s * (s + 1.0) * l + s * s * (s + 1.0) + 2.0 * s * s * l;
+  }
+  return f * k;
+}
+
+double ns_flops_dense(const Plan& p, int k) {
+  double f = 0.0;
+  for (const MuonMat& m : p.mats) {
+    const double s = m.s, l = m.l;
+    f += 4.0 * s * s * l + 2.0 * s * s * s;
+  }
+  return f * k;
+}
+
+}  // namespace lm

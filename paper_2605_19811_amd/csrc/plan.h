@@ -1,0 +1,97 @@
+// Host planner of the LionMuon step: argument validation, the per-tensor
+// Lion / Muon decision of Algorithm 1, Newton-Schulz shape classes and
+// transpose flags, workspace layout and the GEMM tile work lists.
+// Pure C++: no HIP call, so it runs (and is tested) on a host without a GPU.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "lm_desc.h"
+
+namespace lm {
+
+struct TensorIn {
+  float* w;
+  const float* g;
+  float* m;
+  int64_t rows, cols;
+  uint32_t flags;
+  uint32_t reserved;
+};
+
+enum class Status : int { kOk = 0, kInvalid = 1, kUnsupported = 2, kNoMemory = 3,
+                          kWorkspaceTooSmall = 4, kHip = 5 };
+
+// Largest Muon matrix the kernels accept: short side and element count.
+constexpr int64_t kMaxShortSide = 16384;
+constexpr int64_t kMaxMatrixElems = int64_t(1) << 30;
+
+// Muon branch of Algorithm 1: period P >= 1 and t mod P == 0 (P = 0 is P = inf).
+bool is_muon_step(int64_t t, int32_t P);
+
+// A tensor takes the Muon branch on Muon steps iff it is a real matrix
+// (rows > 1 and cols > 1) and not flagged Lion-only.
+bool is_matrix(const TensorIn& x);
+
+// Newton-Schulz precision of one matrix: bf16 MFMA unless fp32 is asked for
+// or the short side is below bf16_min_side (where bf16 rounding of the s x s
+// products no longer meets the bf16 error budget and fp32 costs little).
+struct NsPrecision {
+  bool all_fp32 = false;
+  int32_t bf16_min_side = 64;
+  bool fp32_for(int64_t short_side) const { return all_fp32 || short_side < bf16_min_side; }
+};
+
+struct Plan {
+  bool muon_step = false;
+
+  // Lion branch
+  std::vector<LionTensor> lion;
+  std::vector<int32_t> lion_block_start;   // lion.size() + 1 prefix
+  int64_t lion_elements = 0;
+
+  // Muon branch
+  std::vector<MuonMat> mats;
+  std::vector<int32_t> prep_start;         // mats.size() + 1 prefix of prep tiles
+  // Newton-Schulz tile lists, [0] bf16 matrices, [1] fp32 matrices, each
+  // grouped per XCD segment
+  std::vector<GemmTask> gram[2], poly[2], apply[2];
+  XcdSplit gram_split[2]{}, poly_split[2]{}, apply_split[2]{};
+  int64_t muon_elements = 0;
+  int32_t n_shape_classes = 0;
+
+  // workspace layout, bytes from the (256-byte aligned) base
+  size_t ws_partials_off = 0;   // float per preparation tile
+  size_t ws_rscale_off = 0;     // float per matrix
+  size_t ws_bytes = 0;
+
+  int32_t n_tensors = 0;        // non-empty tensors
+};
+
+// Validate hyper-parameters of one step. On failure fills *err.
+Status validate_scalars(int64_t t, int32_t P, double beta1, double beta2, double wd,
+                        double lr_muon, double lr_lion, std::string* err);
+
+// Validate the tensor list: pointers, shapes, flags and buffer overlaps.
+Status validate_tensors(const TensorIn* x, int32_t n, std::string* err);
+
+// Build the plan for a Lion step (muon_step = false) or a Muon step;
+// kappa_rms02 selects Table 4 output scaling.
+Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec,
+                  bool kappa_rms02, Plan* out, std::string* err);
+
+// Split an ordered task list (cost = inner dimension of each tile) into one
+// contiguous segment per XCD with near-equal total cost, then order each
+// segment by decreasing cost (stable). Exposed for tests.
+void split_by_xcd(std::vector<GemmTask>* tasks, const std::vector<int64_t>& cost,
+                  XcdSplit* split);
+
+// Algorithmic Newton-Schulz flops of one Muon step over the plan's matrices.
+double ns_flops_symmetric(const Plan& p, int ns_steps);
+double ns_flops_dense(const Plan& p, int ns_steps);
+
+}  // namespace lm

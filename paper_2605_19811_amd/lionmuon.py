@@ -1,0 +1,297 @@
+"""ctypes binding of ``liblionmuon.so`` (the C ABI in ``include/lionmuon.h``).
+
+Argument marshalling only: every step of the optimizer runs in the library's
+gfx950 kernels. PyTorch tensors provide device memory and the HIP stream.
+There is no fallback: a missing library or a non-GPU tensor raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblionmuon.so")
+
+LM_OK = 0
+LM_ERR_INVALID_ARGUMENT = 1
+LM_ERR_UNSUPPORTED = 2
+LM_ERR_OUT_OF_MEMORY = 3
+LM_ERR_WORKSPACE_TOO_SMALL = 4
+LM_ERR_HIP = 5
+
+LM_TENSOR_LION_ONLY = 1
+LM_NS_BF16 = 0
+LM_NS_FP32 = 1
+LM_NS_SCALE_NONE = 0
+LM_NS_SCALE_RMS02 = 1
+
+PHASES = ("lion", "prep", "norm", "gram", "poly", "apply")
+
+EXPORTED = ("lionmuon_config_default", "lionmuon_step", "lionmuon_step_ex",
+            "lionmuon_workspace_bytes", "lionmuon_ns", "lionmuon_plan_info",
+            "lionmuon_profiling_enable", "lionmuon_profiling_read",
+            "lionmuon_profiling_reset", "lionmuon_release",
+            "lionmuon_status_string", "lionmuon_last_error", "lionmuon_abi_version")
+
+
+class lm_shape(ctypes.Structure):
+    _fields_ = [("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("flags", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
+
+
+class lm_config(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("ns_steps", ctypes.c_int32),
+                ("ns_a", ctypes.c_double), ("ns_b", ctypes.c_double),
+                ("ns_c", ctypes.c_double), ("ns_eps", ctypes.c_double),
+                ("ns_precision", ctypes.c_int32), ("ns_scale_mode", ctypes.c_int32),
+                ("lr_muon", ctypes.c_double), ("lr_lion", ctypes.c_double),
+                ("ns_bf16_min_side", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class lm_plan_info(ctypes.Structure):
+    _fields_ = [("n_tensors", ctypes.c_int32), ("n_lion", ctypes.c_int32),
+                ("n_muon", ctypes.c_int32), ("n_shape_classes", ctypes.c_int32),
+                ("lion_elements", ctypes.c_int64), ("muon_elements", ctypes.c_int64),
+                ("gram_tiles", ctypes.c_int64), ("poly_tiles", ctypes.c_int64),
+                ("apply_tiles", ctypes.c_int64), ("ns_flops", ctypes.c_double),
+                ("ns_flops_dense", ctypes.c_double), ("lion_bytes", ctypes.c_double),
+                ("workspace_bytes", ctypes.c_size_t)]
+
+
+class lm_phase_times(ctypes.Structure):
+    _fields_ = [("ms", ctypes.c_double * 6), ("launches", ctypes.c_int64 * 6)]
+
+
+class LionMuonError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(message)
+        self.status = status
+
+
+_lib = None
+
+
+def library():
+    """Load the built library (``__graft_entry__.build()`` builds it)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise LionMuonError(-1, f"{LIB_PATH} is not built: run __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER
+    vp = ctypes.c_void_p
+    i32, i64, f64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_size_t
+    lib.lionmuon_config_default.argtypes = [P(lm_config)]
+    lib.lionmuon_config_default.restype = None
+    lib.lionmuon_step.argtypes = [vp, vp, vp, P(lm_shape), i32, i64, i32, f64, f64, f64, f64, vp]
+    lib.lionmuon_step.restype = ctypes.c_int
+    lib.lionmuon_step_ex.argtypes = [vp, vp, vp, P(lm_shape), i32, i64, i32, f64, f64, f64,
+                                     P(lm_config), vp, sz, vp]
+    lib.lionmuon_step_ex.restype = ctypes.c_int
+    lib.lionmuon_workspace_bytes.argtypes = [P(lm_shape), i32, P(lm_config), P(sz)]
+    lib.lionmuon_workspace_bytes.restype = ctypes.c_int
+    lib.lionmuon_ns.argtypes = [vp, vp, i64, i64, i32, P(lm_config), vp, sz, vp]
+    lib.lionmuon_ns.restype = ctypes.c_int
+    lib.lionmuon_plan_info.argtypes = [P(lm_shape), i32, i64, i32, P(lm_config), P(lm_plan_info)]
+    lib.lionmuon_plan_info.restype = ctypes.c_int
+    lib.lionmuon_profiling_enable.argtypes = [i32]
+    lib.lionmuon_profiling_enable.restype = ctypes.c_int
+    lib.lionmuon_profiling_read.argtypes = [P(lm_phase_times)]
+    lib.lionmuon_profiling_read.restype = ctypes.c_int
+    lib.lionmuon_profiling_reset.argtypes = []
+    lib.lionmuon_profiling_reset.restype = ctypes.c_int
+    lib.lionmuon_release.argtypes = []
+    lib.lionmuon_release.restype = None
+    lib.lionmuon_status_string.argtypes = [ctypes.c_int]
+    lib.lionmuon_status_string.restype = ctypes.c_char_p
+    lib.lionmuon_last_error.argtypes = []
+    lib.lionmuon_last_error.restype = ctypes.c_char_p
+    lib.lionmuon_abi_version.argtypes = []
+    lib.lionmuon_abi_version.restype = i32
+    _lib = lib
+    return lib
+
+
+def _check(status, what):
+    if status != LM_OK:
+        lib = library()
+        raise LionMuonError(status, f"{what}: {lib.lionmuon_status_string(status).decode()}: "
+                                    f"{lib.lionmuon_last_error().decode()}")
+
+
+def config(ns_steps=5, ns_coeffs=(3.4445, -4.7750, 2.0315), ns_eps=1e-7,
+           ns_precision="bf16", ns_scale="none", lr_muon=0.0, lr_lion=0.0,
+           ns_bf16_min_side=64) -> lm_config:
+    cfg = lm_config()
+    library().lionmuon_config_default(ctypes.byref(cfg))
+    cfg.ns_steps = ns_steps
+    cfg.ns_a, cfg.ns_b, cfg.ns_c = ns_coeffs
+    cfg.ns_eps = ns_eps
+    cfg.ns_precision = {"bf16": LM_NS_BF16, "fp32": LM_NS_FP32}[ns_precision]
+    cfg.ns_scale_mode = {"none": LM_NS_SCALE_NONE, "rms02": LM_NS_SCALE_RMS02}[ns_scale]
+    cfg.lr_muon = lr_muon
+    cfg.lr_lion = lr_lion
+    cfg.ns_bf16_min_side = ns_bf16_min_side
+    return cfg
+
+
+def shape_of(t, lion_only=False) -> lm_shape:
+    """rows x cols of a tensor: 1-D -> (1, n); k-D -> (shape[0], prod(rest))."""
+    dims = tuple(t.shape)
+    if len(dims) == 0:
+        rows, cols = 1, 1
+    elif len(dims) == 1:
+        rows, cols = 1, dims[0]
+    else:
+        rows = dims[0]
+        cols = 1
+        for d in dims[1:]:
+            cols *= d
+    return lm_shape(rows, cols, LM_TENSOR_LION_ONLY if lion_only else 0, 0)
+
+
+def shapes_array(specs):
+    """lm_shape array from (rows, cols, lion_only) triples."""
+    arr = (lm_shape * max(len(specs), 1))()
+    for i, (r, c, lo) in enumerate(specs):
+        arr[i] = lm_shape(r, c, LM_TENSOR_LION_ONLY if lo else 0, 0)
+    return arr
+
+
+def _check_tensor(t, name):
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise LionMuonError(LM_ERR_INVALID_ARGUMENT, f"{name} must be a GPU tensor")
+    if t.dtype != torch.float32:
+        raise LionMuonError(LM_ERR_INVALID_ARGUMENT, f"{name} must be float32")
+    if not t.is_contiguous():
+        raise LionMuonError(LM_ERR_INVALID_ARGUMENT, f"{name} must be contiguous")
+
+
+def _stream_handle(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+class TensorList:
+    """Marshalled pointer arrays of one (params, grads, momentum) list."""
+
+    def __init__(self, params, grads, momentum, lion_only=None):
+        n = len(params)
+        if len(grads) != n or len(momentum) != n:
+            raise ValueError("params, grads and momentum must have one length")
+        lion_only = list(lion_only) if lion_only is not None else [False] * n
+        for i in range(n):
+            _check_tensor(params[i], f"params[{i}]")
+            _check_tensor(grads[i], f"grads[{i}]")
+            _check_tensor(momentum[i], f"momentum[{i}]")
+            if params[i].shape != grads[i].shape or params[i].shape != momentum[i].shape:
+                raise ValueError(f"tensor {i}: params, grads and momentum shapes differ")
+        self.n = n
+        k = max(n, 1)
+        self.p = (ctypes.c_void_p * k)(*[t.data_ptr() for t in params])
+        self.g = (ctypes.c_void_p * k)(*[t.data_ptr() for t in grads])
+        self.m = (ctypes.c_void_p * k)(*[t.data_ptr() for t in momentum])
+        self.shapes = (lm_shape * k)(*[shape_of(t, lo) for t, lo in zip(params, lion_only)])
+        self._keep = (list(params), list(grads), list(momentum))
+
+    def set_grads(self, grads):
+        for i, t in enumerate(grads):
+            _check_tensor(t, f"grads[{i}]")
+            if t.shape != self._keep[0][i].shape:
+                raise ValueError(f"grads[{i}] has the wrong shape")
+            self.g[i] = t.data_ptr()
+        self._keep = (self._keep[0], list(grads), self._keep[2])
+
+
+def lionmuon_step(params, grads, momentum, t, P, beta1, beta2, lr, wd, stream=None,
+                  lion_only=None, tensors: TensorList | None = None):
+    """One LionMuon step (Algorithm 1) with eta_M = eta_L = lr, bf16 NS."""
+    tl = tensors or TensorList(params, grads, momentum, lion_only)
+    st = library().lionmuon_step(ctypes.cast(tl.p, ctypes.c_void_p), ctypes.cast(tl.g, ctypes.c_void_p),
+                                 ctypes.cast(tl.m, ctypes.c_void_p), tl.shapes, tl.n, int(t), int(P),
+                                 beta1, beta2, lr, wd, _stream_handle(stream))
+    _check(st, "lionmuon_step")
+
+
+def lionmuon_step_ex(params, grads, momentum, t, P, beta1, beta2, wd, cfg: lm_config,
+                     workspace=None, stream=None, lion_only=None,
+                     tensors: TensorList | None = None):
+    """One LionMuon step with an explicit lm_config; ``workspace`` is an
+    optional uint8 GPU tensor (caller-owned workspace)."""
+    tl = tensors or TensorList(params, grads, momentum, lion_only)
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        if not workspace.is_cuda:
+            raise LionMuonError(LM_ERR_INVALID_ARGUMENT, "workspace must be a GPU tensor")
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    st = library().lionmuon_step_ex(ctypes.cast(tl.p, ctypes.c_void_p), ctypes.cast(tl.g, ctypes.c_void_p),
+                                    ctypes.cast(tl.m, ctypes.c_void_p), tl.shapes, tl.n, int(t),
+                                    int(P), beta1, beta2, wd, ctypes.byref(cfg), ws_ptr, ws_bytes,
+                                    _stream_handle(stream))
+    _check(st, "lionmuon_step_ex")
+
+
+def lionmuon_ns(X, cfg: lm_config | None = None, out=None, stream=None):
+    """O = kappa * NS_K(X) for X of shape (rows, cols) or (batch, rows, cols)."""
+    import torch
+    _check_tensor(X, "X")
+    if X.dim() not in (2, 3):
+        raise ValueError("X must be 2-D or 3-D")
+    batch = 1 if X.dim() == 2 else X.shape[0]
+    rows, cols = X.shape[-2], X.shape[-1]
+    if out is None:
+        out = torch.empty_like(X)
+    _check_tensor(out, "out")
+    st = library().lionmuon_ns(X.data_ptr(), out.data_ptr(), rows, cols, batch,
+                               ctypes.byref(cfg) if cfg is not None else None, None, 0,
+                               _stream_handle(stream))
+    _check(st, "lionmuon_ns")
+    return out
+
+
+def lionmuon_workspace_bytes(specs, cfg: lm_config | None = None) -> int:
+    arr = shapes_array(specs)
+    out = ctypes.c_size_t(0)
+    st = library().lionmuon_workspace_bytes(arr, len(specs),
+                                            ctypes.byref(cfg) if cfg is not None else None,
+                                            ctypes.byref(out))
+    _check(st, "lionmuon_workspace_bytes")
+    return out.value
+
+
+def lionmuon_plan_info(specs, t, P, cfg: lm_config | None = None) -> dict:
+    arr = shapes_array(specs)
+    info = lm_plan_info()
+    st = library().lionmuon_plan_info(arr, len(specs), int(t), int(P),
+                                      ctypes.byref(cfg) if cfg is not None else None,
+                                      ctypes.byref(info))
+    _check(st, "lionmuon_plan_info")
+    return {name: getattr(info, name) for name, _ in lm_plan_info._fields_}
+
+
+def lionmuon_profiling_enable(enable=True):
+    _check(library().lionmuon_profiling_enable(1 if enable else 0), "lionmuon_profiling_enable")
+
+
+def lionmuon_profiling_reset():
+    _check(library().lionmuon_profiling_reset(), "lionmuon_profiling_reset")
+
+
+def lionmuon_profiling_read() -> dict:
+    t = lm_phase_times()
+    _check(library().lionmuon_profiling_read(ctypes.byref(t)), "lionmuon_profiling_read")
+    return {p: {"ms": t.ms[i], "launches": t.launches[i]} for i, p in enumerate(PHASES)}
+
+
+def lionmuon_release():
+    library().lionmuon_release()
+
+
+def lionmuon_abi_version() -> int:
+    return library().lionmuon_abi_version()

@@ -1,0 +1,69 @@
+"""Comparison rules between the GPU step and the fp64 oracle.
+
+Lion branch: the sign pattern must match exactly wherever the fp64 direction
+is clear of the fp32 rounding band |Ghat| <= 2^-22 (beta1 |M| + (1-beta1)|G|)
+(there both signs are correct results of the fp32 computation); weights and
+momentum within 1e-6 norm-wise relative error (max-norm and Frobenius).
+Muon branch: the update direction recovered from W, (W - W')/eta_M - wd W,
+within a relative Frobenius error of 2e-2 (bf16 MFMA path) or 1e-4 (fp32
+path) of kappa NS_5(Ghat); momentum as on the Lion branch.
+"""
+import numpy as np
+
+import oracle
+
+LION_TOL = 1e-6
+NS_TOL = {"bf16": 2e-2, "fp32": 1e-4}
+
+
+def rel_max(a, b):
+    den = np.abs(b).max()
+    return float(np.abs(a - b).max() / den) if den > 0 else float(np.abs(a).max())
+
+
+def rel_fro(a, b):
+    den = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / den) if den > 0 else float(np.linalg.norm(a))
+
+
+def check_momentum(M0, G, M_gpu, beta2):
+    ref = beta2 * M0.astype(np.float64) + (1.0 - beta2) * G.astype(np.float64)
+    assert rel_max(M_gpu, ref) <= LION_TOL, rel_max(M_gpu, ref)
+    assert rel_fro(M_gpu, ref) <= LION_TOL, rel_fro(M_gpu, ref)
+
+
+def check_lion(W0, G, M0, W_gpu, M_gpu, beta1, beta2, lr, wd, lion_only=True):
+    """Returns the number of positions in the rounding band (excluded from
+    the exact-sign comparison)."""
+    W0d, Gd, M0d = (np.asarray(x, np.float64) for x in (W0, G, M0))
+    w_ref, m_ref = oracle.lionmuon_update(W0d, Gd, M0d, 1, 0, beta1, beta2, 0.0, lr, wd,
+                                          lion_only=lion_only)
+    ghat = beta1 * M0d + (1.0 - beta1) * Gd
+    band = np.abs(ghat) <= 2.0 ** -22 * (beta1 * np.abs(M0d) + (1.0 - beta1) * np.abs(Gd))
+    band &= ghat != 0.0
+    W_gpu = np.asarray(W_gpu, np.float64)
+    if lr > 0:
+        s_gpu = np.rint((W0d - W_gpu) / lr - wd * W0d)
+        s_ref = np.sign(ghat)
+        mism = (s_gpu != s_ref) & ~band
+        assert not mism.any(), f"{int(mism.sum())} sign mismatches outside the rounding band"
+    keep = ~band
+    assert rel_max(W_gpu[keep], w_ref[keep]) <= LION_TOL, rel_max(W_gpu[keep], w_ref[keep])
+    assert rel_fro(W_gpu[keep], w_ref[keep]) <= LION_TOL, rel_fro(W_gpu[keep], w_ref[keep])
+    check_momentum(M0, G, M_gpu, beta2)
+    return int(band.sum())
+
+
+def muon_direction_error(W0, G, M0, W_gpu, beta1, lr, wd, kappa=1.0):
+    W0d = np.asarray(W0, np.float64)
+    ghat = beta1 * np.asarray(M0, np.float64) + (1.0 - beta1) * np.asarray(G, np.float64)
+    o_ref = kappa * oracle.newton_schulz(ghat)
+    o_gpu = (W0d - np.asarray(W_gpu, np.float64)) / lr - wd * W0d
+    return rel_fro(o_gpu, o_ref)
+
+
+def check_muon(W0, G, M0, W_gpu, M_gpu, beta1, beta2, lr, wd, precision, kappa=1.0):
+    err = muon_direction_error(W0, G, M0, W_gpu, beta1, lr, wd, kappa)
+    assert err <= NS_TOL[precision], f"Muon direction error {err:.3e} > {NS_TOL[precision]}"
+    check_momentum(M0, G, M_gpu, beta2)
+    return err

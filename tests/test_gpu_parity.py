@@ -1,0 +1,374 @@
+"""GPU parity of the LionMuon step against the fp64 oracle, through the C ABI.
+
+Every input is seeded and synthetic (``workloads``); expected values come from
+``oracle`` only. Sizes span several 128-wide MFMA tiles and ragged tails; the
+full matrix sets of the benchmark are checked on sampled tensors.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from paper_2605_19811_amd import lionmuon as lm
+
+from parity import (NS_TOL, check_lion, check_momentum, check_muon,
+                    muon_direction_error, rel_fro)
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+
+
+def dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def host(t):
+    return t.detach().cpu().double().numpy()
+
+
+def sync():
+    torch.cuda.synchronize()
+
+
+# --------------------------------------------------------------------------
+# Lion branch
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("numel", [1, 3, 4, 1000, 4095, 4096, 4097, 12345, 589824])
+@pytest.mark.parametrize("offset", [0, 1])
+def test_lion_step_ragged_and_misaligned(numel, offset):
+    rng = np.random.default_rng([numel, offset])
+    W0 = (rng.standard_normal(numel) * 0.02).astype(np.float32)
+    M0 = (rng.standard_normal(numel) * 1e-2).astype(np.float32)
+    G = (rng.standard_normal(numel) * 1e-2).astype(np.float32)
+    G[: min(numel, 3)] = 0.0
+    M0[: min(numel, 2)] = 0.0              # Ghat = 0 -> sign 0
+    # offset 1 makes every pointer 4-byte but not 16-byte aligned (scalar path)
+    bufs = [torch.zeros(numel + 8, device=DEV) for _ in range(3)]
+    W, M, Gd = (b[offset:offset + numel] for b in bufs)
+    W.copy_(dev(W0)); M.copy_(dev(M0)); Gd.copy_(dev(G))
+    lm.lionmuon_step([W], [Gd], [M], t=1, P=2, beta1=0.9, beta2=0.99, lr=0.01, wd=0.1)
+    sync()
+    check_lion(W0, G, M0, host(W), host(M), 0.9, 0.99, 0.01, 0.1)
+    assert torch.all(bufs[0][:offset] == 0) and torch.all(bufs[0][offset + numel:] == 0)
+
+
+def test_lion_step_multi_tensor_list():
+    shapes = [(1, 768), (768, 2304), (3, 5), (1, 1), (50, 77), (4096, 3)]
+    rng = np.random.default_rng(7)
+    W0 = [(rng.standard_normal(s) * 0.02).astype(np.float32) for s in shapes]
+    M0 = [(rng.standard_normal(s) * 1e-3).astype(np.float32) for s in shapes]
+    G = [(rng.standard_normal(s) * 1e-3).astype(np.float32) for s in shapes]
+    W, M, Gd = [dev(x) for x in W0], [dev(x) for x in M0], [dev(x) for x in G]
+    cfg = lm.config(lr_muon=1.0, lr_lion=2e-5)
+    lm.lionmuon_step_ex(W, Gd, M, 3, 2, 0.9, 0.99, 0.1, cfg)
+    sync()
+    bands = 0
+    for i in range(len(shapes)):
+        bands += check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 2e-5, 0.1)
+    assert bands < 10
+
+
+def test_pure_lion_period_never_runs_newton_schulz():
+    rng = np.random.default_rng(8)
+    W0 = (rng.standard_normal((256, 384)) * 0.02).astype(np.float32)
+    M0 = (rng.standard_normal((256, 384)) * 1e-2).astype(np.float32)
+    G = (rng.standard_normal((256, 384)) * 1e-2).astype(np.float32)
+    W, M = dev(W0), dev(M0)
+    lm.lionmuon_profiling_reset()
+    lm.lionmuon_profiling_enable(True)
+    lm.lionmuon_step([W], [dev(G)], [M], t=0, P=0, beta1=0.9, beta2=0.99, lr=0.01, wd=0.1)
+    times = lm.lionmuon_profiling_read()
+    lm.lionmuon_profiling_enable(False)
+    assert times["gram"]["launches"] == 0 and times["lion"]["launches"] == 1
+    check_lion(W0, G, M0, host(W), host(M), 0.9, 0.99, 0.01, 0.1)
+
+
+# --------------------------------------------------------------------------
+# Newton-Schulz hook
+# --------------------------------------------------------------------------
+NS_SHAPES = [(2, 2), (2, 7), (100, 37), (37, 100), (128, 128), (130, 250), (250, 130),
+             (256, 640), (640, 256), (768, 768), (300, 1000)]
+
+
+@pytest.mark.parametrize("shape", NS_SHAPES)
+@pytest.mark.parametrize("precision", ["fp32", "bf16"])
+def test_ns_hook_matches_oracle(shape, precision):
+    X = workloads.random_matrix([21, *shape], *shape, std=1e-2)
+    out = lm.lionmuon_ns(dev(X), lm.config(ns_precision=precision))
+    sync()
+    err = rel_fro(host(out), oracle.newton_schulz(X))
+    assert err <= NS_TOL[precision], err
+
+
+def test_ns_hook_batch_and_scaling():
+    X = np.stack([workloads.random_matrix([22, b], 96, 200, std=1.0) for b in range(3)])
+    out = lm.lionmuon_ns(dev(X), lm.config(ns_precision="fp32", ns_scale="rms02"))
+    sync()
+    kappa = 0.2 * np.sqrt(200)
+    for b in range(3):
+        assert rel_fro(host(out[b]), kappa * oracle.newton_schulz(X[b])) <= 1e-4
+
+
+def test_ns_hook_zero_input_gives_zero():
+    out = lm.lionmuon_ns(torch.zeros(64, 200, device=DEV))
+    sync()
+    assert torch.all(out == 0)
+
+
+def test_ns_hook_cubic_coefficients_and_step_count():
+    X = workloads.random_matrix(23, 64, 160, std=1.0)
+    cfg = lm.config(ns_precision="fp32", ns_steps=12, ns_coeffs=(1.5, -0.5, 0.0))
+    out = lm.lionmuon_ns(dev(X), cfg)
+    sync()
+    ref = oracle.newton_schulz(X, 12, oracle.CUBIC, 1e-7)
+    assert rel_fro(host(out), ref) <= 1e-4
+
+
+def test_ns_hook_largest_long_side():
+    """The embedding shape (50257 x 1280), the largest matrix of the benchmark
+    sets, through the Muon kernels (long side padded to 50304)."""
+    X = workloads.random_matrix(24, 50257, 1280, std=1e-3)
+    out = lm.lionmuon_ns(dev(X), lm.config(ns_precision="bf16"))
+    sync()
+    err = rel_fro(host(out), oracle.newton_schulz(X))
+    assert err <= NS_TOL["bf16"], err
+
+
+# --------------------------------------------------------------------------
+# Whole steps
+# --------------------------------------------------------------------------
+def _state(shapes, seed, g_std=1e-2, m_std=1e-2):
+    rng = np.random.default_rng(seed)
+    W0 = [(rng.standard_normal(s) * 0.02).astype(np.float32) for s in shapes]
+    M0 = [(rng.standard_normal(s) * m_std).astype(np.float32) for s in shapes]
+    G = [(rng.standard_normal(s) * g_std).astype(np.float32) for s in shapes]
+    return W0, M0, G
+
+
+@pytest.mark.parametrize("precision", ["fp32", "bf16"])
+def test_mixed_list_muon_step(precision):
+    shapes = [(192, 320), (320, 192), (100, 37), (64, 64), (1, 300), (200, 1), (128, 256)]
+    lion_only = [False, False, False, True, False, False, False]
+    W0, M0, G = _state(shapes, 31)
+    W, M, Gd = [dev(x) for x in W0], [dev(x) for x in M0], [dev(x) for x in G]
+    lr_m, lr_l, wd = 0.02, 1e-3, 0.1
+    cfg = lm.config(ns_precision=precision, lr_muon=lr_m, lr_lion=lr_l)
+    lm.lionmuon_step_ex(W, Gd, M, 4, 2, 0.9, 0.99, wd, cfg, lion_only=lion_only)
+    sync()
+    for i, s in enumerate(shapes):
+        if lion_only[i] or min(s) == 1:
+            check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_l, wd)
+        else:
+            check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_m, wd, precision)
+
+
+def test_single768_four_steps():
+    """The 768x768 workload: M = 0, t = 1..4 with P = 2 (Lion, Muon, Lion,
+    Muon), fp32 Newton-Schulz. Each step starts from the oracle's own state
+    rounded to fp32 (step-local check); a free-running GPU trajectory is
+    compared with the fp64 oracle trajectory as well."""
+    wl = workloads.single768()
+    W0 = workloads.initial_weight(wl, 0)
+    M0 = workloads.initial_momentum(wl, 0)
+    cfg = lm.config(ns_precision="fp32", lr_muon=wl.lr_muon, lr_lion=wl.lr_lion)
+    w_or, m_or = W0.astype(np.float64), M0.astype(np.float64)
+    W_free, M_free = dev(W0), dev(M0)
+    for t in wl.extra["steps"]:
+        G = workloads.gradient(wl, 0, t)
+        Wf32, Mf32 = w_or.astype(np.float32), m_or.astype(np.float32)
+        W, M = dev(Wf32), dev(Mf32)
+        lm.lionmuon_step_ex([W], [dev(G)], [M], t, wl.P, wl.beta1, wl.beta2, wl.wd, cfg)
+        lm.lionmuon_step_ex([W_free], [dev(G)], [M_free], t, wl.P, wl.beta1, wl.beta2, wl.wd, cfg)
+        sync()
+        if oracle.is_muon_step(t, wl.P):
+            check_muon(Wf32, G, Mf32, host(W), host(M), wl.beta1, wl.beta2, wl.lr_muon, wl.wd, "fp32")
+        else:
+            check_lion(Wf32, G, Mf32, host(W), host(M), wl.beta1, wl.beta2, wl.lr_lion, wl.wd)
+        w_or, m_or = oracle.lionmuon_update(w_or, G, m_or, t, wl.P, wl.beta1, wl.beta2,
+                                            wl.lr_muon, wl.lr_lion, wl.wd)
+        # free-running: momentum never depends on W; W accumulates per-step errors
+        assert rel_fro(host(M_free), m_or) <= 1e-6
+        upd_ref = w_or - W0
+        assert rel_fro(host(W_free) - W0, upd_ref) <= 1e-4
+
+
+def test_special_cases_signmuon_and_pure_muon():
+    shapes = [(96, 160)]
+    W0, M0, G = _state(shapes, 41)
+    for beta, P, t in [(0.9, 1, 5), (0.9, 3, 6), (0.9, 3, 7)]:
+        W, M = dev(W0[0]), dev(M0[0])
+        cfg = lm.config(ns_precision="fp32", lr_muon=0.01, lr_lion=0.01)
+        lm.lionmuon_step_ex([W], [dev(G[0])], [M], t, P, beta, beta, 0.1, cfg)
+        sync()
+        if oracle.is_muon_step(t, P):
+            check_muon(W0[0], G[0], M0[0], host(W), host(M), beta, beta, 0.01, 0.1, "fp32")
+        else:
+            check_lion(W0[0], G[0], M0[0], host(W), host(M), beta, beta, 0.01, 0.1)
+
+
+def test_rms02_scaled_muon_step():
+    W0, M0, G = _state([(128, 300)], 42)
+    W, M = dev(W0[0]), dev(M0[0])
+    cfg = lm.config(ns_precision="bf16", ns_scale="rms02", lr_muon=0.002, lr_lion=0.0)
+    lm.lionmuon_step_ex([W], [dev(G[0])], [M], 0, 2, 0.9, 0.99, 0.1, cfg)
+    sync()
+    check_muon(W0[0], G[0], M0[0], host(W), host(M), 0.9, 0.99, 0.002, 0.1, "bf16",
+               kappa=0.2 * np.sqrt(300))
+
+
+def test_nan_gradient_propagates_without_crash():
+    W0, M0, G = _state([(64, 128), (1, 64)], 43)
+    G[0][3, 5] = np.nan
+    G[1][0, 7] = np.nan
+    W, M = [dev(x) for x in W0], [dev(x) for x in M0]
+    lm.lionmuon_step([W[0], W[1].view(-1)], [dev(G[0]), dev(G[1]).view(-1)],
+                     [M[0], M[1].view(-1)], t=0, P=1, beta1=0.9, beta2=0.99, lr=0.01, wd=0.1)
+    sync()
+    assert torch.isnan(M[0][3, 5]) and torch.isnan(M[1][0, 7])
+    assert torch.isnan(W[1][0, 7]) and not torch.isnan(W[1][0, 6])
+    assert torch.isnan(W[0]).all()      # NaN reaches every entry of the Muon direction
+
+
+# --------------------------------------------------------------------------
+# Determinism, resume, workspaces, streams, binding checks
+# --------------------------------------------------------------------------
+def _run_steps(shapes, seed, steps, precision="bf16", state=None):
+    W0, M0, _ = _state(shapes, seed)
+    if state is not None:
+        W0, M0 = state
+    W, M = [dev(x) for x in W0], [dev(x) for x in M0]
+    cfg = lm.config(ns_precision=precision, lr_muon=0.01, lr_lion=1e-3)
+    for t in steps:
+        G = [dev(workloads.random_matrix([seed, t, i], *s, std=1e-2)) for i, s in enumerate(shapes)]
+        lm.lionmuon_step_ex(W, G, M, t, 2, 0.9, 0.99, 0.1, cfg)
+    sync()
+    return [w.cpu().numpy() for w in W], [m.cpu().numpy() for m in M]
+
+
+def test_bitwise_determinism_and_resume():
+    shapes = [(256, 768), (768, 256), (300, 300)]
+    a_w, a_m = _run_steps(shapes, 51, [1, 2, 3, 4])
+    b_w, b_m = _run_steps(shapes, 51, [1, 2, 3, 4])
+    for x, y in zip(a_w + a_m, b_w + b_m):
+        assert np.array_equal(x, y)
+    h_w, h_m = _run_steps(shapes, 51, [1, 2])
+    lm.lionmuon_release()                      # resume from copied-out state only
+    r_w, r_m = _run_steps(shapes, 51, [3, 4], state=(h_w, h_m))
+    for x, y in zip(a_w + a_m, r_w + r_m):
+        assert np.array_equal(x, y)
+
+
+def test_caller_workspace_matches_library_workspace():
+    shapes = [(192, 320), (320, 192)]
+    W0, M0, G = _state(shapes, 52)
+    specs = [(r, c, False) for r, c in shapes]
+    cfg = lm.config(lr_muon=0.01, lr_lion=1e-3)
+    nbytes = lm.lionmuon_workspace_bytes(specs, cfg)
+    outs = []
+    for ws in [None, torch.empty(nbytes, dtype=torch.uint8, device=DEV)]:
+        W, M = [dev(x) for x in W0], [dev(x) for x in M0]
+        lm.lionmuon_step_ex(W, [dev(g) for g in G], M, 0, 1, 0.9, 0.99, 0.1, cfg, workspace=ws)
+        sync()
+        outs.append([w.cpu().numpy() for w in W] + [m.cpu().numpy() for m in M])
+    for x, y in zip(*outs):
+        assert np.array_equal(x, y)
+    small = torch.empty(nbytes // 2, dtype=torch.uint8, device=DEV)
+    W, M = [dev(x) for x in W0], [dev(x) for x in M0]
+    with pytest.raises(lm.LionMuonError) as e:
+        lm.lionmuon_step_ex(W, [dev(g) for g in G], M, 0, 1, 0.9, 0.99, 0.1, cfg, workspace=small)
+    assert e.value.status == lm.LM_ERR_WORKSPACE_TOO_SMALL
+    sync()
+    assert np.array_equal(W[0].cpu().numpy(), W0[0])   # invalid call modified nothing
+
+
+def test_side_stream():
+    W0, M0, G = _state([(128, 384)], 53)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        W, M, Gd = dev(W0[0]), dev(M0[0]), dev(G[0])
+        lm.lionmuon_step([W], [Gd], [M], t=0, P=1, beta1=0.9, beta2=0.99, lr=0.01, wd=0.1)
+    s.synchronize()
+    check_muon(W0[0], G[0], M0[0], host(W), host(M), 0.9, 0.99, 0.01, 0.1, "bf16")
+
+
+def test_binding_rejects_cpu_and_non_contiguous_tensors():
+    W = torch.zeros(8, 8, device=DEV)
+    with pytest.raises(lm.LionMuonError):
+        lm.lionmuon_step([W.cpu()], [W.cpu()], [W.cpu()], 1, 2, 0.9, 0.99, 0.01, 0.1)
+    X = torch.zeros(8, 16, device=DEV).t()
+    with pytest.raises(lm.LionMuonError):
+        lm.lionmuon_step([X], [X.clone()], [X.clone()], 1, 2, 0.9, 0.99, 0.01, 0.1)
+
+
+def test_profiling_counts_every_launch():
+    shapes = [(256, 512), (512, 256)]
+    W0, M0, G = _state(shapes, 54)
+    W, M = [dev(x) for x in W0], [dev(x) for x in M0]
+    lm.lionmuon_profiling_reset()
+    lm.lionmuon_profiling_enable(True)
+    lm.lionmuon_step(W, [dev(g) for g in G], M, 0, 2, 0.9, 0.99, 0.01, 0.1)
+    lm.lionmuon_step(W, [dev(g) for g in G], M, 1, 2, 0.9, 0.99, 0.01, 0.1)
+    t = lm.lionmuon_profiling_read()
+    lm.lionmuon_profiling_enable(False)
+    assert t["prep"]["launches"] == 1 and t["norm"]["launches"] == 1
+    assert t["gram"]["launches"] == 5 and t["poly"]["launches"] == 5 and t["apply"]["launches"] == 5
+    assert t["lion"]["launches"] == 1
+    assert all(v["ms"] > 0 for v in t.values())
+
+
+# --------------------------------------------------------------------------
+# Full benchmark sets, sampled tensors, same launch as the benchmark
+# --------------------------------------------------------------------------
+def _sample_indices(wl):
+    seen, out = set(), []
+    for i, t in enumerate(wl.tensors):
+        key = (t.rows, t.cols, t.lion_only)
+        if key not in seen:
+            seen.add(key)
+            out.append(i)
+    return out
+
+
+@pytest.mark.parametrize("name", ["gpt2-124m", "gpt2-355m", "gpt2-720m"])
+def test_full_set_sampled(name):
+    wl = workloads.get(name)
+    params, moms, grads = workloads.device_state(torch, wl, DEV, seed=5, warm=True, n_grad=1)
+    grads = grads[0]
+    idx = _sample_indices(wl)
+    before = {i: (params[i].cpu().numpy(), moms[i].cpu().numpy(), grads[i].cpu().numpy())
+              for i in idx}
+    lion_only = [t.lion_only for t in wl.tensors]
+    cfg = lm.config(ns_precision="bf16", lr_muon=wl.lr_muon, lr_lion=wl.lr_lion)
+    tl = lm.TensorList(params, grads, moms, lion_only)
+    print(f"{name}: Muon step over {len(params)} tensors", flush=True)
+    lm.lionmuon_step_ex(None, None, None, 2, wl.P, wl.beta1, wl.beta2, wl.wd, cfg, tensors=tl)
+    sync()
+    errs = []
+    rng = np.random.default_rng(0)
+    for i in idx:
+        W0, M0, G = before[i]
+        W1, M1 = params[i].cpu().numpy(), moms[i].cpu().numpy()
+        spec = wl.tensors[i]
+        if spec.lion_only or spec.rows == 1:
+            rows = rng.choice(W0.shape[0], size=min(W0.shape[0], 512), replace=False) \
+                if W0.ndim == 2 else slice(None)
+            check_lion(W0[rows], G[rows], M0[rows], W1[rows], M1[rows], wl.beta1, wl.beta2,
+                       wl.lr_lion, wl.wd)
+        else:
+            errs.append(check_muon(W0, G, M0, W1, M1, wl.beta1, wl.beta2, wl.lr_muon, wl.wd,
+                                   "bf16"))
+    print(f"{name}: Muon direction errors {['%.2e' % e for e in errs]}", flush=True)
+    # the following Lion step on the same tensors
+    before = {i: (params[i].cpu().numpy(), moms[i].cpu().numpy()) for i in idx}
+    lm.lionmuon_step_ex(None, None, None, 3, wl.P, wl.beta1, wl.beta2, wl.wd, cfg, tensors=tl)
+    sync()
+    for i in idx:
+        W0, M0 = before[i]
+        G = grads[i].cpu().numpy()
+        rows = slice(0, min(W0.shape[0], 1024)) if W0.ndim == 2 else slice(None)
+        check_lion(W0[rows], G[rows], M0[rows], params[i].cpu().numpy()[rows],
+                   moms[i].cpu().numpy()[rows], wl.beta1, wl.beta2, wl.lr_lion, wl.wd)
+    del params, moms, grads, tl
+    lm.lionmuon_release()
+    torch.cuda.empty_cache()
