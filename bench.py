@@ -120,7 +120,20 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without per-launch events (no roofline object)")
+    ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
+                    help="only run 4 plain device copies of MIB MiB (counter calibration)")
     args = ap.parse_args()
+    if args.calib_copy:
+        import torch
+        n = args.calib_copy * (1 << 20) // 4
+        x = torch.ones(n, device="cuda:0")
+        y = torch.empty_like(x)
+        for _ in range(4):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"calib_copy_bytes_read": 4 * n, "calib_copy_bytes_written": 4 * n,
+                          "launches": 4}))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
               f"layout is a design, not a build.", file=sys.stderr)

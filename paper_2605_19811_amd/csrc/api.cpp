@@ -313,6 +313,7 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
         gl.split = dp.d_splits + pr * 3 + st3;
         gl.max_count = sp.max_count;
         gl.fp32 = pr;
+        gl.tile = p.tile[pr][st3];
         e = lm::launch_gemm(modes[st3], gl, stream);
         if (e != hipSuccess) return hip_fail(e, "Newton-Schulz kernel launch");
       }

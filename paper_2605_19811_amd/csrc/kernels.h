@@ -55,6 +55,7 @@ struct GemmLaunch {
   float a, b, c;                 // odd polynomial coefficients
   float lr, wd;                  // eta_M and lambda of the W update
   int32_t fp32;                  // element type of the matrices in `tasks`
+  int32_t tile;                  // output tile edge of `tasks`: 128 or 256
 };
 hipError_t launch_gemm(GemmMode mode, const GemmLaunch& a, hipStream_t stream);
 

@@ -247,11 +247,16 @@ __global__ __launch_bounds__(256) void norm_kernel(PrepArgs a) {
 // ---------------------------------------------------------------------------
 // Newton-Schulz GEMMs
 // ---------------------------------------------------------------------------
-// C[128 x 128] = sum_k Aop[row0 + i][k] * Bop[col0 + j][k]: both operands are
+// C[BT x BT] = sum_k Aop[row0 + i][k] * Bop[col0 + j][k]: both operands are
 // K-contiguous ("NT"), staged through LDS 128 bytes of K per row per stage,
-// double buffered via registers. 4 waves, each a 64 x 64 sub-tile of 2 x 2
-// MFMA 32x32 blocks. Accumulator element r of block (mi, ni) sits at
-// row wm + 32 mi + 8 (r / 4) + 4 (lane / 32) + r % 4, col wn + 32 ni + lane % 32.
+// double buffered via registers (the next stage's global loads are in flight
+// while the current stage feeds the MFMAs).
+//   BT = 256: 8 waves (2 x 4), each a 128 x 64 sub-tile of 4 x 2 MFMA 32x32
+//             blocks (32 B of operand loads per CU-clock at full MFMA rate);
+//   BT = 128: 4 waves (2 x 2), each a 64 x 64 sub-tile of 2 x 2 blocks, for
+//             stages with too few 256-tiles to fill the chip.
+// Accumulator element r of block (mi, ni) sits at row
+// wm + 32 mi + 8 (r / 4) + 4 (lane / 32) + r % 4, col wn + 32 ni + lane % 32.
 template <typename T> struct Mfma;
 
 template <> struct Mfma<bf16> {
@@ -276,6 +281,14 @@ template <> struct Mfma<float> {
   }
 };
 
+template <int BT> struct TileGeom {
+  static constexpr int kWM = BT == 256 ? 128 : 64;   // wave sub-tile rows
+  static constexpr int kWN = 64;                      // wave sub-tile cols
+  static constexpr int kWavesN = BT / kWN;
+  static constexpr int kThreads = (BT / kWM) * kWavesN * 64;
+  static constexpr int kMI = kWM / 32, kNI = kWN / 32;
+};
+
 struct GemmArgs {
   const MuonMat* mats;
   const GemmTask* tasks;
@@ -286,14 +299,22 @@ struct GemmArgs {
   float a, b, c, lr, wd;
 };
 
-template <typename T, int MODE>
-__global__ __launch_bounds__(256, 2) void gemm_kernel(GemmArgs g) {
+template <typename T, int MODE, int BT>
+__global__ __launch_bounds__(TileGeom<BT>::kThreads) void gemm_kernel(GemmArgs g) {
   using M = Mfma<T>;
+  using Geo = TileGeom<BT>;
   constexpr int kBK = M::kBK;
   constexpr int kEpc = 16 / sizeof(T);           // elements per 16-byte chunk
   constexpr int kLd = kBK + kEpc;                // LDS row stride: 144 bytes
-  __shared__ __attribute__((aligned(16))) T sA[2][kTile][kLd];
-  __shared__ __attribute__((aligned(16))) T sB[2][kTile][kLd];
+  constexpr int kNT = Geo::kThreads;
+  constexpr int kLoads = BT * 8 / kNT;           // 16-byte chunks per thread per operand
+  constexpr int kMI = Geo::kMI, kNI = Geo::kNI;
+  // One LDS block: two operand stages during the K loop, then the output tile.
+  constexpr int kSt = BT + kEpc;                 // output staging row stride
+  constexpr int kOperand = 2 * 2 * BT * kLd, kStage = BT * kSt;
+  __shared__ __attribute__((aligned(16))) T smem[kOperand > kStage ? kOperand : kStage];
+  T (*sA)[BT][kLd] = reinterpret_cast<T (*)[BT][kLd]>(smem);
+  T (*sB)[BT][kLd] = reinterpret_cast<T (*)[BT][kLd]>(smem + 2 * BT * kLd);
 
   const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
   if (slot >= g.split->count[xcd]) return;
@@ -324,124 +345,207 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmArgs g) {
     lda = ldb = mm.s_pad;
     K = mm.s_pad;
   }
-  const int row0 = task.tm * kTile, col0 = task.tn * kTile;
+  const int row0 = task.tm * BT, col0 = task.tn * BT;
   Aop += row0 * lda;
   Bop += col0 * ldb;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
-  const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;
+  const int wm = (wave / Geo::kWavesN) * Geo::kWM, wn = (wave % Geo::kWavesN) * Geo::kWN;
   const int ld_row = tid >> 3, ld_ch = (tid & 7) * kEpc;
 
-  u32x4 ra[4], rb[4];
-  auto gload = [&](int k0) {
+  // Two register sets of staged global loads: while the MFMAs consume LDS
+  // stage k, the loads of stages k+1 and k+2 are in flight.
+  u32x4 ra0[kLoads], rb0[kLoads], ra1[kLoads], rb1[kLoads];
+  auto gload = [&](u32x4 (&ra)[kLoads], u32x4 (&rb)[kLoads], int k0) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int row = ld_row + 32 * q;
+    for (int q = 0; q < kLoads; ++q) {
+      const int row = ld_row + (kNT / 8) * q;
       ra[q] = *reinterpret_cast<const u32x4*>(Aop + row * lda + k0 + ld_ch);
       rb[q] = *reinterpret_cast<const u32x4*>(Bop + row * ldb + k0 + ld_ch);
     }
   };
-  auto sstore = [&](int buf) {
+  auto sstore = [&](const u32x4 (&ra)[kLoads], const u32x4 (&rb)[kLoads], int buf) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int row = ld_row + 32 * q;
+    for (int q = 0; q < kLoads; ++q) {
+      const int row = ld_row + (kNT / 8) * q;
       *reinterpret_cast<u32x4*>(&sA[buf][row][ld_ch]) = ra[q];
       *reinterpret_cast<u32x4*>(&sB[buf][row][ld_ch]) = rb[q];
     }
   };
 
-  f32x16 acc[2][2];
+  f32x16 acc[kMI][kNI];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < kMI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < kNI; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  const int nk = K / kBK;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * kBK);
+  auto compute = [&](int buf) {
 #pragma unroll
     for (int kk = 0; kk < kBK / M::kKStep; ++kk) {
       const int kc = kk * M::kKStep;
-      const typename M::Frag a0 = M::load(&sA[buf][wm + lr][kc], lk);
-      const typename M::Frag a1 = M::load(&sA[buf][wm + 32 + lr][kc], lk);
-      const typename M::Frag b0 = M::load(&sB[buf][wn + lr][kc], lk);
-      const typename M::Frag b1 = M::load(&sB[buf][wn + 32 + lr][kc], lk);
-      acc[0][0] = M::mma(a0, b0, acc[0][0]);
-      acc[0][1] = M::mma(a0, b1, acc[0][1]);
-      acc[1][0] = M::mma(a1, b0, acc[1][0]);
-      acc[1][1] = M::mma(a1, b1, acc[1][1]);
+      typename M::Frag af[kMI], bfr[kNI];
+#pragma unroll
+      for (int i = 0; i < kMI; ++i) af[i] = M::load(&sA[buf][wm + 32 * i + lr][kc], lk);
+#pragma unroll
+      for (int j = 0; j < kNI; ++j) bfr[j] = M::load(&sB[buf][wn + 32 * j + lr][kc], lk);
+#pragma unroll
+      for (int i = 0; i < kMI; ++i)
+#pragma unroll
+        for (int j = 0; j < kNI; ++j) acc[i][j] = M::mma(af[i], bfr[j], acc[i][j]);
     }
-    if (kt + 1 < nk) sstore(buf ^ 1);
+  };
+
+  // Every K here is a multiple of 128, so nk is even and >= 2. The loads of
+  // the steady-state loop are unconditional so that each LDS store waits only
+  // for its own register set (in-order vmcnt), never for the stage behind it.
+  const int nk = K / kBK;
+  gload(ra0, rb0, 0);
+  gload(ra1, rb1, kBK);
+  sstore(ra0, rb0, 0);
+  __syncthreads();
+  // sched_barrier keeps the compiler from sinking the loads below the MFMAs.
+  for (int kt = 0; kt + 2 < nk; kt += 2) {
+    gload(ra0, rb0, (kt + 2) * kBK);   // stage kt+2 -> set 0
+    __builtin_amdgcn_sched_barrier(0);
+    compute(0);                        // stage kt
+    __builtin_amdgcn_sched_barrier(0);
+    sstore(ra1, rb1, 1);               // stage kt+1
+    __syncthreads();
+    gload(ra1, rb1, (kt + 3) * kBK);   // stage kt+3 -> set 1
+    __builtin_amdgcn_sched_barrier(0);
+    compute(1);                        // stage kt+1
+    __builtin_amdgcn_sched_barrier(0);
+    sstore(ra0, rb0, 0);               // stage kt+2
     __syncthreads();
   }
+  compute(0);                          // stage nk-2
+  sstore(ra1, rb1, 1);                 // stage nk-1
+  __syncthreads();
+  compute(1);
 
-  // ---- epilogues -----------------------------------------------------------
+  // ---- epilogues ----------------------------------------------------------
+  // Results leave through LDS: each lane writes its values into the staging
+  // tile (row-major, or transposed with 8-byte writes), then the workgroup
+  // stores whole rows with coalesced 16-byte stores.
   const int64_t s_pad = mm.s_pad, l_pad = mm.l_pad;
+  T (*stage)[kSt] = reinterpret_cast<T (*)[kSt]>(smem);
+  constexpr int kRowChunks = BT * int(sizeof(T)) / 16;
+  auto flush = [&](T* dst, int64_t ld) {        // stage (BT x BT) -> dst rows
+    __syncthreads();
+#pragma unroll 4
+    for (int c = tid; c < BT * kRowChunks; c += kNT) {
+      const int r = c / kRowChunks, ch = (c % kRowChunks) * kEpc;
+      *reinterpret_cast<u32x4*>(dst + r * ld + ch) = *reinterpret_cast<const u32x4*>(&stage[r][ch]);
+    }
+    __syncthreads();
+  };
+  // v(mi, ni, q, e): value of local row wm + 32 mi + 8 q + 4 lk + e, local
+  // column wn + 32 ni + lr.
+  auto stage_rows = [&](auto&& val) {
+#pragma unroll
+    for (int mi = 0; mi < kMI; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < kNI; ++ni)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int r = wm + 32 * mi + 8 * q + 4 * lk, c = wn + 32 * ni + lr;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) stage[r + e][c] = to_elem<T>(val(mi, ni, q, e));
+        }
+  };
+  auto stage_cols = [&](auto&& val) {           // transposed: stage[col][row..row+3]
+#pragma unroll
+    for (int mi = 0; mi < kMI; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < kNI; ++ni)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int r = wm + 32 * mi + 8 * q + 4 * lk, c = wn + 32 * ni + lr;
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = val(mi, ni, q, e);
+          store4(&stage[c][r], v);
+        }
+  };
+  __syncthreads();                               // operand stages no longer read
+
   if (MODE == kGram || MODE == kPoly) {
     float alpha = 1.0f;
     if (MODE == kGram && g.first) {
       const float r = g.rscale[task.mat];
       alpha = r * r;
     }
-    T* out = at(MODE == kGram ? mm.off_a : mm.off_b);
-    const T* aold = at(mm.off_a);
-    const bool mirror = task.tm != task.tn;
+    if (MODE == kPoly) {
+      // B = b A + c A A: fold b A into the accumulators (A is symmetric, so
+      // A[R][C] is read as A[C][R..R+3] with one 8-byte load)
+      const T* aold = at(mm.off_a);
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+      for (int mi = 0; mi < kMI; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni)
+        for (int ni = 0; ni < kNI; ++ni)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int64_t R = row0 + wm + 32 * mi + 8 * q + 4 * lk;   // 4 rows R..R+3
-          const int64_t C = col0 + wn + 32 * ni + lr;
-          float v[4];
-          if (MODE == kGram) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = alpha * acc[mi][ni][4 * q + e];
-          } else {
+          for (int q = 0; q < 4; ++q) {
+            const int64_t R = row0 + wm + 32 * mi + 8 * q + 4 * lk;
+            const int64_t C = col0 + wn + 32 * ni + lr;
             float old[4];
-            load4(aold + C * s_pad + R, old);        // A is symmetric
+            load4(aold + C * s_pad + R, old);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = fmaf(g.b, old[e], g.c * acc[mi][ni][4 * q + e]);
+            for (int e = 0; e < 4; ++e)
+              acc[mi][ni][4 * q + e] = fmaf(g.b, old[e], g.c * acc[mi][ni][4 * q + e]);
           }
-#pragma unroll
-          for (int e = 0; e < 4; ++e) out[(R + e) * s_pad + C] = to_elem<T>(v[e]);
-          if (mirror) store4(out + C * s_pad + R, v);
-        }
+    }
+    T* out = at(MODE == kGram ? mm.off_a : mm.off_b);
+    auto val = [&](int mi, int ni, int q, int e) { return alpha * acc[mi][ni][4 * q + e]; };
+    stage_rows(val);
+    flush(out + row0 * s_pad + col0, s_pad);
+    if (task.tm != task.tn) {                    // mirror into the upper triangle
+      stage_cols(val);
+      flush(out + col0 * s_pad + row0, s_pad);
+    }
   } else {
     const float alpha = g.first ? g.rscale[task.mat] : 1.0f;
     const T* xt_cur = at(off_xt_cur);
-    T* x_dst = at(off_x_nxt);
-    T* xt_dst = at(off_xt_nxt);
+    // X' = alpha (a X + B X); X[R][C] is read from X^T[C][R..R+3]
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int mi = 0; mi < kMI; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni)
+      for (int ni = 0; ni < kNI; ++ni)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int64_t R = row0 + wm + 32 * mi + 8 * q + 4 * lk;   // short side
-          const int64_t C = col0 + wn + 32 * ni + lr;               // long side
-          float x[4], v[4];
+          const int64_t R = row0 + wm + 32 * mi + 8 * q + 4 * lk;
+          const int64_t C = col0 + wn + 32 * ni + lr;
+          float x[4];
           load4(xt_cur + C * s_pad + R, x);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = alpha * fmaf(g.a, x[e], acc[mi][ni][4 * q + e]);
-          if (!g.last) {
+          for (int e = 0; e < 4; ++e)
+            acc[mi][ni][4 * q + e] = alpha * fmaf(g.a, x[e], acc[mi][ni][4 * q + e]);
+        }
+    if (!g.last) {
+      auto val = [&](int mi, int ni, int q, int e) { return acc[mi][ni][4 * q + e]; };
+      stage_rows(val);
+      flush(at(off_x_nxt) + row0 * l_pad + col0, l_pad);
+      stage_cols(val);
+      flush(at(off_xt_nxt) + col0 * s_pad + row0, s_pad);
+    } else {
+      // last step: W <- W - lr (kappa O + wd W), or O = kappa X_K (NS hook);
+      // O is X_K, transposed back for tall matrices
 #pragma unroll
-            for (int e = 0; e < 4; ++e) x_dst[(R + e) * l_pad + C] = to_elem<T>(v[e]);
-            store4(xt_dst + C * s_pad + R, v);
-          } else if (C < mm.l) {
+      for (int mi = 0; mi < kMI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < kNI; ++ni)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int64_t R = row0 + wm + 32 * mi + 8 * q + 4 * lk;   // short side
+            const int64_t C = col0 + wn + 32 * ni + lr;               // long side
+            if (C >= mm.l) continue;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               if (R + e >= mm.s) break;
               const int64_t widx = mm.transposed ? C * mm.cols + (R + e) : (R + e) * mm.cols + C;
-              const float o = mm.kappa * v[e];
+              const float o = mm.kappa * acc[mi][ni][4 * q + e];
               if (g.store_o) {
                 mm.w[widx] = o;
               } else {
@@ -450,7 +554,7 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmArgs g) {
               }
             }
           }
-        }
+    }
   }
 }
 
@@ -517,16 +621,25 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
   a.c = l.c;
   a.lr = l.lr;
   a.wd = l.wd;
-  const dim3 grid(unsigned(l.max_count) * kXcds), block(256);
+  const dim3 grid(unsigned(l.max_count) * kXcds);
+#define LM_LAUNCH(T, MODE, BT) \
+  hipLaunchKernelGGL((gemm_kernel<T, MODE, BT>), grid, dim3(TileGeom<BT>::kThreads), 0, stream, a)
   if (l.fp32) {
-    if (mode == kGram) hipLaunchKernelGGL((gemm_kernel<float, kGram>), grid, block, 0, stream, a);
-    else if (mode == kPoly) hipLaunchKernelGGL((gemm_kernel<float, kPoly>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((gemm_kernel<float, kApply>), grid, block, 0, stream, a);
+    if (l.tile != 128) return hipErrorInvalidValue;
+    if (mode == kGram) LM_LAUNCH(float, kGram, 128);
+    else if (mode == kPoly) LM_LAUNCH(float, kPoly, 128);
+    else LM_LAUNCH(float, kApply, 128);
+  } else if (l.tile == 256) {
+    if (mode == kGram) LM_LAUNCH(bf16, kGram, 256);
+    else if (mode == kPoly) LM_LAUNCH(bf16, kPoly, 256);
+    else LM_LAUNCH(bf16, kApply, 256);
   } else {
-    if (mode == kGram) hipLaunchKernelGGL((gemm_kernel<bf16, kGram>), grid, block, 0, stream, a);
-    else if (mode == kPoly) hipLaunchKernelGGL((gemm_kernel<bf16, kPoly>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((gemm_kernel<bf16, kApply>), grid, block, 0, stream, a);
+    if (l.tile != 128) return hipErrorInvalidValue;
+    if (mode == kGram) LM_LAUNCH(bf16, kGram, 128);
+    else if (mode == kPoly) LM_LAUNCH(bf16, kPoly, 128);
+    else LM_LAUNCH(bf16, kApply, 128);
   }
+#undef LM_LAUNCH
   return hipGetLastError();
 }
 

@@ -9,7 +9,10 @@
 namespace lm {
 
 // Tile sizes of the Newton-Schulz GEMMs and of the Muon preparation pass.
-constexpr int kTile = 128;       // MFMA output tile (both dims); buffers padded to it
+constexpr int kTileSmall = 128;  // MFMA output tile edges; fp32 buffers are padded
+constexpr int kTileBig = 256;    // to 128, bf16 buffers to 256
+constexpr int kMinBigTiles = 512;  // a bf16 Gram / polynomial stage uses 256-tiles
+                                   // only with at least this many (two per CU)
 constexpr int kPrepTile = 64;    // square tile of the preparation / transpose pass
 constexpr int kLionBlockElems = 4096;  // elements per Lion workgroup (256 x float4 x 4)
 constexpr int kXcds = 8;         // accelerator complex dies of one MI355X
@@ -33,7 +36,7 @@ struct MuonMat {
   float* m;          // M, or null (NS hook: no momentum)
   int64_t rows, cols;      // m, n of the original tensor
   int32_t s, l;            // short and long side
-  int32_t s_pad, l_pad;    // padded to kTile
+  int32_t s_pad, l_pad;    // padded to 128 (fp32) or 256 (bf16)
   int32_t transposed;      // rows > cols: iterate on G^T
   int32_t vec_ok;          // 16-byte vector access legal on w, g, m rows
   int32_t fp32;            // 1: fp32 Newton-Schulz buffers, 0: bf16
@@ -51,7 +54,7 @@ struct MuonMat {
 // One output tile of one Newton-Schulz GEMM.
 struct GemmTask {
   int32_t mat;
-  int16_t tm, tn;          // tile row / column (units of kTile)
+  int16_t tm, tn;          // tile row / column (units of the launch's tile edge)
 };
 
 // Per-launch partition of a task list into one contiguous segment per XCD.

@@ -168,17 +168,18 @@ Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec
     mm.cols = t.cols;
     mm.transposed = t.rows > t.cols ? 1 : 0;
     const int64_t s = std::min(t.rows, t.cols), l = std::max(t.rows, t.cols);
-    if (s > kMaxShortSide || round_up(s, kTile) * round_up(l, kTile) > kMaxMatrixElems) {
+    if (s > kMaxShortSide || round_up(s, kTileBig) * round_up(l, kTileBig) > kMaxMatrixElems) {
       *err = "tensor " + std::to_string(i) + ": matrix too large for the Newton-Schulz kernels";
       return Status::kUnsupported;
     }
     mm.s = int32_t(s);
     mm.l = int32_t(l);
-    mm.s_pad = int32_t(round_up(s, kTile));
-    mm.l_pad = int32_t(round_up(l, kTile));
+    mm.fp32 = prec.fp32_for(s) ? 1 : 0;
+    const int64_t pad = mm.fp32 ? kTileSmall : kTileBig;
+    mm.s_pad = int32_t(round_up(s, pad));
+    mm.l_pad = int32_t(round_up(l, pad));
     // vector path on the original rows needs 16-byte aligned rows
     mm.vec_ok = (vec_ok && (t.cols % 4) == 0) ? 1 : 0;
-    mm.fp32 = prec.fp32_for(s) ? 1 : 0;
     const int64_t eb = mm.fp32 ? 4 : 2;
     const int64_t sl = int64_t(mm.s_pad) * mm.l_pad * eb, ss = int64_t(mm.s_pad) * mm.s_pad * eb;
     mm.off_x[0] = ns_off;  ns_off += sl;
@@ -206,12 +207,24 @@ Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec
 
   // GEMM work lists in canonical order (matrix, then tiles), cost = inner
   // dimension, one list per Newton-Schulz precision.
+  // bf16: apply on 256-tiles; Gram and polynomial (s x s outputs, lower
+  // triangle) on 256-tiles only when there are enough of them. fp32: 128.
+  int64_t big_sym = 0;
+  for (const MuonMat& mm : p->mats) {
+    if (mm.fp32) continue;
+    const int64_t ts = mm.s_pad / kTileBig;
+    big_sym += ts * (ts + 1) / 2;
+  }
+  const int32_t sym_tile = big_sym >= kMinBigTiles ? kTileBig : kTileSmall;
+  p->tile[0][0] = p->tile[0][1] = sym_tile;
+  p->tile[0][2] = kTileBig;
   for (int pr = 0; pr < 2; ++pr) {
     std::vector<int64_t> cg, cp, ca;
+    const int t_sym = p->tile[pr][0], t_app = p->tile[pr][2];
     for (int32_t mi = 0; mi < int32_t(p->mats.size()); ++mi) {
       const MuonMat& mm = p->mats[mi];
       if (mm.fp32 != pr) continue;
-      const int ts = mm.s_pad / kTile, tl = mm.l_pad / kTile;
+      const int ts = mm.s_pad / t_sym;
       for (int tm = 0; tm < ts; ++tm) {
         for (int tn = 0; tn <= tm; ++tn) {      // symmetric: lower triangle
           p->gram[pr].push_back({mi, int16_t(tm), int16_t(tn)});
@@ -220,8 +233,9 @@ Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec
           cp.push_back(mm.s_pad);
         }
       }
-      for (int tn = 0; tn < tl; ++tn) {
-        for (int tm = 0; tm < ts; ++tm) {
+      const int ts_a = mm.s_pad / t_app, tl_a = mm.l_pad / t_app;
+      for (int tn = 0; tn < tl_a; ++tn) {
+        for (int tm = 0; tm < ts_a; ++tm) {
           p->apply[pr].push_back({mi, int16_t(tm), int16_t(tn)});
           ca.push_back(mm.s_pad);
         }

@@ -61,6 +61,7 @@ struct Plan {
   // grouped per XCD segment
   std::vector<GemmTask> gram[2], poly[2], apply[2];
   XcdSplit gram_split[2]{}, poly_split[2]{}, apply_split[2]{};
+  int32_t tile[2][3] = {{kTileBig, kTileBig, kTileBig}, {kTileSmall, kTileSmall, kTileSmall}};
   int64_t muon_elements = 0;
   int32_t n_shape_classes = 0;
 

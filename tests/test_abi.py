@@ -117,14 +117,33 @@ def test_plan_info_vectors_and_lion_only_never_muon(lib):
     info = lm.lionmuon_plan_info(specs, t=0, P=1)
     assert info["n_tensors"] == 4            # the empty tensor is skipped
     assert info["n_muon"] == 1 and info["n_lion"] == 3
+    # 64 x 96 runs bf16 (short side >= 64): padded to 256; the symmetric stages
+    # use 128-tiles (too few 256-tiles), apply one 256-tile
+    assert info["gram_tiles"] == 3 and info["poly_tiles"] == 3 and info["apply_tiles"] == 1
+    info = lm.lionmuon_plan_info(specs, t=0, P=1, cfg=lm.config(ns_bf16_min_side=65))
     assert info["gram_tiles"] == 1 and info["poly_tiles"] == 1 and info["apply_tiles"] == 1
 
 
 def test_plan_info_tiles_span_ragged_shapes(lib):
-    info = lm.lionmuon_plan_info([(300, 520, False), (520, 300, False)], t=0, P=1)
-    # s = 300 -> 3 tiles, l = 520 -> 5 tiles; lower triangle 6; apply 15
+    specs = [(300, 520, False), (520, 300, False)]
+    # fp32: padded to 128, s -> 3 tiles, l -> 5 tiles; lower triangle 6; apply 15
+    info = lm.lionmuon_plan_info(specs, t=0, P=1, cfg=lm.config(ns_precision="fp32"))
     assert info["n_shape_classes"] == 1
     assert info["gram_tiles"] == 12 and info["poly_tiles"] == 12 and info["apply_tiles"] == 30
+    # bf16: padded to 256 (512 x 768); symmetric stages on 128-tiles (4 -> 10
+    # lower), apply on 256-tiles (2 x 3)
+    info = lm.lionmuon_plan_info(specs, t=0, P=1)
+    assert info["gram_tiles"] == 20 and info["poly_tiles"] == 20 and info["apply_tiles"] == 12
+
+
+@pytest.mark.parametrize("name,sym_tiles,apply_tiles", [
+    ("gpt2-124m", 48 * 21, 12 * 27 + 12 * 9 + 24 * 36),   # 128-tiles for Gram/poly
+    ("gpt2-355m", 96 * 10, 24 * 48 + 24 * 16 + 48 * 64),  # 256-tiles everywhere
+    ("gpt2-720m", 144 * 15, 36 * 75 + 36 * 25 + 72 * 100)])
+def test_plan_tile_choice_for_benchmark_sets(lib, name, sym_tiles, apply_tiles):
+    info = lm.lionmuon_plan_info(_specs(workloads.get(name)), t=0, P=1)
+    assert info["gram_tiles"] == sym_tiles and info["poly_tiles"] == sym_tiles
+    assert info["apply_tiles"] == apply_tiles
 
 
 def test_workspace_bytes_matches_plan_info(lib):
