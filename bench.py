@@ -50,6 +50,89 @@ def load_traffic(workload, kernel):
     return None if k is None else k.get("bytes_per_launch")
 
 
+PHASE_OF_KERNEL = (("lion_kernel", "lion"), ("prep_kernel", "prep"), ("norm_kernel", "norm"),
+                   ("ns_gram_kernel", "gram"), ("ns_poly_kernel", "poly"),
+                   ("ns_apply_kernel", "apply"))
+
+
+def phase_of(kernel_name):
+    """Phase name of a library kernel from its (mangled or demangled) name."""
+    for key, phase in PHASE_OF_KERNEL:
+        if key in kernel_name:
+            return phase
+    return None
+
+
+def _counter_means(csv_path, counter):
+    import collections
+    import csv
+    vals = collections.defaultdict(list)
+    with open(csv_path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] == counter:
+                vals[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+    return vals
+
+
+def pmc_summary(wl_name, fetch_csv, write_csv, calib_fetch_csv, calib_write_csv, calib_mib,
+                commands):
+    """Per-launch HBM traffic of each library kernel from rocprofv3 FETCH_SIZE
+    and WRITE_SIZE (KiB per dispatch), each scaled by what the same counter
+    reads for a plain device copy of a known size."""
+    copy_bytes = calib_mib * (1 << 20)
+    cf = [v for k, vs in _counter_means(calib_fetch_csv, "FETCH_SIZE").items() for v in vs
+          if "copy" in k.lower() or "elementwise" in k.lower()]
+    cw = [v for k, vs in _counter_means(calib_write_csv, "WRITE_SIZE").items() for v in vs
+          if "copy" in k.lower() or "elementwise" in k.lower()]
+    f_scale = copy_bytes / (sum(cf) / len(cf) * 1024.0)
+    w_scale = copy_bytes / (sum(cw) / len(cw) * 1024.0)
+    fetch = _counter_means(fetch_csv, "FETCH_SIZE")
+    write = _counter_means(write_csv, "WRITE_SIZE")
+    kernels = {}
+    for name in set(fetch) | set(write):
+        ph = phase_of(name)
+        if ph is None:
+            continue
+        fv, wv = fetch.get(name, []), write.get(name, [])
+        fb = sum(fv) / len(fv) * 1024.0 * f_scale if fv else 0.0
+        wb = sum(wv) / len(wv) * 1024.0 * w_scale if wv else 0.0
+        k = kernels.setdefault(ph, {"fetch_bytes": 0.0, "write_bytes": 0.0, "launch_kinds": 0})
+        k["fetch_bytes"] += fb
+        k["write_bytes"] += wb
+        k["launch_kinds"] += 1
+    for k in kernels.values():
+        k["fetch_bytes"] /= k["launch_kinds"]
+        k["write_bytes"] /= k["launch_kinds"]
+        k["bytes_per_launch"] = k["fetch_bytes"] + k["write_bytes"]
+        del k["launch_kinds"]
+    out = {"workload": wl_name, "kernel_source_sha256_16": kernel_hash(),
+           "fetch_scale": f_scale, "write_scale": w_scale,
+           "calibration": f"plain device copy of {calib_mib} MiB (torch copy_)",
+           "commands": commands, "kernels": kernels}
+    path = os.path.join(TRAFFIC_DIR, f"traffic_{wl_name}.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    return path
+
+
+def trace_summary(wl_name, stats_csv, command):
+    """Text summary of a rocprofv3 --kernel-trace --stats run."""
+    import csv
+    rows = list(csv.DictReader(open(stats_csv)))
+    lines = [f"# Kernel trace: {wl_name}", "", f"Command: `{command}`", "",
+             "| kernel | phase | calls | avg us | total us | % |", "|---|---|---|---|---|---|"]
+    for r in rows:
+        name = r["Name"]
+        ph = phase_of(name) or "-"
+        short = name if len(name) < 70 else name[:67] + "..."
+        lines.append(f"| `{short}` | {ph} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                     f"{float(r['TotalDurationNs']) / 1e3:.1f} | {float(r['Percentage']):.2f} |")
+    path = os.path.join(TRAFFIC_DIR, f"kernel_trace_{wl_name}.md")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    return path
+
+
 def ns_flops_per_launch(wl):
     gram = poly = apply = 0.0
     for t in wl.tensors:
@@ -122,7 +205,20 @@ def main():
                     help="time without per-launch events (no roofline object)")
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                     help="only run 4 plain device copies of MIB MiB (counter calibration)")
+    ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CALIB_FETCH_CSV",
+                                                        "CALIB_WRITE_CSV"),
+                    help="write profiles/traffic_<workload>.json from rocprofv3 counter CSVs")
+    ap.add_argument("--trace-summary", metavar="KERNEL_STATS_CSV",
+                    help="write profiles/kernel_trace_<workload>.md from a rocprofv3 stats CSV")
+    ap.add_argument("--command", default="", help="profiling command recorded in summaries")
     args = ap.parse_args()
+    if args.pmc_summary:
+        print(pmc_summary(args.workload, *args.pmc_summary, calib_mib=1024,
+                          commands=args.command))
+        return
+    if args.trace_summary:
+        print(trace_summary(args.workload, args.trace_summary, args.command))
+        return
     if args.calib_copy:
         import torch
         n = args.calib_copy * (1 << 20) // 4
@@ -239,8 +335,8 @@ def main():
         dom = max((p for p in phases if phases[p]["launches"]), key=lambda p: phases[p]["ms"])
         d = ph[dom]
         kernel_names = {"lion": "lion_kernel", "prep": "prep_kernel", "norm": "norm_kernel",
-                        "gram": "gemm_kernel<bf16, Gram>", "poly": "gemm_kernel<bf16, Poly>",
-                        "apply": "gemm_kernel<bf16, Apply>"}
+                        "gram": "ns_gram_kernel<bf16>", "poly": "ns_poly_kernel<bf16>",
+                        "apply": "ns_apply_kernel<bf16>"}
         if dom in flops:
             roof = {"kernel": kernel_names[dom], "bound": "mfma", "achieved": d["tflops"],
                     "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": d["frac_bf16_peak"]}

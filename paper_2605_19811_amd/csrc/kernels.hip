@@ -7,7 +7,7 @@
 //                iteration orientation X (rows <= cols) and its transpose, and
 //                a per-tile partial sum of Ghat^2 (wave shuffles + LDS).
 //  norm_kernel   fixed-order reduction of the partials -> 1/(||Ghat||_F + eps).
-//  gemm_kernel   the Newton-Schulz products on MFMA with fp32 accumulation:
+//  ns_*_kernel   the Newton-Schulz products on MFMA with fp32 accumulation:
 //                Gram A = X X^T and polynomial B = b A + c A A on the lower
 //                triangle of tiles (mirrored on store), apply X' = a X + B X
 //                with the W update fused into the last step's epilogue.
@@ -300,7 +300,7 @@ struct GemmArgs {
 };
 
 template <typename T, int MODE, int BT>
-__global__ __launch_bounds__(TileGeom<BT>::kThreads) void gemm_kernel(GemmArgs g) {
+__device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   using M = Mfma<T>;
   using Geo = TileGeom<BT>;
   constexpr int kBK = M::kBK;
@@ -530,32 +530,86 @@ __global__ __launch_bounds__(TileGeom<BT>::kThreads) void gemm_kernel(GemmArgs g
       stage_cols(val);
       flush(at(off_xt_nxt) + col0 * s_pad + row0, s_pad);
     } else {
-      // last step: W <- W - lr (kappa O + wd W), or O = kappa X_K (NS hook);
-      // O is X_K, transposed back for tall matrices
+      // last step: W <- W - lr (kappa O + wd W), or O = kappa X_K (NS hook).
+      // O is X_K, transposed back for tall matrices. The fp32 O tile goes
+      // through LDS in two halves of W rows so that W is read and written in
+      // whole 16-byte pieces of its rows.
+      constexpr int kHalf = BT / 2, kFs = BT + 4;
+      float (*fst)[kFs] = reinterpret_cast<float (*)[kFs]>(smem);
+      const bool tall = mm.transposed != 0;
+      const int64_t wrow0 = tall ? col0 : row0, wcol0 = tall ? row0 : col0;
+      const int64_t wrows = mm.rows, wcols = mm.cols;
+      const float kappa = mm.kappa;
 #pragma unroll
-      for (int mi = 0; mi < kMI; ++mi)
+      for (int h = 0; h < 2; ++h) {
 #pragma unroll
-        for (int ni = 0; ni < kNI; ++ni)
+        for (int mi = 0; mi < kMI; ++mi)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int64_t R = row0 + wm + 32 * mi + 8 * q + 4 * lk;   // short side
-            const int64_t C = col0 + wn + 32 * ni + lr;               // long side
-            if (C >= mm.l) continue;
+          for (int ni = 0; ni < kNI; ++ni)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int r = wm + 32 * mi + 8 * q + 4 * lk, c = wn + 32 * ni + lr;
+              if (!tall) {
+                if (wm / kHalf == h) {
+#pragma unroll
+                  for (int e = 0; e < 4; ++e) fst[r - h * kHalf + e][c] = kappa * acc[mi][ni][4 * q + e];
+                }
+              } else if ((wn + 32 * ni) / kHalf == h) {
+                float o[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[e] = kappa * acc[mi][ni][4 * q + e];
+                store4(&fst[c - h * kHalf][r], o);
+              }
+            }
+        __syncthreads();
+        for (int idx = tid; idx < kHalf * (BT / 4); idx += kNT) {
+          const int i = idx / (BT / 4), j = (idx % (BT / 4)) * 4;
+          const int64_t gr = wrow0 + h * kHalf + i, gc = wcol0 + j;
+          if (gr >= wrows || gc >= wcols) continue;
+          float* wp = mm.w + gr * wcols + gc;
+          float o[4];
+          load4(&fst[i][j], o);
+          if (mm.vec_ok && gc + 3 < wcols) {
+            float w[4];
+            if (g.store_o) {
+              store4(wp, o);
+            } else {
+              load4(wp, w);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) w[e] = fmaf(-g.lr, fmaf(g.wd, w[e], o[e]), w[e]);
+              store4(wp, w);
+            }
+          } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              if (R + e >= mm.s) break;
-              const int64_t widx = mm.transposed ? C * mm.cols + (R + e) : (R + e) * mm.cols + C;
-              const float o = mm.kappa * acc[mi][ni][4 * q + e];
+              if (gc + e >= wcols) break;
               if (g.store_o) {
-                mm.w[widx] = o;
+                wp[e] = o[e];
               } else {
-                const float w = mm.w[widx];
-                mm.w[widx] = fmaf(-g.lr, fmaf(g.wd, w, o), w);
+                const float w = wp[e];
+                wp[e] = fmaf(-g.lr, fmaf(g.wd, w, o[e]), w);
               }
             }
           }
+        }
+        __syncthreads();
+      }
     }
   }
+}
+
+// One entry point per Newton-Schulz product, so profiles name each stage.
+template <typename T, int BT>
+__global__ __launch_bounds__(TileGeom<BT>::kThreads) void ns_gram_kernel(GemmArgs g) {
+  gemm_body<T, kGram, BT>(g);
+}
+template <typename T, int BT>
+__global__ __launch_bounds__(TileGeom<BT>::kThreads) void ns_poly_kernel(GemmArgs g) {
+  gemm_body<T, kPoly, BT>(g);
+}
+template <typename T, int BT>
+__global__ __launch_bounds__(TileGeom<BT>::kThreads) void ns_apply_kernel(GemmArgs g) {
+  gemm_body<T, kApply, BT>(g);
 }
 
 }  // namespace
@@ -622,23 +676,24 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
   a.lr = l.lr;
   a.wd = l.wd;
   const dim3 grid(unsigned(l.max_count) * kXcds);
-#define LM_LAUNCH(T, MODE, BT) \
-  hipLaunchKernelGGL((gemm_kernel<T, MODE, BT>), grid, dim3(TileGeom<BT>::kThreads), 0, stream, a)
+#define LM_LAUNCH(KERNEL, T, BT) \
+  hipLaunchKernelGGL((KERNEL<T, BT>), grid, dim3(TileGeom<BT>::kThreads), 0, stream, a)
+#define LM_LAUNCH_MODE(T, BT)                                   \
+  do {                                                          \
+    if (mode == kGram) LM_LAUNCH(ns_gram_kernel, T, BT);        \
+    else if (mode == kPoly) LM_LAUNCH(ns_poly_kernel, T, BT);   \
+    else LM_LAUNCH(ns_apply_kernel, T, BT);                     \
+  } while (0)
   if (l.fp32) {
     if (l.tile != 128) return hipErrorInvalidValue;
-    if (mode == kGram) LM_LAUNCH(float, kGram, 128);
-    else if (mode == kPoly) LM_LAUNCH(float, kPoly, 128);
-    else LM_LAUNCH(float, kApply, 128);
+    LM_LAUNCH_MODE(float, 128);
   } else if (l.tile == 256) {
-    if (mode == kGram) LM_LAUNCH(bf16, kGram, 256);
-    else if (mode == kPoly) LM_LAUNCH(bf16, kPoly, 256);
-    else LM_LAUNCH(bf16, kApply, 256);
+    LM_LAUNCH_MODE(bf16, 256);
   } else {
     if (l.tile != 128) return hipErrorInvalidValue;
-    if (mode == kGram) LM_LAUNCH(bf16, kGram, 128);
-    else if (mode == kPoly) LM_LAUNCH(bf16, kPoly, 128);
-    else LM_LAUNCH(bf16, kApply, 128);
+    LM_LAUNCH_MODE(bf16, 128);
   }
+#undef LM_LAUNCH_MODE
 #undef LM_LAUNCH
   return hipGetLastError();
 }
