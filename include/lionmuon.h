@@ -16,10 +16,10 @@
  *
  * NS_K is K steps of the odd quintic Newton-Schulz iteration towards the
  * matrix sign msign(X) = U V^T (Section 2, "Spectral methods" and
- * "Approximating the matrix sign"; K_NS = 5 in Table 4):
+ * "Approximating the matrix sign"; K_NS = 5 in Table 3):
  *   X0 = Ghat / (||Ghat||_F + eps), iterated in the orientation with
  *   rows <= cols; each step A = X X^T, B = b*A + c*A A, X <- a*X + B X.
- * kappa is 1 (Algorithm 1) or 0.2*sqrt(max(m, n)) (Table 4 "NS scaling").
+ * kappa is 1 (Algorithm 1) or 0.2*sqrt(max(m, n)) (Table 3 "NS scaling").
  *
  * Conventions shared by every entry point:
  *  - Pointer arrays (params, grads, momentum, shapes) live in HOST memory;
@@ -72,7 +72,7 @@ enum { LM_NS_BF16 = 0,   /* bf16 operands on MFMA, fp32 accumulation, for every
 
 /* Output scaling kappa of the Muon direction. */
 enum { LM_NS_SCALE_NONE = 0,    /* kappa = 1 (Algorithm 1)                        */
-       LM_NS_SCALE_RMS02 = 1 }; /* kappa = 0.2*sqrt(max(rows, cols)) (Table 4)    */
+       LM_NS_SCALE_RMS02 = 1 }; /* kappa = 0.2*sqrt(max(rows, cols)) (Table 3)    */
 
 /* Shape of one tensor: rows x cols, row-major; rows = 1 for a vector.
  * rows = 0 or cols = 0 is an empty tensor (skipped). */
@@ -89,7 +89,7 @@ typedef struct lm_shape {
  * double before rounding). */
 typedef struct lm_config {
   uint32_t struct_size;     /* sizeof(lm_config)                                 */
-  int32_t ns_steps;         /* K_NS in [1, 64], default 5 (Table 4)              */
+  int32_t ns_steps;         /* K_NS in [1, 64], default 5 (Table 3)              */
   double ns_a, ns_b, ns_c;  /* odd polynomial a x + b x^3 + c x^5,
                                default (3.4445, -4.7750, 2.0315)                  */
   double ns_eps;            /* Frobenius guard eps >= 0, default 1e-7            */

@@ -17,10 +17,10 @@ Spectral and Sign Descent for Efficient Training"):
   odd-polynomial Newton-Schulz iteration.
 * Section 3, "Implementation notes": one momentum buffer per parameter; 1-D
   parameters do not take the spectral branch.
-* Table 4 (Appendix, full experimental setup): K_NS = 5 and the optional NS
+* Table 3 (Appendix D, full experimental configuration): K_NS = 5 and the optional NS
   output scaling 0.2*sqrt(max(m, n)).
 
-Readings where the paper is silent (each listed in the design doc):
+Readings where the paper is silent:
 
 * The quintic coefficients (a, b, c) = (3.4445, -4.7750, 2.0315) are the ones
   published with Muon (the paper cites it as the source of the NS step); the
@@ -48,11 +48,11 @@ QUINTIC = (3.4445, -4.7750, 2.0315)
 # Classical cubic Newton-Schulz p(x) = 1.5*x - 0.5*x^3 (converges to U V^T).
 CUBIC = (1.5, -0.5, 0.0)
 
-NS_STEPS = 5          # K_NS, Table 4
+NS_STEPS = 5          # K_NS, Table 3
 NS_EPS = 1e-7         # Frobenius pre-normalisation guard (reading)
 
 SCALE_NONE = 0        # Algorithm 1 uses NS output as is
-SCALE_RMS02 = 1       # Table 4: NS output times 0.2*sqrt(max(m, n))
+SCALE_RMS02 = 1       # Table 3: NS output times 0.2*sqrt(max(m, n))
 
 
 def is_muon_step(t: int, P: int) -> bool:
@@ -73,7 +73,7 @@ def elementwise_sign(x: np.ndarray) -> np.ndarray:
 
 
 def ns_output_scale(m: int, n: int, scale_mode: int) -> float:
-    """Optional NS output scaling of Table 4 (0.2*sqrt(max(m, n)))."""
+    """Optional NS output scaling of Table 3 (0.2*sqrt(max(m, n)))."""
     if scale_mode == SCALE_NONE:
         return 1.0
     if scale_mode == SCALE_RMS02:

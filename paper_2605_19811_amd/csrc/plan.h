@@ -81,7 +81,7 @@ Status validate_scalars(int64_t t, int32_t P, double beta1, double beta2, double
 Status validate_tensors(const TensorIn* x, int32_t n, std::string* err);
 
 // Build the plan for a Lion step (muon_step = false) or a Muon step;
-// kappa_rms02 selects Table 4 output scaling.
+// kappa_rms02 selects Table 3 output scaling.
 Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec,
                   bool kappa_rms02, Plan* out, std::string* err);
 

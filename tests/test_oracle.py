@@ -57,7 +57,7 @@ def test_quintic_coefficients_match_published_values():
     assert oracle.QUINTIC == (g["a"], g["b"], g["c"])
     cub = g["cubic_textbook"]
     assert oracle.CUBIC == (cub["a"], cub["b"], cub["c"])
-    assert oracle.NS_STEPS == 5  # Table 4
+    assert oracle.NS_STEPS == 5  # Table 3
 
 
 @pytest.mark.parametrize("shape", [(2, 3), (3, 2), (5, 7), (7, 5), (32, 48),
