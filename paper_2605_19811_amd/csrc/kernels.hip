@@ -8,9 +8,10 @@
 //                a per-tile partial sum of Ghat^2 (wave shuffles + LDS).
 //  norm_kernel   fixed-order reduction of the partials -> 1/(||Ghat||_F + eps).
 //  ns_*_kernel   the Newton-Schulz products on MFMA with fp32 accumulation:
-//                Gram A = X X^T and polynomial B = b A + c A A on the lower
-//                triangle of tiles (mirrored on store), apply X' = a X + B X
-//                with the W update fused into the last step's epilogue.
+//                Gram A = X X^T and polynomial B' = a I + b A + c A A on the
+//                lower triangle of tiles (mirrored on store), then apply
+//                X' = B' X (= a X + (b A + c A A) X) with the W update fused
+//                into the last step's epilogue.
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -479,22 +480,25 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
       alpha = r * r;
     }
     if (MODE == kPoly) {
-      // B = b A + c A A: fold b A into the accumulators (A is symmetric, so
-      // A[R][C] is read as A[C][R..R+3] with one 8-byte load)
+      // B' = a I + b A + c A A (the a X term of the apply step folded into B;
+      // A is symmetric, so A[R][C] is read as A[C][R..R+3] with one 8-byte load)
       const T* aold = at(mm.off_a);
+      const bool diag = task.tm == task.tn;
 #pragma unroll
       for (int mi = 0; mi < kMI; ++mi)
 #pragma unroll
         for (int ni = 0; ni < kNI; ++ni)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int64_t R = row0 + wm + 32 * mi + 8 * q + 4 * lk;
-            const int64_t C = col0 + wn + 32 * ni + lr;
+            const int r = wm + 32 * mi + 8 * q + 4 * lk, c = wn + 32 * ni + lr;
             float old[4];
-            load4(aold + C * s_pad + R, old);
+            load4(aold + int64_t(col0 + c) * s_pad + row0 + r, old);
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-              acc[mi][ni][4 * q + e] = fmaf(g.b, old[e], g.c * acc[mi][ni][4 * q + e]);
+            for (int e = 0; e < 4; ++e) {
+              float v = fmaf(g.b, old[e], g.c * acc[mi][ni][4 * q + e]);
+              if (diag && r + e == c) v += g.a;
+              acc[mi][ni][4 * q + e] = v;
+            }
           }
     }
     T* out = at(MODE == kGram ? mm.off_a : mm.off_b);
@@ -506,23 +510,14 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
       flush(out + col0 * s_pad + row0, s_pad);
     }
   } else {
+    // X' = alpha B' X with B' = a I + b A + c A A from the polynomial step
     const float alpha = g.first ? g.rscale[task.mat] : 1.0f;
-    const T* xt_cur = at(off_xt_cur);
-    // X' = alpha (a X + B X); X[R][C] is read from X^T[C][R..R+3]
 #pragma unroll
     for (int mi = 0; mi < kMI; ++mi)
 #pragma unroll
       for (int ni = 0; ni < kNI; ++ni)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int64_t R = row0 + wm + 32 * mi + 8 * q + 4 * lk;
-          const int64_t C = col0 + wn + 32 * ni + lr;
-          float x[4];
-          load4(xt_cur + C * s_pad + R, x);
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            acc[mi][ni][4 * q + e] = alpha * fmaf(g.a, x[e], acc[mi][ni][4 * q + e]);
-        }
+        for (int r = 0; r < 16; ++r) acc[mi][ni][r] *= alpha;
     if (!g.last) {
       auto val = [&](int mi, int ni, int q, int e) { return acc[mi][ni][4 * q + e]; };
       stage_rows(val);

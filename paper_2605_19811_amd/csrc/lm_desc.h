@@ -44,7 +44,7 @@ struct MuonMat {
   int64_t off_x[2];        // X  (s_pad x l_pad), ping-pong
   int64_t off_xt[2];       // X^T (l_pad x s_pad), ping-pong
   int64_t off_a;           // A = X X^T (s_pad x s_pad)
-  int64_t off_b;           // B = b A + c A A (s_pad x s_pad)
+  int64_t off_b;           // B' = a I + b A + c A A (s_pad x s_pad)
   int32_t prep_first;      // first preparation tile of this matrix
   int32_t prep_tiles_n;    // preparation tiles along the original columns
   int32_t prep_count;      // preparation tiles of this matrix
