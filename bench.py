@@ -80,10 +80,11 @@ def pmc_summary(wl_name, fetch_csv, write_csv, calib_fetch_csv, calib_write_csv,
     and WRITE_SIZE (KiB per dispatch), each scaled by what the same counter
     reads for a plain device copy of a known size."""
     copy_bytes = calib_mib * (1 << 20)
+    # only the copy kernel itself (the buffer's initial fill kernel reads nothing)
     cf = [v for k, vs in _counter_means(calib_fetch_csv, "FETCH_SIZE").items() for v in vs
-          if "copy" in k.lower() or "elementwise" in k.lower()]
+          if "copy" in k.lower()]
     cw = [v for k, vs in _counter_means(calib_write_csv, "WRITE_SIZE").items() for v in vs
-          if "copy" in k.lower() or "elementwise" in k.lower()]
+          if "copy" in k.lower()]
     f_scale = copy_bytes / (sum(cf) / len(cf) * 1024.0)
     w_scale = copy_bytes / (sum(cw) / len(cw) * 1024.0)
     fetch = _counter_means(fetch_csv, "FETCH_SIZE")

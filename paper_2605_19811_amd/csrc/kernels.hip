@@ -249,9 +249,11 @@ __global__ __launch_bounds__(256) void norm_kernel(PrepArgs a) {
 // Newton-Schulz GEMMs
 // ---------------------------------------------------------------------------
 // C[BT x BT] = sum_k Aop[row0 + i][k] * Bop[col0 + j][k]: both operands are
-// K-contiguous ("NT"), staged through LDS 128 bytes of K per row per stage,
-// double buffered via registers (the next stage's global loads are in flight
-// while the current stage feeds the MFMAs).
+// K-contiguous ("NT"). K is staged through LDS 128 bytes per row at a time by
+// direct global->LDS loads (no register staging), double buffered: the loads
+// of stage k+1 are in flight while stage k feeds the MFMAs. Rows are
+// unpadded; their eight 16-byte chunks are XOR-swizzled by row so that the
+// MFMA fragment reads are bank-conflict free.
 //   BT = 256: 8 waves (2 x 4), each a 128 x 64 sub-tile of 4 x 2 MFMA 32x32
 //             blocks (32 B of operand loads per CU-clock at full MFMA rate);
 //   BT = 128: 4 waves (2 x 2), each a 64 x 64 sub-tile of 2 x 2 blocks, for
@@ -306,7 +308,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   using Geo = TileGeom<BT>;
   constexpr int kBK = M::kBK;
   constexpr int kEpc = 16 / sizeof(T);           // elements per 16-byte chunk
-  constexpr int kLd = kBK + kEpc;                // LDS row stride: 144 bytes
+  constexpr int kLd = kBK;                       // LDS row: 128 bytes, chunks XOR-swizzled
   constexpr int kNT = Geo::kThreads;
   constexpr int kLoads = BT * 8 / kNT;           // 16-byte chunks per thread per operand
   constexpr int kMI = Geo::kMI, kNI = Geo::kNI;
@@ -355,23 +357,18 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   const int wm = (wave / Geo::kWavesN) * Geo::kWM, wn = (wave % Geo::kWavesN) * Geo::kWN;
   const int ld_row = tid >> 3, ld_ch = (tid & 7) * kEpc;
 
-  // Two register sets of staged global loads: while the MFMAs consume LDS
-  // stage k, the loads of stages k+1 and k+2 are in flight.
-  u32x4 ra0[kLoads], rb0[kLoads], ra1[kLoads], rb1[kLoads];
-  auto gload = [&](u32x4 (&ra)[kLoads], u32x4 (&rb)[kLoads], int k0) {
+  // Each wave instruction fills 8 rows (1 KB): lane L writes row L/8,
+  // physical chunk L%8, and fetches logical chunk (L%8) ^ (row & 7).
+  constexpr int kWaves = kNT / 64;
+  constexpr int kInst = BT / 8 / kWaves;         // wave instructions per operand per stage
+  auto dma = [&](int buf, int k0) {
 #pragma unroll
-    for (int q = 0; q < kLoads; ++q) {
-      const int row = ld_row + (kNT / 8) * q;
-      ra[q] = *reinterpret_cast<const u32x4*>(Aop + row * lda + k0 + ld_ch);
-      rb[q] = *reinterpret_cast<const u32x4*>(Bop + row * ldb + k0 + ld_ch);
-    }
-  };
-  auto sstore = [&](const u32x4 (&ra)[kLoads], const u32x4 (&rb)[kLoads], int buf) {
-#pragma unroll
-    for (int q = 0; q < kLoads; ++q) {
-      const int row = ld_row + (kNT / 8) * q;
-      *reinterpret_cast<u32x4*>(&sA[buf][row][ld_ch]) = ra[q];
-      *reinterpret_cast<u32x4*>(&sB[buf][row][ld_ch]) = rb[q];
+    for (int q = 0; q < kInst; ++q) {
+      const int blk = q * kWaves + wave;         // 8-row block
+      const int row = blk * 8 + (lane >> 3);
+      const int ch = (lane & 7) ^ (row & 7);
+      __builtin_amdgcn_global_load_lds(Aop + row * lda + k0 + ch * kEpc, &sA[buf][blk * 8][0], 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(Bop + row * ldb + k0 + ch * kEpc, &sB[buf][blk * 8][0], 16, 0, 0);
     }
   };
 
@@ -383,49 +380,48 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+  auto frag = [&](const T* rowp, int row, int kc) {
+    const int e = kc + lk * (M::kKStep / 2);
+    const int off = (((e / kEpc) ^ (row & 7)) * kEpc) + (e % kEpc);
+    return M::load(rowp + off, 0);
+  };
   auto compute = [&](int buf) {
-#pragma unroll
-    for (int kk = 0; kk < kBK / M::kKStep; ++kk) {
+    // fragments double-buffered in registers: the LDS reads of substep kk+1
+    // are issued before the MFMAs of substep kk
+    constexpr int kSub = kBK / M::kKStep;
+    typename M::Frag af[2][kMI], bfr[2][kNI];
+    auto fetch = [&](int s, int kk) {
       const int kc = kk * M::kKStep;
-      typename M::Frag af[kMI], bfr[kNI];
 #pragma unroll
-      for (int i = 0; i < kMI; ++i) af[i] = M::load(&sA[buf][wm + 32 * i + lr][kc], lk);
+      for (int i = 0; i < kMI; ++i) af[s][i] = frag(&sA[buf][wm + 32 * i + lr][0], wm + 32 * i + lr, kc);
 #pragma unroll
-      for (int j = 0; j < kNI; ++j) bfr[j] = M::load(&sB[buf][wn + 32 * j + lr][kc], lk);
+      for (int j = 0; j < kNI; ++j) bfr[s][j] = frag(&sB[buf][wn + 32 * j + lr][0], wn + 32 * j + lr, kc);
+    };
+    fetch(0, 0);
+#pragma unroll
+    for (int kk = 0; kk < kSub; ++kk) {
+      if (kk + 1 < kSub) fetch((kk + 1) & 1, kk + 1);
 #pragma unroll
       for (int i = 0; i < kMI; ++i)
 #pragma unroll
-        for (int j = 0; j < kNI; ++j) acc[i][j] = M::mma(af[i], bfr[j], acc[i][j]);
+        for (int j = 0; j < kNI; ++j) acc[i][j] = M::mma(af[kk & 1][i], bfr[kk & 1][j], acc[i][j]);
     }
   };
 
-  // Every K here is a multiple of 128, so nk is even and >= 2. The loads of
-  // the steady-state loop are unconditional so that each LDS store waits only
-  // for its own register set (in-order vmcnt), never for the stage behind it.
+  // The barrier after each stage both publishes the stage just loaded (every
+  // wave has waited for its own loads) and frees the buffer just read.
   const int nk = K / kBK;
-  gload(ra0, rb0, 0);
-  gload(ra1, rb1, kBK);
-  sstore(ra0, rb0, 0);
+  dma(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  // sched_barrier keeps the compiler from sinking the loads below the MFMAs.
-  for (int kt = 0; kt + 2 < nk; kt += 2) {
-    gload(ra0, rb0, (kt + 2) * kBK);   // stage kt+2 -> set 0
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk) dma((kt + 1) & 1, (kt + 1) * kBK);
     __builtin_amdgcn_sched_barrier(0);
-    compute(0);                        // stage kt
+    compute(kt & 1);
     __builtin_amdgcn_sched_barrier(0);
-    sstore(ra1, rb1, 1);               // stage kt+1
-    __syncthreads();
-    gload(ra1, rb1, (kt + 3) * kBK);   // stage kt+3 -> set 1
-    __builtin_amdgcn_sched_barrier(0);
-    compute(1);                        // stage kt+1
-    __builtin_amdgcn_sched_barrier(0);
-    sstore(ra0, rb0, 0);               // stage kt+2
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
-  compute(0);                          // stage nk-2
-  sstore(ra1, rb1, 1);                 // stage nk-1
-  __syncthreads();
-  compute(1);
 
   // ---- epilogues ----------------------------------------------------------
   // Results leave through LDS: each lane writes its values into the staging
