@@ -59,10 +59,15 @@ typedef enum lm_status {
   LM_ERR_HIP = 5                 /* a HIP runtime call or kernel launch failed        */
 } lm_status;
 
-/* Per-tensor flag: never take the Muon branch (Lion update on every step).
- * A tensor with rows == 1 or cols == 1 is always treated as Lion-only
- * (1-D parameters do not take the spectral step, Section 3). */
-enum { LM_TENSOR_LION_ONLY = 1u };
+/* Per-tensor flags.
+ * LM_TENSOR_LION_ONLY: never take the Muon branch (Lion update every step).
+ *   A tensor with rows == 1 or cols == 1 is always treated as Lion-only
+ *   (1-D parameters do not take the spectral step, Section 3).
+ * LM_TENSOR_ADAMW: AdamW with decoupled weight decay on every step instead
+ *   of Algorithm 1 -- the fallback Section 3 names for 1-D parameters
+ *   (Table 3: betas (0.8, 0.999), lr 1e-3). Its `momentum` buffer is AdamW's
+ *   first moment; it also needs a second-moment buffer (lionmuon_step_ex). */
+enum { LM_TENSOR_LION_ONLY = 1u, LM_TENSOR_ADAMW = 2u };
 
 /* Precision of the Newton-Schulz matrix products. */
 enum { LM_NS_BF16 = 0,   /* bf16 operands on MFMA, fp32 accumulation, for every
@@ -100,7 +105,20 @@ typedef struct lm_config {
   int32_t ns_bf16_min_side; /* LM_NS_BF16 only: matrices with a shorter short
                                side run the fp32 path; default 64, >= 0          */
   int32_t reserved;         /* must be 0                                          */
+  /* Per-step odd-polynomial schedule (Section 2: classical, Polar Express and
+   * Chebyshev-type schedules share the NS cost structure). 0 (default): step
+   * k uses (ns_a, ns_b, ns_c) for every k; otherwise it must equal ns_steps
+   * (<= LM_MAX_NS_SCHEDULE) and step k uses ns_schedule[k] = {a_k, b_k, c_k}. */
+  int32_t ns_schedule_steps;
+  int32_t reserved2;        /* must be 0                                          */
+  double ns_schedule[16][3];
+  /* AdamW for LM_TENSOR_ADAMW tensors: W <- W - adam_lr (mhat/(sqrt(vhat) +
+   * adam_eps) + adam_wd W), bias corrections with AdamW step t + 1.
+   * Defaults (1e-3, 0.8, 0.999, 1e-8, 0). */
+  double adam_lr, adam_beta1, adam_beta2, adam_eps, adam_wd;
 } lm_config;
+
+#define LM_MAX_NS_SCHEDULE 16
 
 /* Fill *cfg with the defaults listed above; lr_muon = lr_lion = 0. */
 void lionmuon_config_default(lm_config* cfg);
@@ -122,14 +140,19 @@ lm_status lionmuon_step(float* const* params, const float* const* grads,
 
 /*
  * lionmuon_step with an explicit configuration (two learning rates, fp32 or
- * bf16 Newton-Schulz, coefficients, eps, output scaling) and an optional
- * caller-owned device workspace. workspace == NULL with workspace_bytes == 0
- * selects the library-owned workspace; otherwise workspace must hold at least
+ * bf16 Newton-Schulz, coefficients or a per-step schedule, eps, output
+ * scaling, AdamW settings) and an optional caller-owned device workspace.
+ * second_moment: host array of n_tensors device pointers, read only for
+ *   LM_TENSOR_ADAMW tensors (AdamW's v, same shape, updated in place); may
+ *   be NULL when no tensor has that flag.
+ * workspace == NULL with workspace_bytes == 0 selects the library-owned
+ * workspace; otherwise workspace must hold at least
  * lionmuon_workspace_bytes(...) bytes, be 256-byte aligned, stay valid until
  * the enqueued work finishes, and must not be used by a concurrent call.
  */
 lm_status lionmuon_step_ex(float* const* params, const float* const* grads,
-                           float* const* momentum, const lm_shape* shapes,
+                           float* const* momentum, float* const* second_moment,
+                           const lm_shape* shapes,
                            int32_t n_tensors, int64_t t, int32_t P, double beta1,
                            double beta2, double wd, const lm_config* cfg,
                            void* workspace, size_t workspace_bytes,
@@ -156,15 +179,18 @@ lm_status lionmuon_ns(const float* X, float* O, int64_t rows, int64_t cols,
 typedef struct lm_plan_info {
   int32_t n_tensors;        /* non-empty tensors                               */
   int32_t n_lion;           /* tensors updated by the Lion branch this step    */
+  int32_t n_adamw;          /* tensors updated by AdamW (LM_TENSOR_ADAMW)      */
+  int32_t reserved;
   int32_t n_muon;           /* matrices updated by the Muon branch this step   */
   int32_t n_shape_classes;  /* distinct (short side, long side) Muon shapes    */
   int64_t lion_elements;    /* elements on the Lion branch                     */
+  int64_t adamw_elements;   /* elements updated by AdamW                       */
   int64_t muon_elements;    /* elements on the Muon branch                     */
   int64_t gram_tiles, poly_tiles, apply_tiles; /* MFMA output tiles per NS step */
   double ns_flops;          /* algorithmic NS flops, symmetric products counted
                                once: K * sum s(s+1)l + s^2(s+1) + 2 s^2 l       */
   double ns_flops_dense;    /* dense convention K * sum 4 s^2 l + 2 s^3        */
-  double lion_bytes;        /* 20 bytes per Lion-branch element                 */
+  double lion_bytes;        /* 20 bytes per Lion-branch element, 28 per AdamW   */
   size_t workspace_bytes;   /* device workspace this step needs                */
 } lm_plan_info;
 

@@ -81,15 +81,30 @@ def ns_output_scale(m: int, n: int, scale_mode: int) -> float:
     raise ValueError(f"unknown scale mode {scale_mode}")
 
 
+def coefficient_schedule(steps: int, coeffs) -> list:
+    """Per-step (a, b, c) list: one triple repeated ``steps`` times, or an
+    explicit list of ``steps`` triples (an odd-polynomial schedule of the
+    kind Section 2 mentions: classical, Polar Express, Chebyshev-type)."""
+    c0 = np.asarray(coeffs, dtype=np.float64)
+    if c0.ndim == 1:
+        if c0.shape != (3,):
+            raise ValueError("coefficients must be (a, b, c)")
+        return [tuple(c0)] * steps
+    if c0.shape != (steps, 3):
+        raise ValueError("a schedule needs one (a, b, c) triple per step")
+    return [tuple(r) for r in c0]
+
+
 def newton_schulz(G: np.ndarray, steps: int = NS_STEPS, coeffs=QUINTIC,
                   eps: float = NS_EPS) -> np.ndarray:
     """NS_K(G): K Newton-Schulz steps towards msign(G) = U V^T (Section 2).
 
     X0 = G / (||G||_F + eps), oriented so that X has no more rows than
-    columns; each step forms A = X X^T, B = b*A + c*A A and X <- a*X + B X;
-    the result is turned back to G's orientation.
+    columns; step k forms A = X X^T, B = b_k*A + c_k*A A and
+    X <- a_k*X + B X; the result is turned back to G's orientation.
+    ``coeffs`` is one (a, b, c) for every step or a list of per-step triples.
     """
-    a, b, c = (float(v) for v in coeffs)
+    schedule = coefficient_schedule(steps, coeffs)
     X = np.array(G, dtype=np.float64, copy=True)
     if X.ndim != 2:
         raise ValueError("Newton-Schulz needs a 2-D matrix")
@@ -97,13 +112,37 @@ def newton_schulz(G: np.ndarray, steps: int = NS_STEPS, coeffs=QUINTIC,
     if transposed:
         X = X.T
     X = X / (np.linalg.norm(X, "fro") + eps)
-    for _ in range(steps):
+    for a, b, c in schedule:
         A = X @ X.T
         B = b * A + c * (A @ A)
         X = a * X + B @ X
     if transposed:
         X = X.T
     return X
+
+
+ADAMW_DEFAULTS = dict(lr=1e-3, beta1=0.8, beta2=0.999, eps=1e-8, wd=0.0)
+
+
+def adamw_update(W, G, m, v, step, lr, beta1, beta2, eps, wd):
+    """AdamW with decoupled weight decay (Loshchilov & Hutter), the fallback
+    Section 3 names for 1-D parameters (Table 3: betas (0.8, 0.999), lr 1e-3):
+
+        m <- beta1 m + (1-beta1) g;   v <- beta2 v + (1-beta2) g^2
+        mhat = m / (1 - beta1^step);  vhat = v / (1 - beta2^step)
+        W <- W - lr (mhat / (sqrt(vhat) + eps) + wd W)
+
+    ``step`` counts AdamW steps from 1. Returns (W', m', v') in float64.
+    """
+    W, G, m, v = (np.asarray(x, dtype=np.float64) for x in (W, G, m, v))
+    if step < 1:
+        raise ValueError("AdamW steps count from 1")
+    m_new = beta1 * m + (1.0 - beta1) * G
+    v_new = beta2 * v + (1.0 - beta2) * G * G
+    mhat = m_new / (1.0 - beta1 ** step)
+    vhat = v_new / (1.0 - beta2 ** step)
+    W_new = W - lr * (mhat / (np.sqrt(vhat) + eps) + wd * W)
+    return W_new, m_new, v_new
 
 
 def lionmuon_update(W, G, M, t, P, beta1, beta2, lr_muon, lr_lion, wd, *,

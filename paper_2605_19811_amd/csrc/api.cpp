@@ -233,8 +233,20 @@ struct Timer {
 };
 
 lm::StepConsts step_consts(double beta1, double beta2, double wd, double lr_muon,
-                           double lr_lion, double eps) {
-  lm::StepConsts k;
+                           double lr_lion, double eps, const lm_config* cfg, int64_t t) {
+  lm::StepConsts k{};
+  if (cfg) {                       // AdamW; the AdamW step count is t + 1
+    const double step = double(t) + 1.0;
+    k.adam_lr = float(cfg->adam_lr);
+    k.adam_b1 = float(cfg->adam_beta1);
+    k.adam_omb1 = float(1.0 - cfg->adam_beta1);
+    k.adam_b2 = float(cfg->adam_beta2);
+    k.adam_omb2 = float(1.0 - cfg->adam_beta2);
+    k.adam_eps = float(cfg->adam_eps);
+    k.adam_wd = float(cfg->adam_wd);
+    k.adam_c1 = float(1.0 / (1.0 - std::pow(cfg->adam_beta1, step)));
+    k.adam_c2 = float(1.0 / (1.0 - std::pow(cfg->adam_beta2, step)));
+  }
   k.beta1 = float(beta1);
   k.one_minus_beta1 = float(1.0 - beta1);
   k.beta2 = float(beta2);
@@ -292,14 +304,15 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
   gl.ws = ws;
   gl.rscale = rscale;
   gl.store_o = store_o ? 1 : 0;
-  gl.a = float(cfg.ns_a);
-  gl.b = float(cfg.ns_b);
-  gl.c = float(cfg.ns_c);
   gl.lr = k.lr_muon;
   gl.wd = k.wd;
   const lm::GemmMode modes[3] = {lm::kGram, lm::kPoly, lm::kApply};
   const int phases[3] = {LM_PHASE_GRAM, LM_PHASE_POLY, LM_PHASE_APPLY};
   for (int it = 0; it < cfg.ns_steps; ++it) {
+    const bool sched = cfg.ns_schedule_steps != 0;
+    gl.a = float(sched ? cfg.ns_schedule[it][0] : cfg.ns_a);
+    gl.b = float(sched ? cfg.ns_schedule[it][1] : cfg.ns_b);
+    gl.c = float(sched ? cfg.ns_schedule[it][2] : cfg.ns_c);
     gl.src = it & 1;
     gl.first = it == 0;
     gl.last = it == cfg.ns_steps - 1;
@@ -334,7 +347,23 @@ lm_status check_config(const lm_config* cfg) {
   if (cfg->ns_scale_mode != LM_NS_SCALE_NONE && cfg->ns_scale_mode != LM_NS_SCALE_RMS02)
     return fail(LM_ERR_INVALID_ARGUMENT, "unknown ns_scale_mode");
   if (cfg->ns_bf16_min_side < 0) return fail(LM_ERR_INVALID_ARGUMENT, "ns_bf16_min_side must be >= 0");
-  if (cfg->reserved != 0) return fail(LM_ERR_INVALID_ARGUMENT, "lm_config.reserved must be 0");
+  if (cfg->reserved != 0 || cfg->reserved2 != 0)
+    return fail(LM_ERR_INVALID_ARGUMENT, "lm_config reserved fields must be 0");
+  if (!(cfg->adam_beta1 >= 0.0 && cfg->adam_beta1 < 1.0) ||
+      !(cfg->adam_beta2 >= 0.0 && cfg->adam_beta2 < 1.0))
+    return fail(LM_ERR_INVALID_ARGUMENT, "adam betas must lie in [0, 1)");
+  if (!(cfg->adam_lr >= 0.0) || !std::isfinite(cfg->adam_lr) || !(cfg->adam_eps >= 0.0) ||
+      !std::isfinite(cfg->adam_eps) || !(cfg->adam_wd >= 0.0) || !std::isfinite(cfg->adam_wd))
+    return fail(LM_ERR_INVALID_ARGUMENT, "adam_lr, adam_eps and adam_wd must be finite and >= 0");
+  if (cfg->ns_schedule_steps != 0) {
+    if (cfg->ns_schedule_steps != cfg->ns_steps || cfg->ns_steps > LM_MAX_NS_SCHEDULE)
+      return fail(LM_ERR_INVALID_ARGUMENT,
+                  "ns_schedule_steps must be 0 or equal ns_steps (at most 16)");
+    for (int k = 0; k < cfg->ns_steps; ++k)
+      for (int j = 0; j < 3; ++j)
+        if (!std::isfinite(cfg->ns_schedule[k][j]))
+          return fail(LM_ERR_INVALID_ARGUMENT, "ns_schedule coefficients must be finite");
+  }
   return LM_OK;
 }
 
@@ -346,12 +375,13 @@ lm::NsPrecision precision_of(const lm_config& cfg) {
 }
 
 std::vector<TensorIn> gather(float* const* params, const float* const* grads, float* const* momentum,
-                             const lm_shape* shapes, int32_t n) {
+                             float* const* second_moment, const lm_shape* shapes, int32_t n) {
   std::vector<TensorIn> v(size_t(n > 0 ? n : 0));
   for (int32_t i = 0; i < n; ++i) {
     v[i].w = params[i];
     v[i].g = grads[i];
     v[i].m = momentum[i];
+    v[i].v = (second_moment && (shapes[i].flags & lm::kFlagAdamW)) ? second_moment[i] : nullptr;
     v[i].rows = shapes[i].rows;
     v[i].cols = shapes[i].cols;
     v[i].flags = shapes[i].flags;
@@ -361,7 +391,8 @@ std::vector<TensorIn> gather(float* const* params, const float* const* grads, fl
 }
 
 lm_status step_impl(float* const* params, const float* const* grads, float* const* momentum,
-                    const lm_shape* shapes, int32_t n, int64_t t, int32_t P, double beta1,
+                    float* const* second_moment, const lm_shape* shapes, int32_t n, int64_t t,
+                    int32_t P, double beta1,
                     double beta2, double wd, const lm_config* cfg, void* workspace,
                     size_t workspace_bytes, hipStream_t stream) {
   if (cfg == nullptr) return fail(LM_ERR_INVALID_ARGUMENT, "null config");
@@ -377,7 +408,7 @@ lm_status step_impl(float* const* params, const float* const* grads, float* cons
     return fail(LM_ERR_INVALID_ARGUMENT, "workspace and workspace_bytes must both be set or both be 0");
   if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u))
     return fail(LM_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
-  std::vector<TensorIn> x = gather(params, grads, momentum, shapes, n);
+  std::vector<TensorIn> x = gather(params, grads, momentum, second_moment, shapes, n);
   st = lm::validate_tensors(x.data(), n, &err);
   if (st != Status::kOk) return fail(to_c(st), err);
   bool any = false;
@@ -400,7 +431,7 @@ lm_status step_impl(float* const* params, const float* const* grads, float* cons
       if (s != LM_OK) return s;
     }
   }
-  return enqueue(*dp, step_consts(beta1, beta2, wd, cfg->lr_muon, cfg->lr_lion, cfg->ns_eps),
+  return enqueue(*dp, step_consts(beta1, beta2, wd, cfg->lr_muon, cfg->lr_lion, cfg->ns_eps, cfg, t),
                  *cfg, ws, false, stream);
 }
 
@@ -423,6 +454,13 @@ void lionmuon_config_default(lm_config* cfg) {
   cfg->lr_lion = 0.0;
   cfg->ns_bf16_min_side = 64;
   cfg->reserved = 0;
+  cfg->ns_schedule_steps = 0;
+  cfg->reserved2 = 0;
+  cfg->adam_lr = 1e-3;
+  cfg->adam_beta1 = 0.8;
+  cfg->adam_beta2 = 0.999;
+  cfg->adam_eps = 1e-8;
+  cfg->adam_wd = 0.0;
 }
 
 lm_status lionmuon_step(float* const* params, const float* const* grads, float* const* momentum,
@@ -432,16 +470,17 @@ lm_status lionmuon_step(float* const* params, const float* const* grads, float* 
   lionmuon_config_default(&cfg);
   cfg.lr_muon = lr;
   cfg.lr_lion = lr;
-  return step_impl(params, grads, momentum, shapes, n_tensors, t, P, beta1, beta2, wd, &cfg,
-                   nullptr, 0, stream);
+  return step_impl(params, grads, momentum, nullptr, shapes, n_tensors, t, P, beta1, beta2, wd,
+                   &cfg, nullptr, 0, stream);
 }
 
 lm_status lionmuon_step_ex(float* const* params, const float* const* grads, float* const* momentum,
-                           const lm_shape* shapes, int32_t n_tensors, int64_t t, int32_t P,
-                           double beta1, double beta2, double wd, const lm_config* cfg,
-                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  return step_impl(params, grads, momentum, shapes, n_tensors, t, P, beta1, beta2, wd, cfg,
-                   workspace, workspace_bytes, stream);
+                           float* const* second_moment, const lm_shape* shapes, int32_t n_tensors,
+                           int64_t t, int32_t P, double beta1, double beta2, double wd,
+                           const lm_config* cfg, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream) {
+  return step_impl(params, grads, momentum, second_moment, shapes, n_tensors, t, P, beta1, beta2,
+                   wd, cfg, workspace, workspace_bytes, stream);
 }
 
 lm_status lionmuon_workspace_bytes(const lm_shape* shapes, int32_t n_tensors, const lm_config* cfg,
@@ -478,6 +517,7 @@ lm_status lionmuon_plan_info(const lm_shape* shapes, int32_t n, int64_t t, int32
     x[i].w = reinterpret_cast<float*>(addr); addr += bytes + 16;
     x[i].g = reinterpret_cast<const float*>(addr); addr += bytes + 16;
     x[i].m = reinterpret_cast<float*>(addr); addr += bytes + 16;
+    x[i].v = reinterpret_cast<float*>(addr); addr += bytes + 16;
   }
   std::string err;
   Status st = lm::validate_tensors(x.data(), n, &err);
@@ -488,7 +528,9 @@ lm_status lionmuon_plan_info(const lm_shape* shapes, int32_t n, int64_t t, int32
   if (st != Status::kOk) return fail(to_c(st), err);
   std::memset(out, 0, sizeof(*out));
   out->n_tensors = p.n_tensors;
-  out->n_lion = int32_t(p.lion.size());
+  out->n_lion = int32_t(p.lion.size()) - p.n_adamw;
+  out->n_adamw = p.n_adamw;
+  out->adamw_elements = p.adamw_elements;
   out->n_muon = int32_t(p.mats.size());
   out->n_shape_classes = p.n_shape_classes;
   out->lion_elements = p.lion_elements;
@@ -498,7 +540,7 @@ lm_status lionmuon_plan_info(const lm_shape* shapes, int32_t n, int64_t t, int32
   out->apply_tiles = int64_t(p.apply[0].size() + p.apply[1].size());
   out->ns_flops = lm::ns_flops_symmetric(p, cfg->ns_steps);
   out->ns_flops_dense = lm::ns_flops_dense(p, cfg->ns_steps);
-  out->lion_bytes = 20.0 * double(p.lion_elements);
+  out->lion_bytes = 20.0 * double(p.lion_elements) + 28.0 * double(p.adamw_elements);
   out->workspace_bytes = p.ws_bytes;
   return LM_OK;
 }
@@ -531,6 +573,7 @@ lm_status lionmuon_ns(const float* X, float* O, int64_t rows, int64_t cols, int3
     x[b].w = O + b * numel;
     x[b].g = X + b * numel;
     x[b].m = nullptr;
+    x[b].v = nullptr;
     x[b].rows = rows;
     x[b].cols = cols;
     x[b].flags = 0;
@@ -549,7 +592,8 @@ lm_status lionmuon_ns(const float* X, float* O, int64_t rows, int64_t cols, int3
     s = owned_workspace(dp->plan.ws_bytes, &ws);
     if (s != LM_OK) return s;
   }
-  return enqueue(*dp, step_consts(0.0, 0.0, 0.0, 0.0, 0.0, cfg->ns_eps), *cfg, ws, true, stream);
+  return enqueue(*dp, step_consts(0.0, 0.0, 0.0, 0.0, 0.0, cfg->ns_eps, nullptr, 0), *cfg, ws, true,
+                 stream);
 }
 
 lm_status lionmuon_profiling_enable(int32_t enable) {

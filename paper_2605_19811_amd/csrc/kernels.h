@@ -13,6 +13,8 @@ namespace lm {
 struct StepConsts {
   float beta1, one_minus_beta1, beta2, one_minus_beta2;
   float lr_lion, lr_muon, wd, eps;
+  // AdamW (LM_TENSOR_ADAMW tensors); c1, c2 = 1 / (1 - beta^step)
+  float adam_lr, adam_b1, adam_omb1, adam_b2, adam_omb2, adam_eps, adam_wd, adam_c1, adam_c2;
 };
 
 struct LionLaunch {
@@ -22,6 +24,7 @@ struct LionLaunch {
   int32_t n_blocks;
   StepConsts k;
 };
+// Elementwise pass: Lion-branch tensors and AdamW tensors in one launch.
 hipError_t launch_lion(const LionLaunch& a, hipStream_t stream);
 
 struct PrepLaunch {

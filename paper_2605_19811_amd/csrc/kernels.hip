@@ -2,6 +2,7 @@
 //
 //  lion_kernel   Lion branch: Ghat = b1*M + (1-b1)*G; W -= lr*(sign(Ghat) + wd*W);
 //                M = b2*M + (1-b2)*G. Multi-tensor, 16-byte vectors, HBM bound.
+//                Tensors flagged AdamW take the AdamW update in the same launch.
 //  prep_kernel   Muon branch, first pass: the same interpolation and momentum
 //                update, Ghat stored in the NS element type in both the
 //                iteration orientation X (rows <= cols) and its transpose, and
@@ -56,12 +57,22 @@ struct LionArgs {
   const int32_t* block_start;
   int32_t n_tensors;
   float b1, omb1, b2, omb2, lr, wd;
+  float ab1, aomb1, ab2, aomb2, alr, aeps, awd, ac1, ac2;   // AdamW
 };
 
 __device__ __forceinline__ void lion_elem(float& w, float g, float& m, const LionArgs& a) {
   const float c = fmaf(a.b1, m, a.omb1 * g);
   w = fmaf(-a.lr, fmaf(a.wd, w, sign_f(c)), w);
   m = fmaf(a.b2, m, a.omb2 * g);
+}
+
+// AdamW with decoupled weight decay; ac1, ac2 are the bias corrections.
+__device__ __forceinline__ void adamw_elem(float& w, float g, float& m, float& v,
+                                           const LionArgs& a) {
+  m = fmaf(a.ab1, m, a.aomb1 * g);
+  v = fmaf(a.ab2, v, a.aomb2 * (g * g));
+  const float upd = (m * a.ac1) / (sqrtf(v * a.ac2) + a.aeps);
+  w = fmaf(-a.alr, fmaf(a.awd, w, upd), w);
 }
 
 constexpr int kLionUnroll = kLionBlockElems / (256 * 4);
@@ -72,7 +83,8 @@ __global__ __launch_bounds__(256) void lion_kernel(LionArgs a) {
   const LionTensor t = a.tensors[ti];
   const int64_t base = int64_t(b - a.block_start[ti]) * kLionBlockElems;
   const int tid = threadIdx.x;
-  if (t.vec_ok && base + kLionBlockElems <= t.numel) {
+  const bool full = t.vec_ok && base + kLionBlockElems <= t.numel;
+  if (full && !t.adamw) {
     f32x4* w4 = reinterpret_cast<f32x4*>(t.w + base);
     const f32x4* g4 = reinterpret_cast<const f32x4*>(t.g + base);
     f32x4* m4 = reinterpret_cast<f32x4*>(t.m + base);
@@ -100,11 +112,38 @@ __global__ __launch_bounds__(256) void lion_kernel(LionArgs a) {
       __builtin_nontemporal_store(w[u], &w4[i]);
       __builtin_nontemporal_store(m[u], &m4[i]);
     }
+  } else if (full) {
+    f32x4* w4 = reinterpret_cast<f32x4*>(t.w + base);
+    const f32x4* g4 = reinterpret_cast<const f32x4*>(t.g + base);
+    f32x4* m4 = reinterpret_cast<f32x4*>(t.m + base);
+    f32x4* v4 = reinterpret_cast<f32x4*>(t.v + base);
+#pragma unroll
+    for (int u = 0; u < kLionUnroll; ++u) {
+      const int i = tid + 256 * u;
+      f32x4 w = w4[i], g = g4[i], m = m4[i], v = v4[i];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float we = w[e], me = m[e], ve = v[e];
+        adamw_elem(we, g[e], me, ve, a);
+        w[e] = we;
+        m[e] = me;
+        v[e] = ve;
+      }
+      w4[i] = w;
+      m4[i] = m;
+      v4[i] = v;
+    }
   } else {
     const int64_t end = min(base + int64_t(kLionBlockElems), t.numel);
     for (int64_t i = base + tid; i < end; i += 256) {
       float w = t.w[i], m = t.m[i];
-      lion_elem(w, t.g[i], m, a);
+      if (t.adamw) {
+        float v = t.v[i];
+        adamw_elem(w, t.g[i], m, v, a);
+        t.v[i] = v;
+      } else {
+        lion_elem(w, t.g[i], m, a);
+      }
       t.w[i] = w;
       t.m[i] = m;
     }
@@ -617,6 +656,15 @@ hipError_t launch_lion(const LionLaunch& l, hipStream_t stream) {
   a.omb2 = l.k.one_minus_beta2;
   a.lr = l.k.lr_lion;
   a.wd = l.k.wd;
+  a.ab1 = l.k.adam_b1;
+  a.aomb1 = l.k.adam_omb1;
+  a.ab2 = l.k.adam_b2;
+  a.aomb2 = l.k.adam_omb2;
+  a.alr = l.k.adam_lr;
+  a.aeps = l.k.adam_eps;
+  a.awd = l.k.adam_wd;
+  a.ac1 = l.k.adam_c1;
+  a.ac2 = l.k.adam_c2;
   hipLaunchKernelGGL(lion_kernel, dim3(l.n_blocks), dim3(256), 0, stream, a);
   return hipGetLastError();
 }

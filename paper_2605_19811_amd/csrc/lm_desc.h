@@ -17,14 +17,15 @@ constexpr int kPrepTile = 64;    // square tile of the preparation / transpose p
 constexpr int kLionBlockElems = 4096;  // elements per Lion workgroup (256 x float4 x 4)
 constexpr int kXcds = 8;         // accelerator complex dies of one MI355X
 
-// One tensor on the Lion branch.
+// One tensor of the elementwise pass: the Lion branch, or AdamW.
 struct LionTensor {
   float* w;
   const float* g;
-  float* m;
+  float* m;         // Lion momentum / AdamW first moment
+  float* v;         // AdamW second moment (null for Lion)
   int64_t numel;
-  int32_t vec_ok;   // w, g, m are all 16-byte aligned
-  int32_t pad_;
+  int32_t vec_ok;   // every buffer of the tensor is 16-byte aligned
+  int32_t adamw;    // 1: AdamW, 0: Lion
 };
 
 // One matrix on the Muon branch. Workspace offsets are in BYTES from the

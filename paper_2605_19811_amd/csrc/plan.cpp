@@ -21,7 +21,7 @@ bool finite_nonneg(double v) { return std::isfinite(v) && v >= 0.0; }
 bool is_muon_step(int64_t t, int32_t P) { return P >= 1 && t % P == 0; }
 
 bool is_matrix(const TensorIn& x) {
-  return x.rows > 1 && x.cols > 1 && !(x.flags & 1u);
+  return x.rows > 1 && x.cols > 1 && !(x.flags & (kFlagLionOnly | kFlagAdamW));
 }
 
 Status validate_scalars(int64_t t, int32_t P, double beta1, double beta2, double wd,
@@ -51,8 +51,9 @@ Status validate_tensors(const TensorIn* x, int32_t n, std::string* err) {
       *err = "tensor " + std::to_string(i) + ": negative dimension";
       return Status::kInvalid;
     }
-    if (t.reserved != 0 || (t.flags & ~1u)) {
-      *err = "tensor " + std::to_string(i) + ": unknown flag bits or reserved field set";
+    if (t.reserved != 0 || (t.flags & ~(kFlagLionOnly | kFlagAdamW)) ||
+        t.flags == (kFlagLionOnly | kFlagAdamW)) {
+      *err = "tensor " + std::to_string(i) + ": unknown or conflicting flag bits, or reserved field set";
       return Status::kInvalid;
     }
     if (t.rows == 0 || t.cols == 0) continue;
@@ -60,18 +61,22 @@ Status validate_tensors(const TensorIn* x, int32_t n, std::string* err) {
       *err = "tensor " + std::to_string(i) + ": too many elements";
       return Status::kInvalid;
     }
-    if (!t.w || !t.g || !t.m) {
-      *err = "tensor " + std::to_string(i) + ": null params, grads or momentum pointer";
+    const bool adamw = (t.flags & kFlagAdamW) != 0;
+    if (!t.w || !t.g || !t.m || (adamw && !t.v)) {
+      *err = "tensor " + std::to_string(i) +
+             ": null params, grads, momentum or (AdamW) second-moment pointer";
       return Status::kInvalid;
     }
     auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; };
-    if (!al(t.w) || !al(t.g) || !al(t.m)) {
+    if (!al(t.w) || !al(t.g) || !al(t.m) || (adamw && !al(t.v))) {
       *err = "tensor " + std::to_string(i) + ": pointers must be 4-byte aligned fp32";
       return Status::kInvalid;
     }
     const uintptr_t bytes = uintptr_t(t.rows * t.cols) * 4u;
     wr.push_back({reinterpret_cast<uintptr_t>(t.w), reinterpret_cast<uintptr_t>(t.w) + bytes});
     wr.push_back({reinterpret_cast<uintptr_t>(t.m), reinterpret_cast<uintptr_t>(t.m) + bytes});
+    if (adamw)
+      wr.push_back({reinterpret_cast<uintptr_t>(t.v), reinterpret_cast<uintptr_t>(t.v) + bytes});
     rd.push_back({reinterpret_cast<uintptr_t>(t.g), reinterpret_cast<uintptr_t>(t.g) + bytes});
   }
   std::sort(wr.begin(), wr.end());
@@ -141,15 +146,19 @@ Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec
     const TensorIn& t = x[i];
     if (t.rows == 0 || t.cols == 0) continue;
     ++p->n_tensors;
+    const bool adamw = (t.flags & kFlagAdamW) != 0;
+    const uintptr_t vbits = adamw ? reinterpret_cast<uintptr_t>(t.v) : 0;
     const bool vec_ok = ((reinterpret_cast<uintptr_t>(t.w) | reinterpret_cast<uintptr_t>(t.g) |
-                          reinterpret_cast<uintptr_t>(t.m)) & 15u) == 0;
+                          reinterpret_cast<uintptr_t>(t.m) | vbits) & 15u) == 0;
     if (!(muon_step && is_matrix(t))) {
       LionTensor lt{};
       lt.w = t.w;
       lt.g = t.g;
       lt.m = t.m;
+      lt.v = adamw ? t.v : nullptr;
       lt.numel = t.rows * t.cols;
       lt.vec_ok = vec_ok ? 1 : 0;
+      lt.adamw = adamw ? 1 : 0;
       const int64_t blocks = (lt.numel + kLionBlockElems - 1) / kLionBlockElems;
       if (int64_t(p->lion_block_start.back()) + blocks > INT32_MAX) {
         *err = "too many elements on the Lion branch";
@@ -157,7 +166,12 @@ Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec
       }
       p->lion.push_back(lt);
       p->lion_block_start.push_back(p->lion_block_start.back() + int32_t(blocks));
-      p->lion_elements += lt.numel;
+      if (adamw) {
+        p->adamw_elements += lt.numel;
+        ++p->n_adamw;
+      } else {
+        p->lion_elements += lt.numel;
+      }
       continue;
     }
     MuonMat mm{};

@@ -18,10 +18,13 @@ struct TensorIn {
   float* w;
   const float* g;
   float* m;
+  float* v;          // AdamW second moment (flag 2), else unused
   int64_t rows, cols;
   uint32_t flags;
   uint32_t reserved;
 };
+
+constexpr uint32_t kFlagLionOnly = 1u, kFlagAdamW = 2u;
 
 enum class Status : int { kOk = 0, kInvalid = 1, kUnsupported = 2, kNoMemory = 3,
                           kWorkspaceTooSmall = 4, kHip = 5 };
@@ -34,7 +37,7 @@ constexpr int64_t kMaxMatrixElems = int64_t(1) << 30;
 bool is_muon_step(int64_t t, int32_t P);
 
 // A tensor takes the Muon branch on Muon steps iff it is a real matrix
-// (rows > 1 and cols > 1) and not flagged Lion-only.
+// (rows > 1 and cols > 1) and flagged neither Lion-only nor AdamW.
 bool is_matrix(const TensorIn& x);
 
 // Newton-Schulz precision of one matrix: bf16 MFMA unless fp32 is asked for
@@ -52,7 +55,9 @@ struct Plan {
   // Lion branch
   std::vector<LionTensor> lion;
   std::vector<int32_t> lion_block_start;   // lion.size() + 1 prefix
-  int64_t lion_elements = 0;
+  int64_t lion_elements = 0;               // Lion-branch elements
+  int64_t adamw_elements = 0;              // AdamW elements
+  int32_t n_adamw = 0;
 
   // Muon branch
   std::vector<MuonMat> mats;

@@ -20,6 +20,7 @@ LM_ERR_WORKSPACE_TOO_SMALL = 4
 LM_ERR_HIP = 5
 
 LM_TENSOR_LION_ONLY = 1
+LM_TENSOR_ADAMW = 2
 LM_NS_BF16 = 0
 LM_NS_FP32 = 1
 LM_NS_SCALE_NONE = 0
@@ -45,13 +46,20 @@ class lm_config(ctypes.Structure):
                 ("ns_c", ctypes.c_double), ("ns_eps", ctypes.c_double),
                 ("ns_precision", ctypes.c_int32), ("ns_scale_mode", ctypes.c_int32),
                 ("lr_muon", ctypes.c_double), ("lr_lion", ctypes.c_double),
-                ("ns_bf16_min_side", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("ns_bf16_min_side", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("ns_schedule_steps", ctypes.c_int32), ("reserved2", ctypes.c_int32),
+                ("ns_schedule", (ctypes.c_double * 3) * 16),
+                ("adam_lr", ctypes.c_double), ("adam_beta1", ctypes.c_double),
+                ("adam_beta2", ctypes.c_double), ("adam_eps", ctypes.c_double),
+                ("adam_wd", ctypes.c_double)]
 
 
 class lm_plan_info(ctypes.Structure):
     _fields_ = [("n_tensors", ctypes.c_int32), ("n_lion", ctypes.c_int32),
+                ("n_adamw", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("n_muon", ctypes.c_int32), ("n_shape_classes", ctypes.c_int32),
-                ("lion_elements", ctypes.c_int64), ("muon_elements", ctypes.c_int64),
+                ("lion_elements", ctypes.c_int64), ("adamw_elements", ctypes.c_int64),
+                ("muon_elements", ctypes.c_int64),
                 ("gram_tiles", ctypes.c_int64), ("poly_tiles", ctypes.c_int64),
                 ("apply_tiles", ctypes.c_int64), ("ns_flops", ctypes.c_double),
                 ("ns_flops_dense", ctypes.c_double), ("lion_bytes", ctypes.c_double),
@@ -86,7 +94,7 @@ def library():
     lib.lionmuon_config_default.restype = None
     lib.lionmuon_step.argtypes = [vp, vp, vp, P(lm_shape), i32, i64, i32, f64, f64, f64, f64, vp]
     lib.lionmuon_step.restype = ctypes.c_int
-    lib.lionmuon_step_ex.argtypes = [vp, vp, vp, P(lm_shape), i32, i64, i32, f64, f64, f64,
+    lib.lionmuon_step_ex.argtypes = [vp, vp, vp, vp, P(lm_shape), i32, i64, i32, f64, f64, f64,
                                      P(lm_config), vp, sz, vp]
     lib.lionmuon_step_ex.restype = ctypes.c_int
     lib.lionmuon_workspace_bytes.argtypes = [P(lm_shape), i32, P(lm_config), P(sz)]
@@ -122,7 +130,10 @@ def _check(status, what):
 
 def config(ns_steps=5, ns_coeffs=(3.4445, -4.7750, 2.0315), ns_eps=1e-7,
            ns_precision="bf16", ns_scale="none", lr_muon=0.0, lr_lion=0.0,
-           ns_bf16_min_side=64) -> lm_config:
+           ns_bf16_min_side=64, ns_schedule=None, adam_lr=1e-3, adam_betas=(0.8, 0.999),
+           adam_eps=1e-8, adam_wd=0.0) -> lm_config:
+    """lm_config with defaults; ``ns_schedule`` is an optional list of
+    per-step (a, b, c) triples (its length sets ns_steps)."""
     cfg = lm_config()
     library().lionmuon_config_default(ctypes.byref(cfg))
     cfg.ns_steps = ns_steps
@@ -133,11 +144,32 @@ def config(ns_steps=5, ns_coeffs=(3.4445, -4.7750, 2.0315), ns_eps=1e-7,
     cfg.lr_muon = lr_muon
     cfg.lr_lion = lr_lion
     cfg.ns_bf16_min_side = ns_bf16_min_side
+    cfg.adam_lr = adam_lr
+    cfg.adam_beta1, cfg.adam_beta2 = adam_betas
+    cfg.adam_eps = adam_eps
+    cfg.adam_wd = adam_wd
+    if ns_schedule is not None:
+        sched = [tuple(float(v) for v in t) for t in ns_schedule]
+        if not 1 <= len(sched) <= 16 or any(len(t) != 3 for t in sched):
+            raise ValueError("ns_schedule needs 1..16 (a, b, c) triples")
+        cfg.ns_steps = len(sched)
+        cfg.ns_schedule_steps = len(sched)
+        for k, t in enumerate(sched):
+            for j in range(3):
+                cfg.ns_schedule[k][j] = t[j]
     return cfg
 
 
+def _flags(flag):
+    """Tensor flags from a bool (Lion-only) or an int of LM_TENSOR_* bits."""
+    if isinstance(flag, bool):
+        return LM_TENSOR_LION_ONLY if flag else 0
+    return int(flag)
+
+
 def shape_of(t, lion_only=False) -> lm_shape:
-    """rows x cols of a tensor: 1-D -> (1, n); k-D -> (shape[0], prod(rest))."""
+    """rows x cols of a tensor: 1-D -> (1, n); k-D -> (shape[0], prod(rest)).
+    ``lion_only`` is a bool or LM_TENSOR_* flag bits."""
     dims = tuple(t.shape)
     if len(dims) == 0:
         rows, cols = 1, 1
@@ -148,14 +180,15 @@ def shape_of(t, lion_only=False) -> lm_shape:
         cols = 1
         for d in dims[1:]:
             cols *= d
-    return lm_shape(rows, cols, LM_TENSOR_LION_ONLY if lion_only else 0, 0)
+    return lm_shape(rows, cols, _flags(lion_only), 0)
 
 
 def shapes_array(specs):
-    """lm_shape array from (rows, cols, lion_only) triples."""
+    """lm_shape array from (rows, cols, flags) triples (flags: bool Lion-only
+    or LM_TENSOR_* bits)."""
     arr = (lm_shape * max(len(specs), 1))()
     for i, (r, c, lo) in enumerate(specs):
-        arr[i] = lm_shape(r, c, LM_TENSOR_LION_ONLY if lo else 0, 0)
+        arr[i] = lm_shape(r, c, _flags(lo), 0)
     return arr
 
 
@@ -179,13 +212,22 @@ def _stream_handle(stream):
 
 
 class TensorList:
-    """Marshalled pointer arrays of one (params, grads, momentum) list."""
+    """Marshalled pointer arrays of one (params, grads, momentum) list.
 
-    def __init__(self, params, grads, momentum, lion_only=None):
+    ``lion_only``: per-tensor bool or LM_TENSOR_* flags; ``second_moment``:
+    per-tensor AdamW second-moment tensors (None where not AdamW)."""
+
+    def __init__(self, params, grads, momentum, lion_only=None, second_moment=None):
         n = len(params)
         if len(grads) != n or len(momentum) != n:
             raise ValueError("params, grads and momentum must have one length")
         lion_only = list(lion_only) if lion_only is not None else [False] * n
+        second_moment = list(second_moment) if second_moment is not None else [None] * n
+        for i, v in enumerate(second_moment):
+            if v is not None:
+                _check_tensor(v, f"second_moment[{i}]")
+                if v.shape != params[i].shape:
+                    raise ValueError(f"second_moment[{i}] has the wrong shape")
         for i in range(n):
             _check_tensor(params[i], f"params[{i}]")
             _check_tensor(grads[i], f"grads[{i}]")
@@ -197,8 +239,9 @@ class TensorList:
         self.p = (ctypes.c_void_p * k)(*[t.data_ptr() for t in params])
         self.g = (ctypes.c_void_p * k)(*[t.data_ptr() for t in grads])
         self.m = (ctypes.c_void_p * k)(*[t.data_ptr() for t in momentum])
+        self.v = (ctypes.c_void_p * k)(*[0 if t is None else t.data_ptr() for t in second_moment])
         self.shapes = (lm_shape * k)(*[shape_of(t, lo) for t, lo in zip(params, lion_only)])
-        self._keep = (list(params), list(grads), list(momentum))
+        self._keep = (list(params), list(grads), list(momentum), second_moment)
 
     def set_grads(self, grads):
         for i, t in enumerate(grads):
@@ -206,7 +249,7 @@ class TensorList:
             if t.shape != self._keep[0][i].shape:
                 raise ValueError(f"grads[{i}] has the wrong shape")
             self.g[i] = t.data_ptr()
-        self._keep = (self._keep[0], list(grads), self._keep[2])
+        self._keep = (self._keep[0], list(grads), self._keep[2], self._keep[3])
 
 
 def lionmuon_step(params, grads, momentum, t, P, beta1, beta2, lr, wd, stream=None,
@@ -221,17 +264,19 @@ def lionmuon_step(params, grads, momentum, t, P, beta1, beta2, lr, wd, stream=No
 
 def lionmuon_step_ex(params, grads, momentum, t, P, beta1, beta2, wd, cfg: lm_config,
                      workspace=None, stream=None, lion_only=None,
-                     tensors: TensorList | None = None):
+                     tensors: TensorList | None = None, second_moment=None):
     """One LionMuon step with an explicit lm_config; ``workspace`` is an
-    optional uint8 GPU tensor (caller-owned workspace)."""
-    tl = tensors or TensorList(params, grads, momentum, lion_only)
+    optional uint8 GPU tensor (caller-owned workspace); ``second_moment``
+    lists the AdamW second moments of LM_TENSOR_ADAMW tensors."""
+    tl = tensors or TensorList(params, grads, momentum, lion_only, second_moment)
     ws_ptr, ws_bytes = None, 0
     if workspace is not None:
         if not workspace.is_cuda:
             raise LionMuonError(LM_ERR_INVALID_ARGUMENT, "workspace must be a GPU tensor")
         ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
     st = library().lionmuon_step_ex(ctypes.cast(tl.p, ctypes.c_void_p), ctypes.cast(tl.g, ctypes.c_void_p),
-                                    ctypes.cast(tl.m, ctypes.c_void_p), tl.shapes, tl.n, int(t),
+                                    ctypes.cast(tl.m, ctypes.c_void_p), ctypes.cast(tl.v, ctypes.c_void_p),
+                                    tl.shapes, tl.n, int(t),
                                     int(P), beta1, beta2, wd, ctypes.byref(cfg), ws_ptr, ws_bytes,
                                     _stream_handle(stream))
     _check(st, "lionmuon_step_ex")

@@ -67,3 +67,14 @@ def check_muon(W0, G, M0, W_gpu, M_gpu, beta1, beta2, lr, wd, precision, kappa=1
     assert err <= NS_TOL[precision], f"Muon direction error {err:.3e} > {NS_TOL[precision]}"
     check_momentum(M0, G, M_gpu, beta2)
     return err
+
+
+def check_adamw(W0, G, m0, v0, W_gpu, m_gpu, v_gpu, step, cfg):
+    """AdamW tensors: weights and both moments within 1e-6 (max-norm and
+    Frobenius relative) of the fp64 oracle."""
+    w_ref, m_ref, v_ref = oracle.adamw_update(W0, G, m0, v0, step, cfg.adam_lr, cfg.adam_beta1,
+                                              cfg.adam_beta2, cfg.adam_eps, cfg.adam_wd)
+    for got, ref in ((W_gpu, w_ref), (m_gpu, m_ref), (v_gpu, v_ref)):
+        got = np.asarray(got, np.float64)
+        assert rel_max(got, ref) <= LION_TOL, rel_max(got, ref)
+        assert rel_fro(got, ref) <= LION_TOL, rel_fro(got, ref)

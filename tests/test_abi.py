@@ -46,6 +46,18 @@ def test_status_strings(lib):
         assert lib.lionmuon_status_string(code).decode() == name
 
 
+def test_config_schedule_fields(lib):
+    cfg = lm.config(ns_schedule=[(3.4445, -4.775, 2.0315)] * 3 + [(1.5, -0.5, 0.0)] * 2)
+    assert cfg.ns_steps == 5 and cfg.ns_schedule_steps == 5
+    assert tuple(cfg.ns_schedule[4]) == (1.5, -0.5, 0.0)
+    with pytest.raises(ValueError):
+        lm.config(ns_schedule=[(1.0, 0.0)])
+    bad = lm.config(ns_schedule=[(1.5, -0.5, 0.0)] * 2)
+    bad.ns_schedule[1][2] = float("nan")
+    with pytest.raises(lm.LionMuonError):
+        lm.lionmuon_workspace_bytes([(8, 8, False)], bad)
+
+
 def test_config_defaults(lib):
     cfg = lm.lm_config()
     lib.lionmuon_config_default(ctypes.byref(cfg))
@@ -192,9 +204,9 @@ def _step(lib, fl, t=1, P=2, b1=0.9, b2=0.99, lr=0.01, wd=0.1):
                              wd, None)
 
 
-def _step_ex(lib, fl, cfg, ws=None, ws_bytes=0, t=0, P=1):
+def _step_ex(lib, fl, cfg, ws=None, ws_bytes=0, t=0, P=1, v=None):
     return lib.lionmuon_step_ex(ctypes.cast(fl.p, ctypes.c_void_p), ctypes.cast(fl.g, ctypes.c_void_p),
-                                ctypes.cast(fl.m, ctypes.c_void_p), fl.shapes, fl.n, t, P, 0.9,
+                                ctypes.cast(fl.m, ctypes.c_void_p), v, fl.shapes, fl.n, t, P, 0.9,
                                 0.99, 0.1, ctypes.byref(cfg), ws, ws_bytes, None)
 
 
@@ -263,11 +275,39 @@ def test_step_ex_rejects_bad_configs_and_workspaces(lib):
     for bad in [dict(struct_size=4), dict(ns_steps=0), dict(ns_steps=65), dict(ns_precision=7),
                 dict(ns_scale_mode=3), dict(ns_eps=-1.0), dict(ns_a=float("nan")),
                 dict(lr_muon=-1.0), dict(lr_lion=float("nan")), dict(ns_bf16_min_side=-1),
-                dict(reserved=1)]:
+                dict(reserved=1), dict(reserved2=1), dict(ns_schedule_steps=4),
+                dict(ns_steps=17, ns_schedule_steps=17), dict(adam_beta1=1.0),
+                dict(adam_beta2=-0.5), dict(adam_lr=-1.0), dict(adam_eps=float("inf")),
+                dict(adam_wd=-0.1)]:
         assert _step_ex(lib, fl, cfg(**bad)) == INVALID, bad
     assert _step_ex(lib, fl, cfg(), ws=1 << 34, ws_bytes=0) == INVALID
     assert _step_ex(lib, fl, cfg(), ws=None, ws_bytes=4096) == INVALID
     assert _step_ex(lib, fl, cfg(), ws=(1 << 34) + 64, ws_bytes=1 << 20) == INVALID
+
+
+def test_adamw_tensors_need_second_moments(lib):
+    fl = FakeList([(1, 64, lm.LM_TENSOR_ADAMW)])
+    cfg = lm.config()
+    assert _step_ex(lib, fl, cfg) == INVALID                  # no second-moment array
+    assert "second-moment" in lib.lionmuon_last_error().decode()
+    assert _step(lib, fl) == INVALID                          # lionmuon_step has none
+    base = 1 << 35
+    v = (ctypes.c_void_p * 1)(fl.p[0] + 64)                   # overlaps params
+    assert _step_ex(lib, fl, cfg, v=ctypes.cast(v, ctypes.c_void_p)) == INVALID
+    fl2 = FakeList([(1, 64, lm.LM_TENSOR_ADAMW | lm.LM_TENSOR_LION_ONLY)])
+    v2 = (ctypes.c_void_p * 1)(base)
+    assert _step_ex(lib, fl2, cfg, v=ctypes.cast(v2, ctypes.c_void_p)) == INVALID
+
+
+def test_plan_info_counts_adamw_tensors(lib):
+    specs = [(768, 768, False), (1, 768, lm.LM_TENSOR_ADAMW), (1, 3072, lm.LM_TENSOR_ADAMW),
+             (64, 64, lm.LM_TENSOR_ADAMW), (1, 100, False)]
+    for t, P in [(0, 1), (1, 2)]:
+        info = lm.lionmuon_plan_info(specs, t=t, P=P)
+        assert info["n_adamw"] == 3 and info["adamw_elements"] == 768 + 3072 + 4096
+        assert info["lion_bytes"] == 20.0 * info["lion_elements"] + 28.0 * info["adamw_elements"]
+    assert lm.lionmuon_plan_info(specs, t=0, P=1)["n_muon"] == 1
+    assert lm.lionmuon_plan_info(specs, t=1, P=2)["n_lion"] == 2
 
 
 def test_ns_hook_rejects_bad_arguments(lib):

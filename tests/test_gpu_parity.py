@@ -12,7 +12,7 @@ import oracle
 import workloads
 from paper_2605_19811_amd import lionmuon as lm
 
-from parity import (NS_TOL, check_lion, check_momentum, check_muon,
+from parity import (NS_TOL, check_adamw, check_lion, check_momentum, check_muon,
                     muon_direction_error, rel_fro)
 
 pytestmark = pytest.mark.gpu
@@ -125,6 +125,17 @@ def test_ns_hook_cubic_coefficients_and_step_count():
     assert rel_fro(host(out), ref) <= 1e-4
 
 
+@pytest.mark.parametrize("precision", ["fp32", "bf16"])
+def test_ns_hook_per_step_schedule(precision):
+    """A per-step coefficient schedule (three quintic then two cubic steps)."""
+    sched = [oracle.QUINTIC] * 3 + [oracle.CUBIC] * 2
+    X = workloads.random_matrix(25, 192, 448, std=1e-2)
+    out = lm.lionmuon_ns(dev(X), lm.config(ns_precision=precision, ns_schedule=sched))
+    sync()
+    err = rel_fro(host(out), oracle.newton_schulz(X, 5, sched))
+    assert err <= NS_TOL[precision], err
+
+
 def test_ns_hook_largest_long_side():
     """The embedding shape (50257 x 1280), the largest matrix of the benchmark
     sets, through the Muon kernels (long side padded to 50304)."""
@@ -161,6 +172,47 @@ def test_mixed_list_muon_step(precision):
             check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_l, wd)
         else:
             check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_m, wd, precision)
+
+
+@pytest.mark.parametrize("t,P", [(0, 2), (1, 2), (5, 0)])
+def test_adamw_tensors_in_mixed_list(t, P):
+    """1-D tensors (and a matrix) flagged AdamW take AdamW every step
+    (Section 3's fallback), beside Lion and Muon tensors in one call."""
+    shapes = [(1, 768), (1, 4099), (96, 130), (256, 320), (1, 300)]
+    flags = [lm.LM_TENSOR_ADAMW, lm.LM_TENSOR_ADAMW, lm.LM_TENSOR_ADAMW, 0, 0]
+    W0, M0, G = _state(shapes, 61)
+    V0 = [np.abs(x).astype(np.float32) * 1e-2 for x in _state(shapes, 62)[2]]
+    W, M = [dev(x) for x in W0], [dev(x) for x in M0]
+    V = [dev(x) if f else None for x, f in zip(V0, flags)]
+    cfg = lm.config(ns_precision="fp32", lr_muon=0.01, lr_lion=1e-3, adam_wd=0.05)
+    lm.lionmuon_step_ex(W, [dev(g) for g in G], M, t, P, 0.9, 0.99, 0.1, cfg, lion_only=flags,
+                        second_moment=V)
+    sync()
+    for i, f in enumerate(flags):
+        if f:
+            check_adamw(W0[i], G[i], M0[i], V0[i], host(W[i]), host(M[i]), host(V[i]), t + 1, cfg)
+        elif oracle.is_muon_step(t, P) and min(shapes[i]) > 1:
+            check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 0.01, 0.1, "fp32")
+        else:
+            check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 1e-3, 0.1)
+
+
+def test_adamw_trajectory_bias_correction():
+    """Four AdamW steps from zero moments: the bias corrections follow the
+    step count t + 1."""
+    W0 = workloads.random_matrix(63, 1, 5000, std=0.02)[0]
+    W, M, V = dev(W0), torch.zeros(5000, device=DEV), torch.zeros(5000, device=DEV)
+    cfg = lm.config()
+    w, m, v = W0.astype(np.float64), np.zeros(5000), np.zeros(5000)
+    for t in range(4):
+        G = workloads.random_matrix([64, t], 1, 5000, std=1e-3)[0]
+        w_prev, m_prev, v_prev = host(W), host(M), host(V)
+        lm.lionmuon_step_ex([W], [dev(G)], [M], t, 2, 0.9, 0.99, 0.1, cfg,
+                            lion_only=[lm.LM_TENSOR_ADAMW], second_moment=[V])
+        sync()
+        check_adamw(w_prev, G, m_prev, v_prev, host(W), host(M), host(V), t + 1, cfg)
+        w, m, v = oracle.adamw_update(w, G, m, v, t + 1, 1e-3, 0.8, 0.999, 1e-8, 0.0)
+    assert rel_fro(host(W) - W0, w - W0) <= 1e-5
 
 
 def test_single768_four_steps():

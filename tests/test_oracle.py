@@ -25,9 +25,11 @@ def _golden(name):
 
 
 def _scalar_iterate(x, coeffs, steps):
-    """The scalar odd polynomial applied ``steps`` times to singular values."""
-    a, b, c = coeffs
-    for _ in range(steps):
+    """The scalar odd polynomial(s) applied ``steps`` times to singular
+    values; ``coeffs`` is one (a, b, c) or a list of per-step triples."""
+    sched = [coeffs] * steps if np.ndim(coeffs) == 1 else list(coeffs)
+    assert len(sched) == steps
+    for a, b, c in sched:
         x = a * x + b * x ** 3 + c * x ** 5
     return x
 
@@ -79,6 +81,30 @@ def test_ns_step_count_matches_closed_form(steps):
     got = oracle.newton_schulz(G, steps, oracle.QUINTIC, 1e-7)
     ref = _svd_closed_form(G, steps, oracle.QUINTIC, 1e-7)
     assert _rel(got, ref) < 1e-12
+
+
+SCHEDULES = {
+    "quintic3_cubic2": [oracle.QUINTIC] * 3 + [oracle.CUBIC] * 2,
+    "decreasing": [(3.0, -3.2, 1.2), (2.5, -2.0, 0.5), (2.0, -1.3, 0.3), (1.7, -0.8, 0.1),
+                   (1.5, -0.5, 0.0)],
+}
+
+
+@pytest.mark.parametrize("name", sorted(SCHEDULES))
+@pytest.mark.parametrize("shape", [(6, 9), (40, 24), (64, 64)])
+def test_ns_per_step_schedule_matches_closed_form(name, shape):
+    """Section 2: other odd-polynomial schedules (per-step coefficients) share
+    the cost structure; the oracle takes one triple per step."""
+    rng = np.random.default_rng([31, *shape])
+    G = rng.standard_normal(shape)
+    sched = SCHEDULES[name]
+    got = oracle.newton_schulz(G, 5, sched, 1e-7)
+    assert _rel(got, _svd_closed_form(G, 5, sched, 1e-7)) < 1e-12
+    # a constant schedule equals the single-triple form
+    assert np.array_equal(oracle.newton_schulz(G, 5, [oracle.QUINTIC] * 5),
+                          oracle.newton_schulz(G, 5, oracle.QUINTIC))
+    with pytest.raises(ValueError):
+        oracle.newton_schulz(G, 4, sched)
 
 
 @pytest.mark.parametrize("shape", [(3, 5), (6, 4), (8, 8)])
@@ -330,3 +356,49 @@ def test_stable_rank_estimate():
     assert oracle.stable_rank_estimate(G, power_steps=500) == pytest.approx(
         np.sum(s ** 2) / s[0] ** 2, rel=1e-8)
     assert oracle.stable_rank_estimate(np.zeros((3, 4))) == 0.0
+
+
+# --------------------------------------------------------------------------
+# AdamW fallback for 1-D parameters (Section 3, implementation notes; Table 3)
+# --------------------------------------------------------------------------
+def test_adamw_first_step_is_independent_of_betas():
+    """At step 1 from zero moments, bias correction gives mhat = g and
+    vhat = g^2 exactly, whatever the betas."""
+    rng = np.random.default_rng(40)
+    W, G = rng.standard_normal(50), rng.standard_normal(50)
+    G[3] = 0.0
+    Z = np.zeros(50)
+    lr, eps, wd = 1e-3, 1e-8, 0.05
+    expect = W - lr * (G / (np.abs(G) + eps) + wd * W)
+    for b1, b2 in [(0.8, 0.999), (0.9, 0.95), (0.0, 0.5)]:
+        w, m, v = oracle.adamw_update(W, G, Z, Z, 1, lr, b1, b2, eps, wd)
+        assert np.allclose(w, expect, rtol=0, atol=1e-15)
+        assert np.allclose(m, (1 - b1) * G) and np.allclose(v, (1 - b2) * G ** 2)
+
+
+def test_adamw_constant_gradient_gives_unit_steps():
+    """With a constant gradient the bias-corrected moments equal g and g^2
+    exactly at every step, so each update is lr * g / (|g| + eps)."""
+    g = np.array([0.3, -2.0, 1e-3, 5.0])
+    W = np.array([0.1, 0.2, -0.3, 0.4])
+    m = v = np.zeros(4)
+    lr, eps = 1e-3, 1e-8
+    for step in range(1, 8):
+        w_new, m, v = oracle.adamw_update(W, g, m, v, step, lr, 0.8, 0.999, eps, 0.0)
+        assert np.allclose(W - w_new, lr * g / (np.abs(g) + eps), rtol=1e-12, atol=0)
+        W = w_new
+
+
+def test_adamw_scale_invariance_and_zero_gradient():
+    rng = np.random.default_rng(41)
+    W, G1, G2 = rng.standard_normal(20), rng.standard_normal(20), rng.standard_normal(20)
+    Z = np.zeros(20)
+    a = oracle.adamw_update(W, G1, Z, Z, 1, 1e-3, 0.8, 0.999, 0.0, 0.0)
+    a = oracle.adamw_update(a[0], G2, a[1], a[2], 2, 1e-3, 0.8, 0.999, 0.0, 0.0)
+    b = oracle.adamw_update(W, 7 * G1, Z, Z, 1, 1e-3, 0.8, 0.999, 0.0, 0.0)
+    b = oracle.adamw_update(b[0], 7 * G2, b[1], b[2], 2, 1e-3, 0.8, 0.999, 0.0, 0.0)
+    assert _rel(a[0], b[0]) < 1e-13
+    w, m, v = oracle.adamw_update(W, Z, Z, Z, 3, 1e-3, 0.8, 0.999, 1e-8, 0.1)
+    assert np.allclose(w, W * (1 - 1e-4), rtol=1e-15, atol=0)
+    with pytest.raises(ValueError):
+        oracle.adamw_update(W, G1, Z, Z, 0, 1e-3, 0.8, 0.999, 1e-8, 0.0)
