@@ -199,20 +199,55 @@ def stable_rank_estimate(M: np.ndarray, power_steps: int = 10,
                          v0: np.ndarray | None = None) -> float:
     """r_hat(M) = ||M||_F^2 / sigma_hat_1(M)^2 (Appendix G, adaptive rule).
 
-    sigma_hat_1 is taken from ``power_steps`` power-iteration steps on M^T M
-    started from ``v0`` (all-ones when not given).
+    sigma_hat_1 comes from ``power_steps`` power-iteration steps on the Gram
+    matrix of the short side: with S = M when M is tall or square and
+    S = M^T when it is wide, v <- S^T S v / ||S^T S v|| from ``v0`` (length
+    min(m, n), all-ones when not given, scaled to unit norm), and then
+    sigma_hat_1 = ||S v||. The estimate is 0 when M = 0 or when an iterate
+    vanishes.
     """
     M = np.asarray(M, dtype=np.float64)
-    n = M.shape[1]
-    v = np.ones(n) if v0 is None else np.asarray(v0, dtype=np.float64)
+    S = M.T if M.shape[0] < M.shape[1] else M
+    s = S.shape[1]
+    v = np.ones(s) if v0 is None else np.asarray(v0, dtype=np.float64)
     v = v / np.linalg.norm(v)
     for _ in range(power_steps):
-        w = M.T @ (M @ v)
+        w = S.T @ (S @ v)
         nw = np.linalg.norm(w)
         if nw == 0.0:
             return 0.0
         v = w / nw
-    sigma1 = np.linalg.norm(M @ v)
+    sigma1 = np.linalg.norm(S @ v)
     if sigma1 == 0.0:
         return 0.0
     return float(np.linalg.norm(M, "fro") ** 2 / sigma1 ** 2)
+
+
+def adaptive_uses_muon(M: np.ndarray, alpha: float, power_steps: int) -> bool:
+    """Appendix G rule: the Muon step is taken on a matrix iff the stable rank
+    of its momentum, r_hat(M) = ||M||_F^2 / sigma_hat_1^2, is at most
+    alpha * min(m, n). M is the buffer before this step's update."""
+    M = np.asarray(M, dtype=np.float64)
+    return stable_rank_estimate(M, power_steps) <= alpha * min(M.shape)
+
+
+def lionmuon_adaptive_step(params, grads, moms, t, beta1, beta2, lr_muon, lr_lion, wd, alpha,
+                           power_steps, *, lion_only=None, **ns_kwargs):
+    """One step of the adaptive variant (Appendix G): each 2-D matrix that is
+    not Lion-only takes the Muon branch iff ``adaptive_uses_muon`` holds for
+    its current momentum, the Lion branch otherwise; 1-D and Lion-only
+    tensors take the Lion branch. Returns (W' list, M' list, decisions)."""
+    n = len(params)
+    lion_only = list(lion_only) if lion_only is not None else [False] * n
+    out_w, out_m, decisions = [], [], []
+    for W, G, M, lo in zip(params, grads, moms, lion_only):
+        M64 = np.asarray(M, dtype=np.float64)
+        eligible = M64.ndim == 2 and min(M64.shape) > 1 and not lo
+        muon = eligible and adaptive_uses_muon(M64, alpha, power_steps)
+        # P = 1 forces the Muon branch, P = 0 (infinity) the Lion branch
+        w, m = lionmuon_update(W, G, M, t, 1 if muon else 0, beta1, beta2, lr_muon, lr_lion, wd,
+                               lion_only=not muon, **ns_kwargs)
+        out_w.append(w)
+        out_m.append(m)
+        decisions.append(bool(muon))
+    return out_w, out_m, decisions

@@ -402,3 +402,64 @@ def test_adamw_scale_invariance_and_zero_gradient():
     assert np.allclose(w, W * (1 - 1e-4), rtol=1e-15, atol=0)
     with pytest.raises(ValueError):
         oracle.adamw_update(W, G1, Z, Z, 0, 1e-3, 0.8, 0.999, 1e-8, 0.0)
+
+
+# --------------------------------------------------------------------------
+# Adaptive Muon / Lion selection by stable rank (Appendix G)
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("shape", [(12, 20), (20, 12), (9, 9)])
+def test_stable_rank_power_iteration_closed_form(shape):
+    """With S the short-side view (M, or M^T for wide M), singular values sigma,
+    and c_i the start vector's components along S's right singular vectors V
+    (square, so nothing of v0 lies outside their span), k power steps give v_k
+    proportional to V diag(sigma^(2k)) c and sigma_hat^2 = sum (sigma_i coef_i)^2
+    / sum coef_i^2 with coef = sigma^(2k) c."""
+    rng = np.random.default_rng(42)
+    m, n = shape
+    s, l = min(m, n), max(m, n)
+    U, _ = np.linalg.qr(rng.standard_normal((l, l)))
+    V, _ = np.linalg.qr(rng.standard_normal((s, s)))
+    sig = np.linspace(3.0, 0.5, s)
+    S = (U[:, :s] * sig) @ V.T                      # l x s, singular values sig
+    M = S.T if m < n else S
+    c = V.T @ (np.ones(s) / np.sqrt(s))
+    for k in (0, 1, 3, 8):
+        coef = sig ** (2 * k) * c
+        sigma_hat2 = np.sum((sig * coef) ** 2) / np.sum(coef ** 2)
+        expect = np.sum(sig ** 2) / sigma_hat2
+        assert oracle.stable_rank_estimate(M, k) == pytest.approx(expect, rel=1e-12)
+    # a start vector along the top singular direction is exact at once
+    assert oracle.stable_rank_estimate(M, 0, v0=V[:, 0]) == pytest.approx(
+        np.sum(sig ** 2) / sig[0] ** 2, rel=1e-12)
+
+
+def test_stable_rank_degenerate_iterates():
+    """A start vector in the null space of S gives a vanishing iterate: the
+    estimate is 0, as for the zero matrix."""
+    M = np.array([[1.0, -1.0], [2.0, -2.0], [3.0, -3.0]])   # tall, S = M, v0 = ones
+    assert oracle.stable_rank_estimate(M, 0) == 0.0
+    assert oracle.stable_rank_estimate(M, 3) == 0.0
+    assert oracle.stable_rank_estimate(M.T, 3) == 0.0        # wide: S = M^T = M
+    assert oracle.stable_rank_estimate(M, 3, v0=np.array([1.0, 0.0])) == pytest.approx(1.0)
+
+
+def test_adaptive_rule_threshold_and_branches():
+    rng = np.random.default_rng(43)
+    m, n = 30, 50
+    u, v = rng.standard_normal(m), rng.standard_normal(n)
+    low = np.outer(u, v) + 1e-3 * rng.standard_normal((m, n))     # stable rank ~ 1
+    high = rng.standard_normal((m, n))                             # stable rank >> 1
+    r_low = oracle.stable_rank_estimate(low, 20)
+    assert 1.0 <= r_low < 1.01
+    assert oracle.adaptive_uses_muon(low, 0.05, 20)                # 1 <= 0.05 * 30
+    assert not oracle.adaptive_uses_muon(high, 0.05, 20)
+    assert oracle.adaptive_uses_muon(low, r_low / 30, 20)          # equality takes Muon
+    W = [rng.standard_normal((m, n)) * 0.02 for _ in range(3)] + [rng.standard_normal((1, 9))]
+    G = [rng.standard_normal(w.shape) * 1e-2 for w in W]
+    Ms = [low, high, low, rng.standard_normal((1, 9))]
+    w, mm, d = oracle.lionmuon_adaptive_step(W, G, Ms, 3, 0.9, 0.99, 0.02, 0.01, 0.1, 0.05, 20,
+                                             lion_only=[False, False, True, False])
+    assert d == [True, False, False, False]
+    ref_muon = oracle.lionmuon_update(W[0], G[0], Ms[0], 0, 1, 0.9, 0.99, 0.02, 0.01, 0.1)
+    ref_lion = oracle.lionmuon_update(W[1], G[1], Ms[1], 1, 0, 0.9, 0.99, 0.02, 0.01, 0.1)
+    assert np.array_equal(w[0], ref_muon[0]) and np.array_equal(w[1], ref_lion[0])
