@@ -52,7 +52,7 @@ def load_traffic(workload, kernel):
 
 PHASE_OF_KERNEL = (("lion_kernel", "lion"), ("prep_kernel", "prep"), ("norm_kernel", "norm"),
                    ("ns_gram_kernel", "gram"), ("ns_poly_kernel", "poly"),
-                   ("ns_apply_kernel", "apply"))
+                   ("ns_apply_kernel", "apply"), ("srank_", "srank"))
 
 
 def phase_of(kernel_name):
@@ -201,6 +201,9 @@ def main():
     ap.add_argument("--workload", default="gpt2-124m", choices=sorted(workloads.WORKLOADS))
     ap.add_argument("--P", type=int, default=2, help="period; 0 = pure Lion")
     ap.add_argument("--pure-muon", action="store_true", help="P=1 with beta1=beta2=0.9")
+    ap.add_argument("--adaptive", type=float, default=0.0, metavar="ALPHA",
+                    help="stable-rank rule of Appendix G with this alpha instead of the period")
+    ap.add_argument("--power-steps", type=int, default=5, help="power-iteration steps (adaptive)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without per-launch events (no roofline object)")
@@ -242,17 +245,21 @@ def main():
     wl = workloads.get(args.workload)
     P = 1 if args.pure_muon else args.P
     beta1, beta2 = (0.9, 0.9) if args.pure_muon else (wl.beta1, wl.beta2)
+    adaptive = args.adaptive > 0.0
     steps = args.steps
-    if P > 1 and steps % P:
+    if P > 1 and steps % P and not adaptive:
         steps += P - steps % P                 # whole periods only
     dev = torch.device("cuda:0")
     params, moms, grad_sets = workloads.device_state(torch, wl, dev, seed=7, warm=True, n_grad=2)
     lion_only = [t.lion_only for t in wl.tensors]
     lists = [lm.TensorList(params, g, moms, lion_only) for g in grad_sets]
-    cfg = lm.config(ns_precision=wl.ns_precision, lr_muon=wl.lr_muon, lr_lion=wl.lr_lion)
+    cfg = lm.config(ns_precision=wl.ns_precision, lr_muon=wl.lr_muon, lr_lion=wl.lr_lion,
+                    adaptive_alpha=args.adaptive, adaptive_power_steps=args.power_steps)
+    cfg_period = lm.config(ns_precision=wl.ns_precision, lr_muon=wl.lr_muon, lr_lion=wl.lr_lion)
     specs = [(t.rows, t.cols, t.lion_only) for t in wl.tensors]
-    info_muon = lm.lionmuon_plan_info(specs, 0, 1, cfg)
-    info_lion = lm.lionmuon_plan_info(specs, 1, 2, cfg)
+    info_muon = lm.lionmuon_plan_info(specs, 0, 1, cfg_period)
+    info_lion = lm.lionmuon_plan_info(specs, 1, 2, cfg_period)
+    info_adaptive = lm.lionmuon_plan_info(specs, 0, 0, cfg) if adaptive else None
     stream = torch.cuda.current_stream()
 
     def run(t0, n):
@@ -282,7 +289,17 @@ def main():
         phases = lm.lionmuon_profiling_read()
         lm.lionmuon_profiling_enable(False)
 
-    n_muon_steps = sum(1 for k in range(steps) if P >= 1 and (t_start + k) % P == 0)
+    muon_fraction = None
+    if adaptive:
+        # decisions of one further step (after the timed region)
+        dec = torch.zeros(len(wl.tensors), dtype=torch.int32, device=dev)
+        lm.lionmuon_step_adaptive(None, None, None, t_start + steps, beta1, beta2, wl.wd, cfg,
+                                  stream=stream, tensors=lists[0], decisions=dec)
+        torch.cuda.synchronize()
+        muon_fraction = round(float(dec.sum().item()) / info_adaptive["n_muon"], 4)
+        n_muon_steps = 0
+    else:
+        n_muon_steps = sum(1 for k in range(steps) if P >= 1 and (t_start + k) % P == 0)
     n_lion_steps = steps - n_muon_steps
     out = {
         "metric": "amortised optimizer-step ms per period P (LionMuon step, 1 GPU)",
@@ -297,12 +314,18 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if wl.ns_precision == "bf16" else "f32",
         "data": "synthetic (seeded gradients of the workload's shapes; random-init weights)",
-        "config": {"workload": wl.name, "P": P, "beta1": beta1, "beta2": beta2,
+        "config": {"workload": wl.name, "P": None if adaptive else P, "beta1": beta1,
+                   "beta2": beta2,
                    "n_tensors": len(wl.tensors), "elements": wl.numel,
                    "muon_elements": info_muon["muon_elements"],
                    "ns_precision": wl.ns_precision, "ns_steps": 5,
                    "state": "fp32 W, M, G; bf16 MFMA Newton-Schulz with fp32 accumulation"},
     }
+    if adaptive:
+        out["metric"] = "optimizer-step ms (adaptive LionMuon step, Appendix G rule, 1 GPU)"
+        out["config"].update({"rule": "adaptive stable rank", "alpha": args.adaptive,
+                              "power_steps": args.power_steps,
+                              "muon_fraction_after_timing": muon_fraction})
     if phases is not None:
         flops = ns_flops_per_launch(wl)
         ph = {}
@@ -311,10 +334,13 @@ def main():
                 continue
             avg = v["ms"] / v["launches"]
             entry = {"launches": v["launches"], "avg_ms": round(avg, 5)}
-            if name in flops:
+            if name in flops and not adaptive:   # adaptive: NS work depends on the decisions
                 entry["tflops"] = round(flops[name] / (avg * 1e-3) / 1e12, 1)
                 entry["frac_bf16_peak"] = round(entry["tflops"] / BF16_PEAK_TFLOPS, 4)
-            if name == "lion":
+            if name == "srank":
+                entry["gbps"] = round(info_adaptive["srank_bytes"] / (avg * 1e-3) / 1e9, 1)
+                entry["frac_hbm_peak"] = round(entry["gbps"] / HBM_PEAK_GBPS, 4)
+            if name == "lion" and not adaptive:
                 # Lion steps update every tensor; Muon steps only the Lion-only ones
                 lion_elems = n_lion_steps * info_lion["lion_elements"]
                 if n_muon_steps and info_muon["lion_elements"]:
@@ -329,7 +355,7 @@ def main():
             out["ns_tflops"] = round(info_muon["ns_flops"] * n_muon_steps / (ns_ms * 1e-3) / 1e12, 1)
             out["ns_frac_bf16_peak"] = round(out["ns_tflops"] / BF16_PEAK_TFLOPS, 4)
             out["ns_ms_per_muon_step"] = round(ns_ms / n_muon_steps, 4)
-        if "lion" in ph:
+        if "lion" in ph and "gbps" in ph["lion"]:
             out["lion_gbps"] = ph["lion"]["gbps"]
             out["lion_frac_hbm_peak"] = ph["lion"]["frac_hbm_peak"]
         # dominant kernel: most total time in the timed region
@@ -337,11 +363,11 @@ def main():
         d = ph[dom]
         kernel_names = {"lion": "lion_kernel", "prep": "prep_kernel", "norm": "norm_kernel",
                         "gram": "ns_gram_kernel<bf16>", "poly": "ns_poly_kernel<bf16>",
-                        "apply": "ns_apply_kernel<bf16>"}
-        if dom in flops:
+                        "apply": "ns_apply_kernel<bf16>", "srank": "srank_pass+reduce+decide"}
+        if "tflops" in d:
             roof = {"kernel": kernel_names[dom], "bound": "mfma", "achieved": d["tflops"],
                     "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": d["frac_bf16_peak"]}
-        elif dom == "lion":
+        elif "gbps" in d:
             roof = {"kernel": kernel_names[dom], "bound": "hbm", "achieved": d["gbps"],
                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": d["frac_hbm_peak"]}
         else:
@@ -350,7 +376,7 @@ def main():
         roof["avg_launch_ms"] = d["avg_ms"]
         roof["traffic"] = load_traffic(wl.name, dom)
         out["roofline"] = roof
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not adaptive:
         out["cpu_baseline"] = cpu_baseline(wl, P)
     print(json.dumps(out), flush=True)
 

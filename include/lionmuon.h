@@ -21,6 +21,17 @@
  *   rows <= cols; each step A = X X^T, B = b*A + c*A A, X <- a*X + B X.
  * kappa is 1 (Algorithm 1) or 0.2*sqrt(max(m, n)) (Table 3 "NS scaling").
  *
+ * Adaptive variant (Appendix G; lm_config.adaptive_alpha > 0): instead of the
+ * period P, each 2-D tensor that is not Lion-only or AdamW takes the Muon
+ * branch on a step iff the stable-rank estimate of its momentum (the buffer
+ * before this step's update),
+ *   r_hat(M) = ||M||_F^2 / sigma_hat_1(M)^2 <= adaptive_alpha * min(m, n),
+ * and the Lion branch otherwise. sigma_hat_1 = ||S v_k|| after k =
+ * adaptive_power_steps power-iteration steps v <- S^T S v / ||S^T S v|| from
+ * v_0 = ones / sqrt(min(m, n)), where S = M if rows >= cols, else M^T; an
+ * iterate that vanishes, or M = 0, gives r_hat = 0. The estimate is computed
+ * in fp64 on the device and the decision never leaves it.
+ *
  * Conventions shared by every entry point:
  *  - Pointer arrays (params, grads, momentum, shapes) live in HOST memory;
  *    the pointers they hold are DEVICE pointers to fp32, contiguous,
@@ -48,7 +59,7 @@
 extern "C" {
 #endif
 
-#define LIONMUON_ABI_VERSION 1
+#define LIONMUON_ABI_VERSION 2
 
 typedef enum lm_status {
   LM_OK = 0,
@@ -116,6 +127,12 @@ typedef struct lm_config {
    * adam_eps) + adam_wd W), bias corrections with AdamW step t + 1.
    * Defaults (1e-3, 0.8, 0.999, 1e-8, 0). */
   double adam_lr, adam_beta1, adam_beta2, adam_eps, adam_wd;
+  /* Adaptive Muon / Lion choice (Appendix G): 0 (default) = off, the period
+   * P decides; in (0, 1] = threshold alpha of the stable-rank rule, P is then
+   * ignored (the Appendix G sweep uses 0.002 ... 0.01). */
+  double adaptive_alpha;
+  int32_t adaptive_power_steps;  /* power-iteration steps k in [0, 64], default 5 */
+  int32_t reserved3;             /* must be 0                                      */
 } lm_config;
 
 #define LM_MAX_NS_SCHEDULE 16
@@ -149,6 +166,8 @@ lm_status lionmuon_step(float* const* params, const float* const* grads,
  * workspace; otherwise workspace must hold at least
  * lionmuon_workspace_bytes(...) bytes, be 256-byte aligned, stay valid until
  * the enqueued work finishes, and must not be used by a concurrent call.
+ * With cfg->adaptive_alpha > 0 the step is the adaptive variant (P ignored,
+ * but still checked >= 0).
  */
 lm_status lionmuon_step_ex(float* const* params, const float* const* grads,
                            float* const* momentum, float* const* second_moment,
@@ -158,8 +177,28 @@ lm_status lionmuon_step_ex(float* const* params, const float* const* grads,
                            void* workspace, size_t workspace_bytes,
                            hipStream_t stream);
 
-/* Device workspace (bytes) a Muon step over these tensors needs with cfg
- * (NULL = defaults). A Lion step needs none. Host-only; no HIP call. */
+/*
+ * One step of the adaptive variant (Appendix G) with per-tensor diagnostics:
+ * lionmuon_step_ex with cfg->adaptive_alpha in (0, 1] (required here), plus
+ *   decisions:   optional device int32[n_tensors]: 1 where the tensor took the
+ *                Muon branch this step, else 0;
+ *   stable_rank: optional device double[n_tensors]: r_hat(M) of each Muon
+ *                candidate, -1 for every other tensor (1-D, Lion-only, AdamW,
+ *                empty).
+ * Both are written on `stream`; either may be NULL. Every matrix that may take
+ * the Muon branch keeps Newton-Schulz workspace (lionmuon_workspace_bytes with
+ * the same cfg).
+ */
+lm_status lionmuon_step_adaptive(float* const* params, const float* const* grads,
+                                 float* const* momentum, float* const* second_moment,
+                                 const lm_shape* shapes, int32_t n_tensors, int64_t t,
+                                 double beta1, double beta2, double wd, const lm_config* cfg,
+                                 void* workspace, size_t workspace_bytes, int32_t* decisions,
+                                 double* stable_rank, hipStream_t stream);
+
+/* Device workspace (bytes) a Muon step -- or, with cfg->adaptive_alpha > 0,
+ * an adaptive step -- over these tensors needs with cfg (NULL = defaults).
+ * A Lion step needs none. Host-only; no HIP call. */
 lm_status lionmuon_workspace_bytes(const lm_shape* shapes, int32_t n_tensors,
                                    const lm_config* cfg, size_t* out_bytes);
 
@@ -175,7 +214,10 @@ lm_status lionmuon_ns(const float* X, float* O, int64_t rows, int64_t cols,
                       int32_t batch, const lm_config* cfg, void* workspace,
                       size_t workspace_bytes, hipStream_t stream);
 
-/* Host-side description of the work one step would enqueue (no HIP call). */
+/* Host-side description of the work one step would enqueue (no HIP call).
+ * With cfg->adaptive_alpha > 0, n_muon / muon_elements count the Muon
+ * candidates (each takes Muon or Lion on the device), n_lion / lion_elements
+ * the tensors that always take the Lion branch. */
 typedef struct lm_plan_info {
   int32_t n_tensors;        /* non-empty tensors                               */
   int32_t n_lion;           /* tensors updated by the Lion branch this step    */
@@ -192,6 +234,9 @@ typedef struct lm_plan_info {
   double ns_flops_dense;    /* dense convention K * sum 4 s^2 l + 2 s^3        */
   double lion_bytes;        /* 20 bytes per Lion-branch element, 28 per AdamW   */
   size_t workspace_bytes;   /* device workspace this step needs                */
+  double srank_bytes;       /* adaptive: algorithmic bytes of the stable-rank
+                               passes, 4 (k+1) per candidate element plus 16 k
+                               per fp64 partial product; else 0               */
 } lm_plan_info;
 
 lm_status lionmuon_plan_info(const lm_shape* shapes, int32_t n_tensors,
@@ -207,7 +252,8 @@ lm_status lionmuon_plan_info(const lm_shape* shapes, int32_t n_tensors,
  */
 enum { LM_PHASE_LION = 0, LM_PHASE_PREP = 1, LM_PHASE_NORM = 2,
        LM_PHASE_GRAM = 3, LM_PHASE_POLY = 4, LM_PHASE_APPLY = 5,
-       LM_PHASE_COUNT = 6 };
+       LM_PHASE_SRANK = 6,   /* adaptive: stable-rank passes and decisions */
+       LM_PHASE_COUNT = 7 };
 typedef struct lm_phase_times {
   double ms[LM_PHASE_COUNT];
   int64_t launches[LM_PHASE_COUNT];

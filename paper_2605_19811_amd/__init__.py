@@ -9,12 +9,13 @@ from .lionmuon import (LM_NS_BF16, LM_NS_FP32, LM_NS_SCALE_NONE, LM_NS_SCALE_RMS
                        library, lionmuon_abi_version, lionmuon_ns, lionmuon_plan_info,
                        lionmuon_profiling_enable, lionmuon_profiling_read,
                        lionmuon_profiling_reset, lionmuon_release, lionmuon_step,
-                       lionmuon_step_ex, lionmuon_workspace_bytes)
+                       lionmuon_step_adaptive, lionmuon_step_ex, lionmuon_workspace_bytes)
 
 __all__ = [
     "LM_NS_BF16", "LM_NS_FP32", "LM_NS_SCALE_NONE", "LM_NS_SCALE_RMS02",
     "LM_TENSOR_ADAMW", "LM_TENSOR_LION_ONLY", "LionMuonError", "TensorList", "config", "library",
     "lionmuon_abi_version", "lionmuon_ns", "lionmuon_plan_info",
     "lionmuon_profiling_enable", "lionmuon_profiling_read", "lionmuon_profiling_reset",
-    "lionmuon_release", "lionmuon_step", "lionmuon_step_ex", "lionmuon_workspace_bytes",
+    "lionmuon_release", "lionmuon_step", "lionmuon_step_adaptive", "lionmuon_step_ex",
+    "lionmuon_workspace_bytes",
 ]

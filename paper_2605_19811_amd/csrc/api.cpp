@@ -52,6 +52,9 @@ struct DevicePlan {
   int32_t* d_lion_start = nullptr;
   lm::MuonMat* d_mats = nullptr;
   int32_t* d_prep_start = nullptr;
+  int32_t* d_sr_start = nullptr;
+  int32_t* d_rd_start = nullptr;
+  int32_t* d_tensor_mat = nullptr;
   lm::GemmTask* d_tasks[2][3] = {};   // [precision][gram, poly, apply]
   lm::XcdSplit* d_splits = nullptr;   // [precision * 3 + stage]
 
@@ -105,15 +108,15 @@ void place(std::vector<T>& v, size_t* off, std::vector<std::pair<size_t, std::pa
   *off = align256(*off + v.size() * sizeof(T));
 }
 
-lm_status get_plan(const TensorIn* x, int32_t n, bool muon, lm::NsPrecision prec, bool rms02,
-                   hipStream_t stream, std::shared_ptr<DevicePlan>* out) {
+lm_status get_plan(const TensorIn* x, int32_t n, lm::StepKind kind, lm::NsPrecision prec,
+                   bool rms02, hipStream_t stream, std::shared_ptr<DevicePlan>* out) {
   int device = 0;
   hipError_t e = hipGetDevice(&device);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   std::vector<uint8_t> key;
   key.reserve(size_t(n) * sizeof(TensorIn) + 16);
-  const int32_t hdr[5] = {device, muon ? 1 : 0, prec.all_fp32 ? 1 : 0, prec.bf16_min_side,
-                          rms02 ? 1 : 0};
+  const int32_t hdr[5] = {device, static_cast<int32_t>(kind), prec.all_fp32 ? 1 : 0,
+                          prec.bf16_min_side, rms02 ? 1 : 0};
   append_key(&key, hdr, sizeof(hdr));
   append_key(&key, x, size_t(n) * sizeof(TensorIn));
   for (auto it = g_plans.begin(); it != g_plans.end(); ++it) {
@@ -131,7 +134,7 @@ lm_status get_plan(const TensorIn* x, int32_t n, bool muon, lm::NsPrecision prec
   dp->device = device;
   dp->key = std::move(key);
   std::string err;
-  Status st = lm::build_plan(x, n, muon, prec, rms02, &dp->plan, &err);
+  Status st = lm::build_plan(x, n, kind, prec, rms02, &dp->plan, &err);
   if (st != Status::kOk) return fail(to_c(st), err);
   Plan& p = dp->plan;
   std::vector<std::pair<size_t, std::pair<const void*, size_t>>> parts;
@@ -140,6 +143,9 @@ lm_status get_plan(const TensorIn* x, int32_t n, bool muon, lm::NsPrecision prec
   const size_t o_lion_start = off; place(p.lion_block_start, &off, &parts);
   const size_t o_mats = off;       place(p.mats, &off, &parts);
   const size_t o_prep = off;       place(p.prep_start, &off, &parts);
+  const size_t o_sr = off;         place(p.sr_start, &off, &parts);
+  const size_t o_rd = off;         place(p.rd_start, &off, &parts);
+  const size_t o_tm = off;         place(p.tensor_mat, &off, &parts);
   size_t o_tasks[2][3];
   std::vector<lm::XcdSplit> splits;
   for (int pr = 0; pr < 2; ++pr) {
@@ -172,6 +178,9 @@ lm_status get_plan(const TensorIn* x, int32_t n, bool muon, lm::NsPrecision prec
   dp->d_lion_start = reinterpret_cast<int32_t*>(base + o_lion_start);
   dp->d_mats = reinterpret_cast<lm::MuonMat*>(base + o_mats);
   dp->d_prep_start = reinterpret_cast<int32_t*>(base + o_prep);
+  dp->d_sr_start = reinterpret_cast<int32_t*>(base + o_sr);
+  dp->d_rd_start = reinterpret_cast<int32_t*>(base + o_rd);
+  dp->d_tensor_mat = reinterpret_cast<int32_t*>(base + o_tm);
   for (int pr = 0; pr < 2; ++pr)
     for (int st3 = 0; st3 < 3; ++st3)
       dp->d_tasks[pr][st3] = reinterpret_cast<lm::GemmTask*>(base + o_tasks[pr][st3]);
@@ -258,16 +267,62 @@ lm::StepConsts step_consts(double beta1, double beta2, double wd, double lr_muon
   return k;
 }
 
+// Optional per-input-tensor outputs of the adaptive step (device pointers).
+struct AdaptiveOut {
+  int32_t* decisions = nullptr;
+  double* srank = nullptr;
+};
+
 lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config& cfg, void* ws,
-                  bool store_o, hipStream_t stream) {
+                  bool store_o, const AdaptiveOut& aout, hipStream_t stream) {
   const Plan& p = dp.plan;
-  hipError_t e;
+  hipError_t e = hipSuccess;
+  uint8_t* wsb = static_cast<uint8_t*>(ws);
+  int32_t* decide = nullptr;
+  if (p.adaptive && !p.mats.empty()) {
+    // Appendix G: stable rank of each candidate's momentum, before this
+    // step updates it, and the per-matrix decision, all on the device.
+    decide = reinterpret_cast<int32_t*>(wsb + p.ws_decide_off);
+    lm::SrankLaunch sl;
+    sl.mats = dp.d_mats;
+    sl.sr_start = dp.d_sr_start;
+    sl.rd_start = dp.d_rd_start;
+    sl.tensor_mat = dp.d_tensor_mat;
+    sl.n_mats = int32_t(p.mats.size());
+    sl.n_blocks = p.sr_start.back();
+    sl.n_chunks = p.rd_start.back();
+    sl.n_inputs = int32_t(p.tensor_mat.size());
+    sl.ws = ws;
+    sl.decide = decide;
+    sl.decisions_out = aout.decisions;
+    sl.srank_out = aout.srank;
+    sl.alpha = cfg.adaptive_alpha;
+    Timer t(stream, LM_PHASE_SRANK);
+    const int steps = cfg.adaptive_power_steps;
+    for (int i = 0; i <= steps && e == hipSuccess; ++i) {
+      e = lm::launch_srank_pass(sl, i == 0, i == steps, stream);
+      if (e == hipSuccess && i < steps) e = lm::launch_srank_reduce(sl, stream);
+    }
+    if (e == hipSuccess) e = lm::launch_srank_decide(sl, stream);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "stable-rank kernel launch");
+  } else if (p.adaptive && (aout.decisions || aout.srank)) {
+    // no candidate matrix: every output entry says "not a candidate"
+    lm::SrankLaunch sl{};
+    sl.tensor_mat = dp.d_tensor_mat;
+    sl.n_inputs = int32_t(p.tensor_mat.size());
+    sl.decisions_out = aout.decisions;
+    sl.srank_out = aout.srank;
+    e = lm::launch_srank_decide(sl, stream);
+    if (e != hipSuccess) return hip_fail(e, "stable-rank kernel launch");
+  }
   if (!p.lion.empty()) {
     lm::LionLaunch l;
     l.tensors = dp.d_lion;
     l.block_start = dp.d_lion_start;
     l.n_tensors = int32_t(p.lion.size());
     l.n_blocks = p.lion_block_start.back();
+    l.decide = decide;
     l.k = k;
     Timer t(stream, LM_PHASE_LION);
     e = lm::launch_lion(l, stream);
@@ -275,7 +330,6 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
     if (e != hipSuccess) return hip_fail(e, "lion kernel launch");
   }
   if (p.mats.empty()) return LM_OK;
-  uint8_t* wsb = static_cast<uint8_t*>(ws);
   float* partials = reinterpret_cast<float*>(wsb + p.ws_partials_off);
   float* rscale = reinterpret_cast<float*>(wsb + p.ws_rscale_off);
   lm::PrepLaunch pl;
@@ -286,6 +340,7 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
   pl.ws = ws;
   pl.partials = partials;
   pl.rscale = rscale;
+  pl.decide = decide;
   pl.k = k;
   {
     Timer t(stream, LM_PHASE_PREP);
@@ -306,6 +361,7 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
   gl.store_o = store_o ? 1 : 0;
   gl.lr = k.lr_muon;
   gl.wd = k.wd;
+  gl.decide = decide;
   const lm::GemmMode modes[3] = {lm::kGram, lm::kPoly, lm::kApply};
   const int phases[3] = {LM_PHASE_GRAM, LM_PHASE_POLY, LM_PHASE_APPLY};
   for (int it = 0; it < cfg.ns_steps; ++it) {
@@ -355,6 +411,11 @@ lm_status check_config(const lm_config* cfg) {
   if (!(cfg->adam_lr >= 0.0) || !std::isfinite(cfg->adam_lr) || !(cfg->adam_eps >= 0.0) ||
       !std::isfinite(cfg->adam_eps) || !(cfg->adam_wd >= 0.0) || !std::isfinite(cfg->adam_wd))
     return fail(LM_ERR_INVALID_ARGUMENT, "adam_lr, adam_eps and adam_wd must be finite and >= 0");
+  if (!(cfg->adaptive_alpha >= 0.0 && cfg->adaptive_alpha <= 1.0))
+    return fail(LM_ERR_INVALID_ARGUMENT, "adaptive_alpha must be 0 (off) or lie in (0, 1]");
+  if (cfg->adaptive_power_steps < 0 || cfg->adaptive_power_steps > 64)
+    return fail(LM_ERR_INVALID_ARGUMENT, "adaptive_power_steps must lie in [0, 64]");
+  if (cfg->reserved3 != 0) return fail(LM_ERR_INVALID_ARGUMENT, "lm_config reserved fields must be 0");
   if (cfg->ns_schedule_steps != 0) {
     if (cfg->ns_schedule_steps != cfg->ns_steps || cfg->ns_steps > LM_MAX_NS_SCHEDULE)
       return fail(LM_ERR_INVALID_ARGUMENT,
@@ -365,6 +426,11 @@ lm_status check_config(const lm_config* cfg) {
           return fail(LM_ERR_INVALID_ARGUMENT, "ns_schedule coefficients must be finite");
   }
   return LM_OK;
+}
+
+lm::StepKind step_kind(const lm_config& cfg, int64_t t, int32_t P) {
+  if (cfg.adaptive_alpha > 0.0) return lm::StepKind::kAdaptive;
+  return lm::is_muon_step(t, P) ? lm::StepKind::kMuon : lm::StepKind::kLion;
 }
 
 lm::NsPrecision precision_of(const lm_config& cfg) {
@@ -394,7 +460,7 @@ lm_status step_impl(float* const* params, const float* const* grads, float* cons
                     float* const* second_moment, const lm_shape* shapes, int32_t n, int64_t t,
                     int32_t P, double beta1,
                     double beta2, double wd, const lm_config* cfg, void* workspace,
-                    size_t workspace_bytes, hipStream_t stream) {
+                    size_t workspace_bytes, const AdaptiveOut& aout, hipStream_t stream) {
   if (cfg == nullptr) return fail(LM_ERR_INVALID_ARGUMENT, "null config");
   lm_status cs = check_config(cfg);
   if (cs != LM_OK) return cs;
@@ -413,13 +479,14 @@ lm_status step_impl(float* const* params, const float* const* grads, float* cons
   if (st != Status::kOk) return fail(to_c(st), err);
   bool any = false;
   for (const TensorIn& ti : x) any = any || (ti.rows > 0 && ti.cols > 0);
-  if (!any) return LM_OK;                          // only empty tensors: nothing to do
-  const bool muon = lm::is_muon_step(t, P);
+  const lm::StepKind kind = step_kind(*cfg, t, P);
+  if (!any && !(kind == lm::StepKind::kAdaptive && (aout.decisions || aout.srank)))
+    return LM_OK;                                  // only empty tensors: nothing to do
   const bool rms02 = cfg->ns_scale_mode == LM_NS_SCALE_RMS02;
 
   std::lock_guard<std::mutex> lock(g_mu);
   std::shared_ptr<DevicePlan> dp;
-  lm_status s = get_plan(x.data(), n, muon, precision_of(*cfg), rms02, stream, &dp);
+  lm_status s = get_plan(x.data(), n, kind, precision_of(*cfg), rms02, stream, &dp);
   if (s != LM_OK) return s;
   void* ws = workspace;
   if (dp->plan.ws_bytes > 0) {
@@ -432,7 +499,7 @@ lm_status step_impl(float* const* params, const float* const* grads, float* cons
     }
   }
   return enqueue(*dp, step_consts(beta1, beta2, wd, cfg->lr_muon, cfg->lr_lion, cfg->ns_eps, cfg, t),
-                 *cfg, ws, false, stream);
+                 *cfg, ws, false, aout, stream);
 }
 
 }  // namespace
@@ -461,6 +528,9 @@ void lionmuon_config_default(lm_config* cfg) {
   cfg->adam_beta2 = 0.999;
   cfg->adam_eps = 1e-8;
   cfg->adam_wd = 0.0;
+  cfg->adaptive_alpha = 0.0;
+  cfg->adaptive_power_steps = 5;
+  cfg->reserved3 = 0;
 }
 
 lm_status lionmuon_step(float* const* params, const float* const* grads, float* const* momentum,
@@ -471,7 +541,7 @@ lm_status lionmuon_step(float* const* params, const float* const* grads, float* 
   cfg.lr_muon = lr;
   cfg.lr_lion = lr;
   return step_impl(params, grads, momentum, nullptr, shapes, n_tensors, t, P, beta1, beta2, wd,
-                   &cfg, nullptr, 0, stream);
+                   &cfg, nullptr, 0, AdaptiveOut(), stream);
 }
 
 lm_status lionmuon_step_ex(float* const* params, const float* const* grads, float* const* momentum,
@@ -480,7 +550,31 @@ lm_status lionmuon_step_ex(float* const* params, const float* const* grads, floa
                            const lm_config* cfg, void* workspace, size_t workspace_bytes,
                            hipStream_t stream) {
   return step_impl(params, grads, momentum, second_moment, shapes, n_tensors, t, P, beta1, beta2,
-                   wd, cfg, workspace, workspace_bytes, stream);
+                   wd, cfg, workspace, workspace_bytes, AdaptiveOut(), stream);
+}
+
+lm_status lionmuon_step_adaptive(float* const* params, const float* const* grads,
+                                 float* const* momentum, float* const* second_moment,
+                                 const lm_shape* shapes, int32_t n_tensors, int64_t t, double beta1,
+                                 double beta2, double wd, const lm_config* cfg, void* workspace,
+                                 size_t workspace_bytes, int32_t* decisions, double* stable_rank,
+                                 hipStream_t stream) {
+  if (cfg == nullptr) return fail(LM_ERR_INVALID_ARGUMENT, "null config");
+  if (!(cfg->adaptive_alpha > 0.0))
+    return fail(LM_ERR_INVALID_ARGUMENT, "lionmuon_step_adaptive needs adaptive_alpha in (0, 1]");
+  if (n_tensors > 0) {
+    const uintptr_t d = reinterpret_cast<uintptr_t>(decisions);
+    const uintptr_t r = reinterpret_cast<uintptr_t>(stable_rank);
+    if ((d & 3u) || (r & 7u))
+      return fail(LM_ERR_INVALID_ARGUMENT, "decisions / stable_rank must be int32 / fp64 aligned");
+    if (d && r && d < r + uintptr_t(n_tensors) * 8u && r < d + uintptr_t(n_tensors) * 4u)
+      return fail(LM_ERR_INVALID_ARGUMENT, "decisions and stable_rank overlap");
+  }
+  AdaptiveOut aout;
+  aout.decisions = n_tensors > 0 ? decisions : nullptr;
+  aout.srank = n_tensors > 0 ? stable_rank : nullptr;
+  return step_impl(params, grads, momentum, second_moment, shapes, n_tensors, t, 0, beta1, beta2,
+                   wd, cfg, workspace, workspace_bytes, aout, stream);
 }
 
 lm_status lionmuon_workspace_bytes(const lm_shape* shapes, int32_t n_tensors, const lm_config* cfg,
@@ -523,12 +617,12 @@ lm_status lionmuon_plan_info(const lm_shape* shapes, int32_t n, int64_t t, int32
   Status st = lm::validate_tensors(x.data(), n, &err);
   if (st != Status::kOk) return fail(to_c(st), err);
   Plan p;
-  st = lm::build_plan(x.data(), n, lm::is_muon_step(t, P), precision_of(*cfg),
+  st = lm::build_plan(x.data(), n, step_kind(*cfg, t, P), precision_of(*cfg),
                       cfg->ns_scale_mode == LM_NS_SCALE_RMS02, &p, &err);
   if (st != Status::kOk) return fail(to_c(st), err);
   std::memset(out, 0, sizeof(*out));
   out->n_tensors = p.n_tensors;
-  out->n_lion = int32_t(p.lion.size()) - p.n_adamw;
+  out->n_lion = int32_t(p.lion.size()) - p.n_adamw - (p.adaptive ? int32_t(p.mats.size()) : 0);
   out->n_adamw = p.n_adamw;
   out->adamw_elements = p.adamw_elements;
   out->n_muon = int32_t(p.mats.size());
@@ -542,6 +636,14 @@ lm_status lionmuon_plan_info(const lm_shape* shapes, int32_t n, int64_t t, int32
   out->ns_flops_dense = lm::ns_flops_dense(p, cfg->ns_steps);
   out->lion_bytes = 20.0 * double(p.lion_elements) + 28.0 * double(p.adamw_elements);
   out->workspace_bytes = p.ws_bytes;
+  if (p.adaptive) {
+    // M read once per pass (power steps + 1), plus the fp64 partial products
+    // written and read back once per power step
+    double part = 0.0;
+    for (const lm::MuonMat& mm : p.mats) part += 16.0 * double(mm.sr_blocks) * double(mm.s);
+    out->srank_bytes = 4.0 * double(p.candidate_elements) * (cfg->adaptive_power_steps + 1) +
+                       part * cfg->adaptive_power_steps;
+  }
   return LM_OK;
 }
 
@@ -582,7 +684,8 @@ lm_status lionmuon_ns(const float* X, float* O, int64_t rows, int64_t cols, int3
   const bool rms02 = cfg->ns_scale_mode == LM_NS_SCALE_RMS02;
   std::lock_guard<std::mutex> lock(g_mu);
   std::shared_ptr<DevicePlan> dp;
-  lm_status s = get_plan(x.data(), batch, true, precision_of(*cfg), rms02, stream, &dp);
+  lm_status s = get_plan(x.data(), batch, lm::StepKind::kMuon, precision_of(*cfg), rms02, stream,
+                         &dp);
   if (s != LM_OK) return s;
   void* ws = workspace;
   if (workspace) {
@@ -593,7 +696,7 @@ lm_status lionmuon_ns(const float* X, float* O, int64_t rows, int64_t cols, int3
     if (s != LM_OK) return s;
   }
   return enqueue(*dp, step_consts(0.0, 0.0, 0.0, 0.0, 0.0, cfg->ns_eps, nullptr, 0), *cfg, ws, true,
-                 stream);
+                 AdaptiveOut(), stream);
 }
 
 lm_status lionmuon_profiling_enable(int32_t enable) {

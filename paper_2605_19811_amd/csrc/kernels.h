@@ -22,6 +22,7 @@ struct LionLaunch {
   const int32_t* block_start;    // device, n_tensors + 1
   int32_t n_tensors;
   int32_t n_blocks;
+  const int32_t* decide;         // adaptive: per-candidate decisions (1 = Muon), else null
   StepConsts k;
 };
 // Elementwise pass: Lion-branch tensors and AdamW tensors in one launch.
@@ -35,6 +36,7 @@ struct PrepLaunch {
   void* ws;                      // workspace base
   float* partials;               // one float per preparation tile
   float* rscale;                 // one float per matrix
+  const int32_t* decide;         // adaptive: matrices with decision 0 are skipped
   StepConsts k;
 };
 // Interpolation, momentum update, X0 / X0^T store and Frobenius partials,
@@ -59,7 +61,34 @@ struct GemmLaunch {
   float lr, wd;                  // eta_M and lambda of the W update
   int32_t fp32;                  // element type of the matrices in `tasks`
   int32_t tile;                  // output tile edge of `tasks`: 128 or 256
+  const int32_t* decide;         // adaptive: tiles of matrices with decision 0 exit
 };
 hipError_t launch_gemm(GemmMode mode, const GemmLaunch& a, hipStream_t stream);
+
+// Adaptive step (Appendix G): stable-rank estimate of each candidate's
+// momentum by power iteration on the Gram matrix of its short side, in fp64.
+struct SrankLaunch {
+  const MuonMat* mats;           // device
+  const int32_t* sr_start;       // device, n_mats + 1: pass blocks
+  const int32_t* rd_start;       // device, n_mats + 1: reduction chunks
+  const int32_t* tensor_mat;     // device, n_inputs: candidate index or -1
+  int32_t n_mats;
+  int32_t n_blocks;              // sr_start[n_mats]
+  int32_t n_chunks;              // rd_start[n_mats]
+  int32_t n_inputs;              // length of the caller's tensor list
+  void* ws;
+  int32_t* decide;               // workspace: one int32 per candidate
+  int32_t* decisions_out;        // optional, per input tensor (device)
+  double* srank_out;             // optional, per input tensor (device)
+  double alpha;
+};
+// One pass over M per power step: z' = S^T S (z / ||z||) as per-block
+// partials (the first pass starts from the all-ones vector and also sums
+// M^2); `last` passes only sum ||S z / ||z|| ||^2.
+hipError_t launch_srank_pass(const SrankLaunch& a, bool first, bool last, hipStream_t stream);
+// Fixed-order sum of the partials into z' and the chunk sums of z'^2.
+hipError_t launch_srank_reduce(const SrankLaunch& a, hipStream_t stream);
+// r_hat = ||M||_F^2 / sigma_hat^2 and the decision r_hat <= alpha * min(m, n).
+hipError_t launch_srank_decide(const SrankLaunch& a, hipStream_t stream);
 
 }  // namespace lm

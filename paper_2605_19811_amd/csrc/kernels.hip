@@ -8,6 +8,9 @@
 //                iteration orientation X (rows <= cols) and its transpose, and
 //                a per-tile partial sum of Ghat^2 (wave shuffles + LDS).
 //  norm_kernel   fixed-order reduction of the partials -> 1/(||Ghat||_F + eps).
+//  srank_*       adaptive step: fp64 power iteration for the stable rank of
+//                each candidate's momentum and the per-matrix Muon / Lion
+//                decision, which the kernels above and below then read.
 //  ns_*_kernel   the Newton-Schulz products on MFMA with fp32 accumulation:
 //                Gram A = X X^T and polynomial B' = a I + b A + c A A on the
 //                lower triangle of tiles (mirrored on store), then apply
@@ -55,6 +58,7 @@ __device__ __forceinline__ float wave_sum(float v) {
 struct LionArgs {
   const LionTensor* tensors;
   const int32_t* block_start;
+  const int32_t* decide;
   int32_t n_tensors;
   float b1, omb1, b2, omb2, lr, wd;
   float ab1, aomb1, ab2, aomb2, alr, aeps, awd, ac1, ac2;   // AdamW
@@ -81,6 +85,7 @@ __global__ __launch_bounds__(256) void lion_kernel(LionArgs a) {
   const int b = blockIdx.x;
   const int ti = find_segment(a.block_start, a.n_tensors, b);
   const LionTensor t = a.tensors[ti];
+  if (t.gate >= 0 && a.decide[t.gate] != 0) return;   // the candidate took Muon
   const int64_t base = int64_t(b - a.block_start[ti]) * kLionBlockElems;
   const int tid = threadIdx.x;
   const bool full = t.vec_ok && base + kLionBlockElems <= t.numel;
@@ -160,6 +165,7 @@ struct PrepArgs {
   void* ws;
   float* partials;
   float* rscale;
+  const int32_t* decide;
   float b1, omb1, b2, omb2, eps;
 };
 
@@ -262,7 +268,9 @@ __device__ __forceinline__ void prep_tile(const PrepArgs& a, const MuonMat& mm, 
 
 __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
   const int b = blockIdx.x;
-  const MuonMat& mm = a.mats[find_segment(a.prep_start, a.n_mats, b)];
+  const int mi = find_segment(a.prep_start, a.n_mats, b);
+  if (a.decide && a.decide[mi] == 0) return;          // the candidate took Lion
+  const MuonMat& mm = a.mats[mi];
   if (mm.fp32)
     prep_tile<float>(a, mm, b);
   else
@@ -271,6 +279,7 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
 
 __global__ __launch_bounds__(256) void norm_kernel(PrepArgs a) {
   __shared__ float red[4];
+  if (a.decide && a.decide[blockIdx.x] == 0) return;
   const MuonMat mm = a.mats[blockIdx.x];
   const float* p = a.partials + mm.prep_first;
   float s = 0.0f;
@@ -281,6 +290,311 @@ __global__ __launch_bounds__(256) void norm_kernel(PrepArgs a) {
   if (threadIdx.x == 0) {
     const float total = (red[0] + red[1]) + (red[2] + red[3]);
     a.rscale[blockIdx.x] = 1.0f / (sqrtf(total) + a.eps);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Adaptive step: stable rank of the momentum (Appendix G)
+// ---------------------------------------------------------------------------
+// S is the long-side view of M (S = M when rows >= cols, else M^T), so the
+// iterate z has min(m, n) entries. A block of kSrBlock long-side positions
+// (rows of a tall M, columns of a wide M) holds whole rows of S, so one read
+// of the block gives u = S_blk v (v = z / ||z||) and then its share
+// S_blk^T u of z' = S^T S v; the block is read a second time for that share,
+// from cache. All sums are fp64 in a fixed order.
+struct SrankArgs {
+  const MuonMat* mats;
+  const int32_t* sr_start;
+  const int32_t* rd_start;
+  const int32_t* tensor_mat;
+  int32_t n_mats;
+  void* ws;
+  int32_t* decide;
+  int32_t* decisions_out;
+  double* srank_out;
+  double alpha;
+};
+
+struct SrBufs {
+  double* z;       // s
+  double* part;    // sr_blocks x s
+  double* usq;     // sr_blocks
+  double* fsq;     // sr_blocks
+  double* nrm;     // ceil(s / kSrChunk)
+  int nchunks;
+};
+
+__device__ __forceinline__ SrBufs sr_bufs(void* ws, const MuonMat& mm) {
+  SrBufs b;
+  b.z = reinterpret_cast<double*>(static_cast<char*>(ws) + mm.off_sr);
+  b.part = b.z + mm.s;
+  b.usq = b.part + int64_t(mm.sr_blocks) * mm.s;
+  b.fsq = b.usq + mm.sr_blocks;
+  b.nrm = b.fsq + mm.sr_blocks;
+  b.nchunks = (mm.s + kSrChunk - 1) / kSrChunk;
+  return b;
+}
+
+// Butterfly sum: every lane ends with the same, order-fixed total.
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+template <int VW>
+__device__ __forceinline__ void load_vw(const float* p, bool ok, double x[VW]) {
+  if (VW == 4) {
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    if (ok) v = *reinterpret_cast<const f32x4*>(p);
+#pragma unroll
+    for (int e = 0; e < VW; ++e) x[e] = double(v[e]);
+  } else {
+    x[0] = ok ? double(*p) : 0.0;
+  }
+}
+
+// Block-level totals of u^2 (same value in every lane of a wave: uu_wave)
+// and M^2 (per-lane partial fs), written by thread 0.
+template <bool FIRST>
+__device__ __forceinline__ void sr_block_sums(double (*red)[256], double uu_wave, double fs,
+                                              const SrBufs& B, int blk) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (FIRST) fs = wave_sum_d(fs);
+  __syncthreads();
+  if (lane == 0) {
+    red[wave][0] = uu_wave;
+    red[wave][1] = fs;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    B.usq[blk] = (red[0][0] + red[1][0]) + (red[2][0] + red[3][0]);
+    if (FIRST) B.fsq[blk] = (red[0][1] + red[1][1]) + (red[2][1] + red[3][1]);
+  }
+}
+
+// Tall M (rows = l >= cols = s): block = kSrBlock rows; wave w owns rows
+// w, w + 4, ... of the block; lanes run along the row, VW floats each.
+template <int VW, bool FIRST, bool LAST>
+__device__ void srank_tall(double (*red)[256], const MuonMat& mm, const SrBufs& B, int blk,
+                           double inv) {
+  constexpr int kRows = kSrBlock / 4;
+  constexpr int kChunk = 64 * VW;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int s = mm.s;
+  const int64_t r0 = int64_t(blk) * kSrBlock;
+  const int nr = int(min(int64_t(kSrBlock), mm.l - r0));
+  const float* M = mm.m + r0 * s;
+  double acc[kRows];
+#pragma unroll
+  for (int j = 0; j < kRows; ++j) acc[j] = 0.0;
+  double fs = 0.0;
+  for (int c0 = 0; c0 < s; c0 += kChunk) {
+    const int c = c0 + lane * VW;
+    const bool ok = c < s;                      // VW = 4: s is a multiple of 4
+    double zc[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) zc[e] = FIRST ? 1.0 : (ok ? B.z[c + e] : 0.0);
+#pragma unroll
+    for (int j = 0; j < kRows; ++j) {
+      const int r = wave + 4 * j;
+      double x[VW];
+      load_vw<VW>(M + int64_t(r) * s + c, ok && r < nr, x);
+#pragma unroll
+      for (int e = 0; e < VW; ++e) {
+        acc[j] = fma(x[e], zc[e], acc[j]);
+        if (FIRST) fs = fma(x[e], x[e], fs);
+      }
+    }
+  }
+  double u[kRows], uu = 0.0;
+#pragma unroll
+  for (int j = 0; j < kRows; ++j) {
+    u[j] = wave_sum_d(acc[j]) * inv;
+    uu = fma(u[j], u[j], uu);
+  }
+  if (!LAST) {
+    for (int c0 = 0; c0 < s; c0 += kChunk) {
+      const int c = c0 + lane * VW;
+      const bool ok = c < s;
+      double wv[VW];
+#pragma unroll
+      for (int e = 0; e < VW; ++e) wv[e] = 0.0;
+#pragma unroll
+      for (int j = 0; j < kRows; ++j) {
+        const int r = wave + 4 * j;
+        double x[VW];
+        load_vw<VW>(M + int64_t(r) * s + c, ok && r < nr, x);
+#pragma unroll
+        for (int e = 0; e < VW; ++e) wv[e] = fma(x[e], u[j], wv[e]);
+      }
+      __syncthreads();                           // previous chunk's reads of red
+#pragma unroll
+      for (int e = 0; e < VW; ++e) red[wave][lane * VW + e] = wv[e];
+      __syncthreads();
+      for (int i = tid; i < kChunk; i += 256) {
+        if (c0 + i < s)
+          B.part[int64_t(blk) * s + c0 + i] = (red[0][i] + red[1][i]) + (red[2][i] + red[3][i]);
+      }
+    }
+  }
+  sr_block_sums<FIRST>(red, uu, fs, B, blk);
+}
+
+// Wide M (rows = s < cols = l): block = kSrBlock columns; LPR lanes cover
+// one row's kSrBlock columns, VW floats each; a wave covers RPW rows per pass.
+template <int VW, bool FIRST, bool LAST>
+__device__ void srank_wide(double (*red)[256], const MuonMat& mm, const SrBufs& B, int blk,
+                           double inv) {
+  constexpr int kLpr = kSrBlock / VW;
+  constexpr int kRpw = 64 / kLpr;
+  constexpr int kRpp = 4 * kRpw;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int s = mm.s;
+  const int64_t l = mm.l;
+  const int sub = lane % kLpr, rsub = lane / kLpr;
+  const int64_t c = int64_t(blk) * kSrBlock + sub * VW;
+  const bool cok = c < l;                        // VW = 4: l is a multiple of 4
+  const int passes = (s + kRpp - 1) / kRpp;
+  const float* Mc = mm.m + c;
+  double acc[VW];
+#pragma unroll
+  for (int e = 0; e < VW; ++e) acc[e] = 0.0;
+  double fs = 0.0;
+  for (int p = 0; p < passes; ++p) {
+    const int r = p * kRpp + wave * kRpw + rsub;
+    const bool ok = cok && r < s;
+    const double zr = FIRST ? 1.0 : (r < s ? B.z[r] : 0.0);
+    double x[VW];
+    load_vw<VW>(Mc + int64_t(r) * l, ok, x);
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+      acc[e] = fma(x[e], zr, acc[e]);
+      if (FIRST) fs = fma(x[e], x[e], fs);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < VW; ++e)
+#pragma unroll
+    for (int off = kLpr; off < 64; off <<= 1) acc[e] += __shfl_xor(acc[e], off, 64);
+  double* ured = &red[0][0];                     // [4][kSrBlock]
+  double* us = &red[2][0];                       // kSrBlock
+  if (rsub == 0) {
+#pragma unroll
+    for (int e = 0; e < VW; ++e) ured[wave * kSrBlock + sub * VW + e] = acc[e];
+  }
+  __syncthreads();
+  double uu = 0.0;
+  if (wave == 0) {
+    double uc = 0.0;
+    if (lane < kSrBlock) {
+      uc = ((ured[lane] + ured[kSrBlock + lane]) +
+            (ured[2 * kSrBlock + lane] + ured[3 * kSrBlock + lane])) * inv;
+      us[lane] = uc;
+    }
+    uu = wave_sum_d(uc * uc);
+  }
+  __syncthreads();
+  if (!LAST) {
+    double uv[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) uv[e] = us[sub * VW + e];
+    for (int p = 0; p < passes; ++p) {
+      const int r = p * kRpp + wave * kRpw + rsub;
+      double x[VW];
+      load_vw<VW>(Mc + int64_t(r) * l, cok && r < s, x);
+      double wr = 0.0;
+#pragma unroll
+      for (int e = 0; e < VW; ++e) wr = fma(x[e], uv[e], wr);
+#pragma unroll
+      for (int off = 1; off < kLpr; off <<= 1) wr += __shfl_xor(wr, off, 64);
+      if (sub == 0 && r < s) B.part[int64_t(blk) * s + r] = wr;
+    }
+  }
+  sr_block_sums<FIRST>(red, uu, fs, B, blk);
+}
+
+template <bool FIRST, bool LAST>
+__global__ __launch_bounds__(256) void srank_pass_kernel(SrankArgs a) {
+  __shared__ double red[4][256];
+  const int b = blockIdx.x;
+  const int mi = find_segment(a.sr_start, a.n_mats, b);
+  const MuonMat& mm = a.mats[mi];
+  const SrBufs B = sr_bufs(a.ws, mm);
+  const int blk = b - a.sr_start[mi];
+  double inv;
+  if (FIRST) {
+    inv = 1.0 / sqrt(double(mm.s));              // v0 = ones / sqrt(s)
+  } else {
+    double n2 = 0.0;
+    for (int i = 0; i < B.nchunks; ++i) n2 += B.nrm[i];
+    inv = n2 > 0.0 ? 1.0 / sqrt(n2) : 0.0;       // a vanished iterate stays zero
+  }
+  if (mm.tall) {
+    if (mm.vec_ok) srank_tall<4, FIRST, LAST>(red, mm, B, blk, inv);
+    else srank_tall<1, FIRST, LAST>(red, mm, B, blk, inv);
+  } else {
+    if (mm.vec_ok) srank_wide<4, FIRST, LAST>(red, mm, B, blk, inv);
+    else srank_wide<1, FIRST, LAST>(red, mm, B, blk, inv);
+  }
+}
+
+__global__ __launch_bounds__(256) void srank_reduce_kernel(SrankArgs a) {
+  __shared__ double red[4][kSrChunk];
+  const int b = blockIdx.x;
+  const int mi = find_segment(a.rd_start, a.n_mats, b);
+  const MuonMat& mm = a.mats[mi];
+  const SrBufs B = sr_bufs(a.ws, mm);
+  const int chunk = b - a.rd_start[mi];
+  const int tid = threadIdx.x, q = tid >> 6;
+  const int j = chunk * kSrChunk + (tid & 63);
+  double acc = 0.0;
+  if (j < mm.s)
+    for (int bb = q; bb < mm.sr_blocks; bb += 4) acc += B.part[int64_t(bb) * mm.s + j];
+  red[q][tid & 63] = acc;
+  __syncthreads();
+  if (tid < 64) {
+    double zj = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
+    if (j < mm.s) B.z[j] = zj;
+    else zj = 0.0;
+    const double sq = wave_sum_d(zj * zj);
+    if (tid == 0) B.nrm[chunk] = sq;
+  }
+}
+
+__global__ __launch_bounds__(256) void srank_decide_kernel(SrankArgs a) {
+  __shared__ double red[4][2];
+  const int i = blockIdx.x, tid = threadIdx.x;
+  const int mi = a.tensor_mat[i];
+  if (mi < 0) {
+    if (tid == 0) {
+      if (a.decisions_out) a.decisions_out[i] = 0;
+      if (a.srank_out) a.srank_out[i] = -1.0;
+    }
+    return;
+  }
+  const MuonMat& mm = a.mats[mi];
+  const SrBufs B = sr_bufs(a.ws, mm);
+  double f = 0.0, u = 0.0;
+  for (int bb = tid; bb < mm.sr_blocks; bb += 256) {
+    f += B.fsq[bb];
+    u += B.usq[bb];
+  }
+  f = wave_sum_d(f);
+  u = wave_sum_d(u);
+  if ((tid & 63) == 0) {
+    red[tid >> 6][0] = f;
+    red[tid >> 6][1] = u;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const double F = (red[0][0] + red[1][0]) + (red[2][0] + red[3][0]);
+    const double U = (red[0][1] + red[1][1]) + (red[2][1] + red[3][1]);
+    const double r = U > 0.0 ? F / U : 0.0;
+    const int d = r <= a.alpha * double(mm.s) ? 1 : 0;
+    a.decide[mi] = d;
+    if (a.decisions_out) a.decisions_out[i] = d;
+    if (a.srank_out) a.srank_out[i] = r;
   }
 }
 
@@ -337,6 +651,7 @@ struct GemmArgs {
   const XcdSplit* split;
   void* ws;
   const float* rscale;
+  const int32_t* decide;
   int32_t src, first, last, store_o;
   float a, b, c, lr, wd;
 };
@@ -361,6 +676,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
   if (slot >= g.split->count[xcd]) return;
   const GemmTask task = g.tasks[g.split->start[xcd] + slot];
+  if (g.decide && g.decide[task.mat] == 0) return;
   const MuonMat& mm = g.mats[task.mat];
   char* wsb = static_cast<char*>(g.ws);
   auto at = [&](int64_t off) { return reinterpret_cast<T*>(wsb + off); };
@@ -665,6 +981,7 @@ hipError_t launch_lion(const LionLaunch& l, hipStream_t stream) {
   a.awd = l.k.adam_wd;
   a.ac1 = l.k.adam_c1;
   a.ac2 = l.k.adam_c2;
+  a.decide = l.decide;
   hipLaunchKernelGGL(lion_kernel, dim3(l.n_blocks), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
@@ -677,6 +994,7 @@ static PrepArgs prep_args(const PrepLaunch& l) {
   a.ws = l.ws;
   a.partials = l.partials;
   a.rscale = l.rscale;
+  a.decide = l.decide;
   a.b1 = l.k.beta1;
   a.omb1 = l.k.one_minus_beta1;
   a.b2 = l.k.beta2;
@@ -714,6 +1032,7 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
   a.c = l.c;
   a.lr = l.lr;
   a.wd = l.wd;
+  a.decide = l.decide;
   const dim3 grid(unsigned(l.max_count) * kXcds);
 #define LM_LAUNCH(KERNEL, T, BT) \
   hipLaunchKernelGGL((KERNEL<T, BT>), grid, dim3(TileGeom<BT>::kThreads), 0, stream, a)
@@ -734,6 +1053,46 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
   }
 #undef LM_LAUNCH_MODE
 #undef LM_LAUNCH
+  return hipGetLastError();
+}
+
+static SrankArgs srank_args(const SrankLaunch& l) {
+  SrankArgs a;
+  a.mats = l.mats;
+  a.sr_start = l.sr_start;
+  a.rd_start = l.rd_start;
+  a.tensor_mat = l.tensor_mat;
+  a.n_mats = l.n_mats;
+  a.ws = l.ws;
+  a.decide = l.decide;
+  a.decisions_out = l.decisions_out;
+  a.srank_out = l.srank_out;
+  a.alpha = l.alpha;
+  return a;
+}
+
+hipError_t launch_srank_pass(const SrankLaunch& l, bool first, bool last, hipStream_t stream) {
+  if (l.n_blocks == 0) return hipSuccess;
+  const SrankArgs a = srank_args(l);
+  const dim3 grid(unsigned(l.n_blocks)), block(256);
+  if (first && last) hipLaunchKernelGGL((srank_pass_kernel<true, true>), grid, block, 0, stream, a);
+  else if (first) hipLaunchKernelGGL((srank_pass_kernel<true, false>), grid, block, 0, stream, a);
+  else if (last) hipLaunchKernelGGL((srank_pass_kernel<false, true>), grid, block, 0, stream, a);
+  else hipLaunchKernelGGL((srank_pass_kernel<false, false>), grid, block, 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_srank_reduce(const SrankLaunch& l, hipStream_t stream) {
+  if (l.n_chunks == 0) return hipSuccess;
+  hipLaunchKernelGGL(srank_reduce_kernel, dim3(unsigned(l.n_chunks)), dim3(256), 0, stream,
+                     srank_args(l));
+  return hipGetLastError();
+}
+
+hipError_t launch_srank_decide(const SrankLaunch& l, hipStream_t stream) {
+  if (l.n_inputs == 0) return hipSuccess;
+  hipLaunchKernelGGL(srank_decide_kernel, dim3(unsigned(l.n_inputs)), dim3(256), 0, stream,
+                     srank_args(l));
   return hipGetLastError();
 }
 

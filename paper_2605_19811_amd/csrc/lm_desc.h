@@ -16,6 +16,8 @@ constexpr int kMinBigTiles = 512;  // a bf16 Gram / polynomial stage uses 256-ti
 constexpr int kPrepTile = 64;    // square tile of the preparation / transpose pass
 constexpr int kLionBlockElems = 4096;  // elements per Lion workgroup (256 x float4 x 4)
 constexpr int kXcds = 8;         // accelerator complex dies of one MI355X
+constexpr int kSrBlock = 32;     // long-side positions per stable-rank block
+constexpr int kSrChunk = 64;     // short-side entries per stable-rank reduction workgroup
 
 // One tensor of the elementwise pass: the Lion branch, or AdamW.
 struct LionTensor {
@@ -26,6 +28,9 @@ struct LionTensor {
   int64_t numel;
   int32_t vec_ok;   // every buffer of the tensor is 16-byte aligned
   int32_t adamw;    // 1: AdamW, 0: Lion
+  int32_t gate;     // adaptive step: Muon-candidate index whose decision gates
+                    // this tensor (skipped when the candidate took Muon); -1: always
+  int32_t pad_;
 };
 
 // One matrix on the Muon branch. Workspace offsets are in BYTES from the
@@ -41,7 +46,7 @@ struct MuonMat {
   int32_t transposed;      // rows > cols: iterate on G^T
   int32_t vec_ok;          // 16-byte vector access legal on w, g, m rows
   int32_t fp32;            // 1: fp32 Newton-Schulz buffers, 0: bf16
-  int32_t pad_;
+  int32_t tensor;          // index of the tensor in the caller's list
   int64_t off_x[2];        // X  (s_pad x l_pad), ping-pong
   int64_t off_xt[2];       // X^T (l_pad x s_pad), ping-pong
   int64_t off_a;           // A = X X^T (s_pad x s_pad)
@@ -50,6 +55,13 @@ struct MuonMat {
   int32_t prep_tiles_n;    // preparation tiles along the original columns
   int32_t prep_count;      // preparation tiles of this matrix
   float kappa;             // output scale
+  // adaptive step (stable-rank estimate of M): blocks of kSrBlock long-side
+  // positions, and the byte offset of the matrix's fp64 buffers: the iterate
+  // z (s), per-block partial products (sr_blocks x s), per-block sums of u^2
+  // and of M^2 (sr_blocks each) and chunk sums of z^2 (ceil(s / kSrChunk)).
+  int32_t sr_blocks;
+  int32_t tall;            // rows >= cols: blocks of rows, else blocks of columns
+  int64_t off_sr;
 };
 
 // One output tile of one Newton-Schulz GEMM.

@@ -134,12 +134,17 @@ void split_by_xcd(std::vector<GemmTask>* tasks, const std::vector<int64_t>& cost
   tasks->swap(out);
 }
 
-Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec,
+Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
                   bool kappa_rms02, Plan* p, std::string* err) {
   *p = Plan();
+  const bool muon_step = kind != StepKind::kLion;
   p->muon_step = muon_step;
+  p->adaptive = kind == StepKind::kAdaptive;
   p->lion_block_start.push_back(0);
   p->prep_start.push_back(0);
+  p->sr_start.push_back(0);
+  p->rd_start.push_back(0);
+  p->tensor_mat.assign(size_t(n > 0 ? n : 0), -1);
   std::map<std::pair<int64_t, int64_t>, int> classes;
   int64_t ns_off = 0;   // bytes
   for (int32_t i = 0; i < n; ++i) {
@@ -150,7 +155,8 @@ Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec
     const uintptr_t vbits = adamw ? reinterpret_cast<uintptr_t>(t.v) : 0;
     const bool vec_ok = ((reinterpret_cast<uintptr_t>(t.w) | reinterpret_cast<uintptr_t>(t.g) |
                           reinterpret_cast<uintptr_t>(t.m) | vbits) & 15u) == 0;
-    if (!(muon_step && is_matrix(t))) {
+    const bool candidate = muon_step && is_matrix(t);
+    if (!candidate || p->adaptive) {
       LionTensor lt{};
       lt.w = t.w;
       lt.g = t.g;
@@ -159,6 +165,7 @@ Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec
       lt.numel = t.rows * t.cols;
       lt.vec_ok = vec_ok ? 1 : 0;
       lt.adamw = adamw ? 1 : 0;
+      lt.gate = candidate ? int32_t(p->mats.size()) : -1;
       const int64_t blocks = (lt.numel + kLionBlockElems - 1) / kLionBlockElems;
       if (int64_t(p->lion_block_start.back()) + blocks > INT32_MAX) {
         *err = "too many elements on the Lion branch";
@@ -169,10 +176,10 @@ Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec
       if (adamw) {
         p->adamw_elements += lt.numel;
         ++p->n_adamw;
-      } else {
+      } else if (!candidate) {
         p->lion_elements += lt.numel;
       }
-      continue;
+      if (!candidate) continue;
     }
     MuonMat mm{};
     mm.w = t.w;
@@ -212,6 +219,21 @@ Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec
       return Status::kUnsupported;
     }
     mm.kappa = kappa_rms02 ? float(0.2 * std::sqrt(double(l))) : 1.0f;
+    mm.tensor = i;
+    mm.tall = t.rows >= t.cols ? 1 : 0;
+    mm.sr_blocks = int32_t((l + kSrBlock - 1) / kSrBlock);
+    if (p->adaptive) {
+      const int64_t chunks = (s + kSrChunk - 1) / kSrChunk;
+      if (int64_t(p->sr_start.back()) + mm.sr_blocks > INT32_MAX ||
+          int64_t(p->rd_start.back()) + chunks > INT32_MAX) {
+        *err = "too many elements for the stable-rank passes";
+        return Status::kUnsupported;
+      }
+      p->sr_start.push_back(p->sr_start.back() + mm.sr_blocks);
+      p->rd_start.push_back(p->rd_start.back() + int32_t(chunks));
+      p->candidate_elements += t.rows * t.cols;
+    }
+    p->tensor_mat[size_t(i)] = int32_t(p->mats.size());
     p->prep_start.push_back(mm.prep_first + mm.prep_count);
     p->mats.push_back(mm);
     p->muon_elements += t.rows * t.cols;
@@ -265,6 +287,16 @@ Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec
   off = align256(off + size_t(p->prep_start.back()) * sizeof(float));
   p->ws_rscale_off = off;
   off = align256(off + p->mats.size() * sizeof(float));
+  if (p->adaptive) {
+    p->ws_decide_off = off;
+    off = align256(off + p->mats.size() * sizeof(int32_t));
+    for (MuonMat& mm : p->mats) {
+      const int64_t nb = mm.sr_blocks, s = mm.s;
+      mm.off_sr = int64_t(off);
+      off = align256(off + size_t(s + nb * s + 2 * nb + (s + kSrChunk - 1) / kSrChunk) *
+                               sizeof(double));
+    }
+  }
   p->ws_bytes = p->mats.empty() ? 0 : off;
   return Status::kOk;
 }

@@ -49,8 +49,14 @@ struct NsPrecision {
   bool fp32_for(int64_t short_side) const { return all_fp32 || short_side < bf16_min_side; }
 };
 
+// What a step does with the Muon candidates (matrices per is_matrix):
+// the Lion branch, the Muon branch, or the per-matrix stable-rank choice of
+// Appendix G made on the device.
+enum class StepKind : int { kLion = 0, kMuon = 1, kAdaptive = 2 };
+
 struct Plan {
   bool muon_step = false;
+  bool adaptive = false;
 
   // Lion branch
   std::vector<LionTensor> lion;
@@ -70,9 +76,17 @@ struct Plan {
   int64_t muon_elements = 0;
   int32_t n_shape_classes = 0;
 
+  // Adaptive step: every candidate sits in `mats` AND in `lion` (gated by its
+  // decision); prefix sums of the stable-rank pass blocks and reduction
+  // chunks, and the candidate index of each input tensor (-1: none).
+  std::vector<int32_t> sr_start, rd_start;
+  std::vector<int32_t> tensor_mat;
+  int64_t candidate_elements = 0;
+
   // workspace layout, bytes from the (256-byte aligned) base
   size_t ws_partials_off = 0;   // float per preparation tile
   size_t ws_rscale_off = 0;     // float per matrix
+  size_t ws_decide_off = 0;     // adaptive: int32 per matrix, 1 = Muon
   size_t ws_bytes = 0;
 
   int32_t n_tensors = 0;        // non-empty tensors
@@ -85,9 +99,9 @@ Status validate_scalars(int64_t t, int32_t P, double beta1, double beta2, double
 // Validate the tensor list: pointers, shapes, flags and buffer overlaps.
 Status validate_tensors(const TensorIn* x, int32_t n, std::string* err);
 
-// Build the plan for a Lion step (muon_step = false) or a Muon step;
-// kappa_rms02 selects Table 3 output scaling.
-Status build_plan(const TensorIn* x, int32_t n, bool muon_step, NsPrecision prec,
+// Build the plan of one step kind; kappa_rms02 selects Table 3 output
+// scaling.
+Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
                   bool kappa_rms02, Plan* out, std::string* err);
 
 // Split an ordered task list (cost = inner dimension of each tile) into one

@@ -26,9 +26,10 @@ LM_NS_FP32 = 1
 LM_NS_SCALE_NONE = 0
 LM_NS_SCALE_RMS02 = 1
 
-PHASES = ("lion", "prep", "norm", "gram", "poly", "apply")
+PHASES = ("lion", "prep", "norm", "gram", "poly", "apply", "srank")
 
 EXPORTED = ("lionmuon_config_default", "lionmuon_step", "lionmuon_step_ex",
+            "lionmuon_step_adaptive",
             "lionmuon_workspace_bytes", "lionmuon_ns", "lionmuon_plan_info",
             "lionmuon_profiling_enable", "lionmuon_profiling_read",
             "lionmuon_profiling_reset", "lionmuon_release",
@@ -51,7 +52,9 @@ class lm_config(ctypes.Structure):
                 ("ns_schedule", (ctypes.c_double * 3) * 16),
                 ("adam_lr", ctypes.c_double), ("adam_beta1", ctypes.c_double),
                 ("adam_beta2", ctypes.c_double), ("adam_eps", ctypes.c_double),
-                ("adam_wd", ctypes.c_double)]
+                ("adam_wd", ctypes.c_double),
+                ("adaptive_alpha", ctypes.c_double), ("adaptive_power_steps", ctypes.c_int32),
+                ("reserved3", ctypes.c_int32)]
 
 
 class lm_plan_info(ctypes.Structure):
@@ -63,11 +66,11 @@ class lm_plan_info(ctypes.Structure):
                 ("gram_tiles", ctypes.c_int64), ("poly_tiles", ctypes.c_int64),
                 ("apply_tiles", ctypes.c_int64), ("ns_flops", ctypes.c_double),
                 ("ns_flops_dense", ctypes.c_double), ("lion_bytes", ctypes.c_double),
-                ("workspace_bytes", ctypes.c_size_t)]
+                ("workspace_bytes", ctypes.c_size_t), ("srank_bytes", ctypes.c_double)]
 
 
 class lm_phase_times(ctypes.Structure):
-    _fields_ = [("ms", ctypes.c_double * 6), ("launches", ctypes.c_int64 * 6)]
+    _fields_ = [("ms", ctypes.c_double * 7), ("launches", ctypes.c_int64 * 7)]
 
 
 class LionMuonError(RuntimeError):
@@ -97,6 +100,9 @@ def library():
     lib.lionmuon_step_ex.argtypes = [vp, vp, vp, vp, P(lm_shape), i32, i64, i32, f64, f64, f64,
                                      P(lm_config), vp, sz, vp]
     lib.lionmuon_step_ex.restype = ctypes.c_int
+    lib.lionmuon_step_adaptive.argtypes = [vp, vp, vp, vp, P(lm_shape), i32, i64, f64, f64, f64,
+                                           P(lm_config), vp, sz, vp, vp, vp]
+    lib.lionmuon_step_adaptive.restype = ctypes.c_int
     lib.lionmuon_workspace_bytes.argtypes = [P(lm_shape), i32, P(lm_config), P(sz)]
     lib.lionmuon_workspace_bytes.restype = ctypes.c_int
     lib.lionmuon_ns.argtypes = [vp, vp, i64, i64, i32, P(lm_config), vp, sz, vp]
@@ -131,9 +137,10 @@ def _check(status, what):
 def config(ns_steps=5, ns_coeffs=(3.4445, -4.7750, 2.0315), ns_eps=1e-7,
            ns_precision="bf16", ns_scale="none", lr_muon=0.0, lr_lion=0.0,
            ns_bf16_min_side=64, ns_schedule=None, adam_lr=1e-3, adam_betas=(0.8, 0.999),
-           adam_eps=1e-8, adam_wd=0.0) -> lm_config:
+           adam_eps=1e-8, adam_wd=0.0, adaptive_alpha=0.0, adaptive_power_steps=5) -> lm_config:
     """lm_config with defaults; ``ns_schedule`` is an optional list of
-    per-step (a, b, c) triples (its length sets ns_steps)."""
+    per-step (a, b, c) triples (its length sets ns_steps); ``adaptive_alpha``
+    > 0 selects the stable-rank rule of Appendix G instead of the period."""
     cfg = lm_config()
     library().lionmuon_config_default(ctypes.byref(cfg))
     cfg.ns_steps = ns_steps
@@ -148,6 +155,8 @@ def config(ns_steps=5, ns_coeffs=(3.4445, -4.7750, 2.0315), ns_eps=1e-7,
     cfg.adam_beta1, cfg.adam_beta2 = adam_betas
     cfg.adam_eps = adam_eps
     cfg.adam_wd = adam_wd
+    cfg.adaptive_alpha = adaptive_alpha
+    cfg.adaptive_power_steps = adaptive_power_steps
     if ns_schedule is not None:
         sched = [tuple(float(v) for v in t) for t in ns_schedule]
         if not 1 <= len(sched) <= 16 or any(len(t) != 3 for t in sched):
@@ -280,6 +289,39 @@ def lionmuon_step_ex(params, grads, momentum, t, P, beta1, beta2, wd, cfg: lm_co
                                     int(P), beta1, beta2, wd, ctypes.byref(cfg), ws_ptr, ws_bytes,
                                     _stream_handle(stream))
     _check(st, "lionmuon_step_ex")
+
+
+def lionmuon_step_adaptive(params, grads, momentum, t, beta1, beta2, wd, cfg: lm_config,
+                           workspace=None, stream=None, lion_only=None,
+                           tensors: TensorList | None = None, second_moment=None,
+                           decisions=None, stable_rank=None):
+    """One step of the adaptive variant (Appendix G); ``decisions`` (int32)
+    and ``stable_rank`` (float64) are optional GPU tensors of one entry per
+    tensor that receive the per-tensor branch and stable-rank estimate."""
+    import torch
+    tl = tensors or TensorList(params, grads, momentum, lion_only, second_moment)
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        if not workspace.is_cuda:
+            raise LionMuonError(LM_ERR_INVALID_ARGUMENT, "workspace must be a GPU tensor")
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    outs = []
+    for name, t_out, dtype in (("decisions", decisions, torch.int32),
+                               ("stable_rank", stable_rank, torch.float64)):
+        if t_out is None:
+            outs.append(None)
+            continue
+        if not t_out.is_cuda or t_out.dtype != dtype or not t_out.is_contiguous() \
+                or t_out.numel() < tl.n:
+            raise LionMuonError(LM_ERR_INVALID_ARGUMENT,
+                                f"{name} must be a contiguous GPU {dtype} tensor of n_tensors entries")
+        outs.append(t_out.data_ptr())
+    st = library().lionmuon_step_adaptive(
+        ctypes.cast(tl.p, ctypes.c_void_p), ctypes.cast(tl.g, ctypes.c_void_p),
+        ctypes.cast(tl.m, ctypes.c_void_p), ctypes.cast(tl.v, ctypes.c_void_p), tl.shapes, tl.n,
+        int(t), beta1, beta2, wd, ctypes.byref(cfg), ws_ptr, ws_bytes, outs[0], outs[1],
+        _stream_handle(stream))
+    _check(st, "lionmuon_step_adaptive")
 
 
 def lionmuon_ns(X, cfg: lm_config | None = None, out=None, stream=None):

@@ -36,7 +36,7 @@ def test_header_declares_the_binding_names():
 def test_library_exports_every_declared_symbol(lib):
     for name in declared_functions():
         assert hasattr(lib, name), name
-    assert lib.lionmuon_abi_version() == 1
+    assert lib.lionmuon_abi_version() == 2
 
 
 def test_status_strings(lib):
@@ -327,3 +327,75 @@ def test_empty_calls_are_no_ops(lib):
     fl.p[0] = None                  # empty tensors need no pointers
     # valid but non-empty calls would reach the device; empty ones never do
     assert _step(lib, fl) == lm.LM_OK
+
+
+# --------------------------------------------------------------------------
+# adaptive variant (Appendix G): configuration, plan and validation
+# --------------------------------------------------------------------------
+def _cfg(lib, **kw):
+    c = lm.lm_config()
+    lib.lionmuon_config_default(ctypes.byref(c))
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+def test_adaptive_config_defaults_and_validation(lib):
+    c = _cfg(lib)
+    assert c.adaptive_alpha == 0.0 and c.adaptive_power_steps == 5 and c.reserved3 == 0
+    fl = FakeList([(64, 64, False)])
+    for bad in [dict(adaptive_alpha=-0.01), dict(adaptive_alpha=1.5),
+                dict(adaptive_alpha=float("nan")), dict(adaptive_power_steps=-1),
+                dict(adaptive_power_steps=65), dict(reserved3=1)]:
+        assert _step_ex(lib, fl, _cfg(lib, **bad)) == INVALID, bad
+
+
+def _step_adaptive(lib, fl, cfg, decisions=None, srank=None):
+    return lib.lionmuon_step_adaptive(ctypes.cast(fl.p, ctypes.c_void_p),
+                                      ctypes.cast(fl.g, ctypes.c_void_p),
+                                      ctypes.cast(fl.m, ctypes.c_void_p), None, fl.shapes, fl.n, 3,
+                                      0.9, 0.99, 0.1, ctypes.byref(cfg), None, 0, decisions, srank,
+                                      None)
+
+
+def test_step_adaptive_rejects_bad_arguments(lib):
+    fl = FakeList([(64, 64, False), (1, 64, False)])
+    assert _step_adaptive(lib, fl, _cfg(lib)) == INVALID            # alpha = 0: not adaptive
+    assert "adaptive_alpha" in lib.lionmuon_last_error().decode()
+    assert lib.lionmuon_step_adaptive(None, None, None, None, None, 1, 0, 0.9, 0.99, 0.1, None,
+                                      None, 0, None, None, None) == INVALID
+    cfg = _cfg(lib, adaptive_alpha=0.01)
+    base = 1 << 36
+    assert _step_adaptive(lib, fl, cfg, decisions=base + 2) == INVALID      # misaligned
+    assert _step_adaptive(lib, fl, cfg, srank=base + 4) == INVALID
+    assert _step_adaptive(lib, fl, cfg, decisions=base + 8, srank=base) == INVALID  # overlap
+    assert "overlap" in lib.lionmuon_last_error().decode()
+    assert _step_adaptive(lib, FakeList([(64, 64, False)]), _cfg(lib, adaptive_alpha=0.01,
+                                                                  adaptive_power_steps=99)) == INVALID
+
+
+def test_plan_info_adaptive_step(lib):
+    wl = workloads.gpt2_124m()
+    specs = _specs(wl)
+    k = 4
+    cfg = lm.config(adaptive_alpha=0.01, adaptive_power_steps=k)
+    info = lm.lionmuon_plan_info(specs, t=1, P=0, cfg=cfg)      # P is ignored
+    muon = lm.lionmuon_plan_info(specs, t=0, P=1)
+    assert info["n_muon"] == 48 and info["muon_elements"] == wl.matrix_numel
+    assert info["n_lion"] == len(wl.tensors) - 48
+    assert info["lion_elements"] == wl.numel - wl.matrix_numel
+    assert info["ns_flops"] == muon["ns_flops"]                  # every candidate may take Muon
+    blocks = part = extra = 0
+    for t in wl.tensors:
+        if t.lion_only or t.rows == 1:
+            continue
+        s, l = min(t.rows, t.cols), max(t.rows, t.cols)
+        nb = -(-l // 32)                                         # 32 long-side positions a block
+        blocks += nb
+        part += nb * s
+        extra += (s + nb * s + 2 * nb + -(-s // 64)) * 8
+    assert info["srank_bytes"] == 4.0 * wl.matrix_numel * (k + 1) + 16.0 * part * k
+    assert muon["srank_bytes"] == 0.0
+    ws_extra = info["workspace_bytes"] - muon["workspace_bytes"]
+    assert extra <= ws_extra < extra + 256 * (48 + 2)
+    assert lm.lionmuon_workspace_bytes(specs, cfg) == info["workspace_bytes"]

@@ -1,0 +1,241 @@
+"""GPU parity of the adaptive Muon / Lion step (Appendix G) against the fp64
+oracle, through the C ABI.
+
+The device estimates the stable rank of every candidate's momentum in fp64;
+the estimate must match ``oracle.stable_rank_estimate`` to 1e-9 relative
+(the two differ only in summation order). The decision is an fp64
+comparison on each side: it must equal the oracle's wherever the oracle's
+estimate is clear of the threshold by more than that tolerance, and it must
+always equal the comparison of the device's own estimate. Each tensor's
+update is then checked against the branch it took.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from paper_2605_19811_amd import lionmuon as lm
+
+from parity import check_lion, check_muon
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+SRANK_TOL = 1e-9
+
+
+def dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def host(t):
+    return t.detach().cpu().double().numpy()
+
+
+def low_rank_momentum(seed, shape, rank, noise):
+    """rank-`rank` matrix plus Gaussian noise of relative size `noise`."""
+    rng = np.random.default_rng(seed)
+    m, n = shape
+    A = rng.standard_normal((m, rank))
+    B = rng.standard_normal((rank, n))
+    M = (A @ B) / np.sqrt(rank * n) + noise * rng.standard_normal((m, n))
+    return (M * 1e-2).astype(np.float32)
+
+
+def check_decisions(M0s, cands, dec, sr, alpha, k):
+    """Estimates against the oracle, decisions against both sides'
+    comparisons; returns the oracle estimates."""
+    ests = {}
+    for i, M0 in enumerate(M0s):
+        if i not in cands:
+            assert dec[i] == 0 and sr[i] == -1.0, i
+            continue
+        s = min(M0.shape)
+        r_or = oracle.stable_rank_estimate(M0.astype(np.float64), k)
+        ests[i] = r_or
+        thr = alpha * s
+        if r_or == 0.0:
+            assert sr[i] == 0.0, (i, sr[i])
+        else:
+            assert abs(sr[i] - r_or) <= SRANK_TOL * r_or, (i, sr[i], r_or)
+        assert dec[i] == int(sr[i] <= thr), (i, sr[i], thr, dec[i])
+        if abs(r_or - thr) > SRANK_TOL * max(thr, 1.0):
+            assert dec[i] == int(oracle.adaptive_uses_muon(M0, alpha, k)), (i, r_or, thr)
+    return ests
+
+
+# tall / wide / square, 16-byte vector and scalar paths (odd widths), ragged
+# last blocks (long side not a multiple of 32), short sides above one
+# 256-wide column chunk, tiny matrices, 1-D and Lion-only tensors
+SHAPES = [(300, 100), (100, 300), (97, 61), (61, 97), (64, 64), (33, 1000), (1000, 33),
+          (513, 260), (260, 513), (2, 2), (2, 50), (1, 300), (300, 1), (128, 256)]
+LION_ONLY = [False] * 13 + [True]
+
+
+def _adaptive_case(seed, alpha, k, precision):
+    rng = np.random.default_rng(seed)
+    W0 = [(rng.standard_normal(s) * 0.02).astype(np.float32) for s in SHAPES]
+    G = [(rng.standard_normal(s) * 1e-2).astype(np.float32) for s in SHAPES]
+    M0 = []
+    for i, s in enumerate(SHAPES):
+        if min(s) > 1 and i % 2 == 0:
+            M0.append(low_rank_momentum([seed, i], s, 1 + i % 3, 1e-3))   # low stable rank
+        else:
+            M0.append((rng.standard_normal(s) * 1e-2).astype(np.float32))
+    cands = {i for i, s in enumerate(SHAPES) if min(s) > 1 and not LION_ONLY[i]}
+    W, M = [dev(x) for x in W0], [dev(x) for x in M0]
+    dec = torch.full((len(SHAPES),), 7, dtype=torch.int32, device=DEV)
+    sr = torch.full((len(SHAPES),), 7.0, dtype=torch.float64, device=DEV)
+    lr_m, lr_l, wd = 0.02, 1e-3, 0.1
+    cfg = lm.config(ns_precision=precision, lr_muon=lr_m, lr_lion=lr_l, adaptive_alpha=alpha,
+                    adaptive_power_steps=k)
+    print(f"adaptive seed={seed} alpha={alpha} k={k} {precision}", flush=True)
+    lm.lionmuon_step_adaptive(W, [dev(g) for g in G], M, 3, 0.9, 0.99, wd, cfg,
+                              lion_only=LION_ONLY, decisions=dec, stable_rank=sr)
+    torch.cuda.synchronize()
+    dec, sr = dec.cpu().numpy(), sr.cpu().numpy()
+    check_decisions(M0, cands, dec, sr, alpha, k)
+    for i in range(len(SHAPES)):
+        if dec[i]:
+            check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_m, wd, precision)
+        else:
+            check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_l, wd)
+    return dec
+
+
+@pytest.mark.parametrize("k", [0, 1, 5])
+def test_adaptive_step_matches_oracle(k):
+    dec = _adaptive_case(71 + k, 0.05, k, "fp32")
+    if k == 5:   # the low-rank momenta take Muon, the Gaussian ones Lion
+        assert dec[[0, 2, 4, 6, 8]].all() and not dec[[1, 3, 5, 7]].any(), dec
+
+
+def test_adaptive_step_bf16_newton_schulz():
+    _adaptive_case(80, 0.05, 5, "bf16")
+
+
+def test_adaptive_zero_and_vanishing_iterates():
+    """M = 0 and an M whose start vector lies in the null space of S both
+    give r_hat = 0 (Muon); the Gaussian matrix beside them takes Lion."""
+    shapes = [(96, 64), (64, 96), (64, 96), (120, 80)]
+    rng = np.random.default_rng(90)
+    a = rng.standard_normal(96).astype(np.float32) * 1e-2
+    signs = np.tile(np.array([1.0, -1.0], np.float32), 32)          # orthogonal to ones
+    M0 = [np.zeros(shapes[0], np.float32),
+          np.zeros(shapes[1], np.float32),
+          np.outer(signs, a).astype(np.float32),                    # wide: S = M^T, S v0 = 0
+          (rng.standard_normal(shapes[3]) * 1e-2).astype(np.float32)]
+    W0 = [(rng.standard_normal(s) * 0.02).astype(np.float32) for s in shapes]
+    G = [(rng.standard_normal(s) * 1e-2).astype(np.float32) for s in shapes]
+    for k in (0, 3):
+        W, M = [dev(x) for x in W0], [dev(x) for x in M0]
+        dec = torch.zeros(4, dtype=torch.int32, device=DEV)
+        sr = torch.zeros(4, dtype=torch.float64, device=DEV)
+        cfg = lm.config(ns_precision="fp32", lr_muon=0.02, lr_lion=1e-3, adaptive_alpha=0.01,
+                        adaptive_power_steps=k)
+        lm.lionmuon_step_adaptive(W, [dev(g) for g in G], M, 0, 0.9, 0.99, 0.1, cfg,
+                                  decisions=dec, stable_rank=sr)
+        torch.cuda.synchronize()
+        assert sr.cpu().tolist()[:3] == [0.0, 0.0, 0.0]
+        assert dec.cpu().tolist() == [1, 1, 1, 0]
+        for i in range(3):
+            assert oracle.stable_rank_estimate(M0[i], k) == 0.0
+            check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 0.02, 0.1, "fp32")
+        check_lion(W0[3], G[3], M0[3], host(W[3]), host(M[3]), 0.9, 0.99, 1e-3, 0.1)
+
+
+def test_adaptive_step_ex_equals_step_adaptive_and_is_deterministic():
+    shapes = [(192, 320), (320, 192), (1, 500)]
+    rng = np.random.default_rng(91)
+    W0 = [(rng.standard_normal(s) * 0.02).astype(np.float32) for s in shapes]
+    G = [(rng.standard_normal(s) * 1e-2).astype(np.float32) for s in shapes]
+    M0 = [low_rank_momentum(92, shapes[0], 2, 1e-3),
+          (rng.standard_normal(shapes[1]) * 1e-2).astype(np.float32),
+          (rng.standard_normal(shapes[2]) * 1e-2).astype(np.float32)]
+    cfg = lm.config(lr_muon=0.02, lr_lion=1e-3, adaptive_alpha=0.02, adaptive_power_steps=4)
+    outs = []
+    for run in range(3):
+        W, M = [dev(x) for x in W0], [dev(x) for x in M0]
+        if run == 0:
+            lm.lionmuon_step_ex(W, [dev(g) for g in G], M, 5, 3, 0.9, 0.99, 0.1, cfg)
+        else:
+            lm.lionmuon_step_adaptive(W, [dev(g) for g in G], M, 5, 0.9, 0.99, 0.1, cfg)
+        torch.cuda.synchronize()
+        outs.append([host(x) for x in W + M])
+    for run in (1, 2):
+        for a, b in zip(outs[0], outs[run]):
+            assert np.array_equal(a, b)
+    # Muon on the low-rank momentum, Lion on the other two
+    check_muon(W0[0], G[0], M0[0], outs[0][0], outs[0][3], 0.9, 0.99, 0.02, 0.1, "bf16")
+    check_lion(W0[1], G[1], M0[1], outs[0][1], outs[0][4], 0.9, 0.99, 1e-3, 0.1)
+
+
+def test_adaptive_outputs_for_a_list_without_candidates():
+    vecs = [torch.randn(300, device=DEV), torch.randn(1, 40, device=DEV)]
+    M = [torch.zeros_like(v) for v in vecs]
+    G = [torch.randn_like(v) * 1e-2 for v in vecs]
+    dec = torch.full((2,), 5, dtype=torch.int32, device=DEV)
+    sr = torch.zeros(2, dtype=torch.float64, device=DEV)
+    W0 = [host(v) for v in vecs]
+    cfg = lm.config(lr_lion=1e-3, adaptive_alpha=0.01)
+    lm.lionmuon_step_adaptive(vecs, G, M, 0, 0.9, 0.99, 0.1, cfg, decisions=dec, stable_rank=sr)
+    torch.cuda.synchronize()
+    assert dec.cpu().tolist() == [0, 0] and sr.cpu().tolist() == [-1.0, -1.0]
+    for i in range(2):
+        check_lion(W0[i], host(G[i]), np.zeros_like(W0[i]), host(vecs[i]), host(M[i]), 0.9, 0.99,
+                   1e-3, 0.1)
+
+
+@pytest.mark.parametrize("name", ["gpt2-124m", "gpt2-720m"])
+def test_adaptive_full_set(name):
+    """The full matrix set with warm momentum; every third candidate's
+    momentum is replaced by a low-rank one so both branches occur. All
+    estimates and decisions are checked; updates on one tensor per shape and
+    branch."""
+    wl = workloads.get(name)
+    params, moms, grads = workloads.device_state(torch, wl, DEV, seed=6, warm=True, n_grad=1)
+    grads = grads[0]
+    lion_only = [t.lion_only for t in wl.tensors]
+    cands = [i for i, t in enumerate(wl.tensors) if not t.lion_only and t.rows > 1]
+    for j, i in enumerate(cands):
+        if j % 3 == 0:
+            moms[i].copy_(dev(low_rank_momentum([93, i], tuple(moms[i].shape), 2, 1e-2)))
+    M0 = {i: moms[i].cpu().numpy() for i in cands}
+    k, alpha = 5, 0.01
+    sample, seen = [], set()
+    for i in cands:
+        key = (tuple(moms[i].shape), cands.index(i) % 3 == 0)
+        if key not in seen:
+            seen.add(key)
+            sample.append(i)
+    lion_sample = [i for i in range(len(wl.tensors)) if i not in cands][:2]
+    before = {i: (params[i].cpu().numpy(), moms[i].cpu().numpy(), grads[i].cpu().numpy())
+              for i in sample + lion_sample}
+    n = len(wl.tensors)
+    dec = torch.full((n,), 7, dtype=torch.int32, device=DEV)
+    sr = torch.zeros(n, dtype=torch.float64, device=DEV)
+    cfg = lm.config(lr_muon=wl.lr_muon, lr_lion=wl.lr_lion, adaptive_alpha=alpha,
+                    adaptive_power_steps=k)
+    tl = lm.TensorList(params, grads, moms, lion_only)
+    print(f"{name}: adaptive step over {n} tensors", flush=True)
+    lm.lionmuon_step_adaptive(None, None, None, 2, wl.beta1, wl.beta2, wl.wd, cfg, tensors=tl,
+                              decisions=dec, stable_rank=sr)
+    torch.cuda.synchronize()
+    dec, sr = dec.cpu().numpy(), sr.cpu().numpy()
+    full_m0 = [M0.get(i, np.zeros((1, 1), np.float32)) for i in range(n)]
+    check_decisions(full_m0, set(cands), dec, sr, alpha, k)
+    n_muon = int(dec.sum())
+    print(f"{name}: {n_muon} of {len(cands)} candidates took Muon", flush=True)
+    assert 0 < n_muon < len(cands)
+    for i in sample + lion_sample:
+        W0, Mb, G = before[i]
+        W1, M1 = params[i].cpu().numpy(), moms[i].cpu().numpy()
+        if dec[i]:
+            check_muon(W0, G, Mb, W1, M1, wl.beta1, wl.beta2, wl.lr_muon, wl.wd, "bf16")
+        else:
+            rows = slice(0, min(W0.shape[0], 512)) if W0.ndim == 2 else slice(None)
+            check_lion(W0[rows], G[rows], Mb[rows], W1[rows], M1[rows], wl.beta1, wl.beta2,
+                       wl.lr_lion, wl.wd)
+    del params, moms, grads, tl
+    lm.lionmuon_release()
+    torch.cuda.empty_cache()

@@ -362,11 +362,18 @@ def test_profiling_counts_every_launch():
     lm.lionmuon_step(W, [dev(g) for g in G], M, 0, 2, 0.9, 0.99, 0.01, 0.1)
     lm.lionmuon_step(W, [dev(g) for g in G], M, 1, 2, 0.9, 0.99, 0.01, 0.1)
     t = lm.lionmuon_profiling_read()
-    lm.lionmuon_profiling_enable(False)
     assert t["prep"]["launches"] == 1 and t["norm"]["launches"] == 1
     assert t["gram"]["launches"] == 5 and t["poly"]["launches"] == 5 and t["apply"]["launches"] == 5
-    assert t["lion"]["launches"] == 1
-    assert all(v["ms"] > 0 for v in t.values())
+    assert t["lion"]["launches"] == 1 and t["srank"]["launches"] == 0
+    assert all(v["ms"] > 0 for k, v in t.items() if k != "srank")
+    # an adaptive step adds one stable-rank phase (all its passes) and runs
+    # every other phase once more, whatever the decisions
+    cfg = lm.config(lr_muon=0.01, lr_lion=0.01, adaptive_alpha=0.05)
+    lm.lionmuon_step_ex(W, [dev(g) for g in G], M, 2, 2, 0.9, 0.99, 0.1, cfg)
+    t = lm.lionmuon_profiling_read()
+    lm.lionmuon_profiling_enable(False)
+    assert t["srank"]["launches"] == 1 and t["srank"]["ms"] > 0
+    assert t["lion"]["launches"] == 2 and t["prep"]["launches"] == 2 and t["gram"]["launches"] == 10
 
 
 # --------------------------------------------------------------------------
