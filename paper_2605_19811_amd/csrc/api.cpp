@@ -52,7 +52,7 @@ struct DevicePlan {
   int32_t* d_lion_start = nullptr;
   lm::MuonMat* d_mats = nullptr;
   int32_t* d_prep_start = nullptr;
-  int32_t* d_sr_start = nullptr;
+  lm::SrBlock* d_sr_tab = nullptr;
   int32_t* d_rd_start = nullptr;
   int32_t* d_tensor_mat = nullptr;
   lm::GemmTask* d_tasks[2][3] = {};   // [precision][gram, poly, apply]
@@ -143,7 +143,7 @@ lm_status get_plan(const TensorIn* x, int32_t n, lm::StepKind kind, lm::NsPrecis
   const size_t o_lion_start = off; place(p.lion_block_start, &off, &parts);
   const size_t o_mats = off;       place(p.mats, &off, &parts);
   const size_t o_prep = off;       place(p.prep_start, &off, &parts);
-  const size_t o_sr = off;         place(p.sr_start, &off, &parts);
+  const size_t o_sr = off;         place(p.sr_tab, &off, &parts);
   const size_t o_rd = off;         place(p.rd_start, &off, &parts);
   const size_t o_tm = off;         place(p.tensor_mat, &off, &parts);
   size_t o_tasks[2][3];
@@ -178,7 +178,7 @@ lm_status get_plan(const TensorIn* x, int32_t n, lm::StepKind kind, lm::NsPrecis
   dp->d_lion_start = reinterpret_cast<int32_t*>(base + o_lion_start);
   dp->d_mats = reinterpret_cast<lm::MuonMat*>(base + o_mats);
   dp->d_prep_start = reinterpret_cast<int32_t*>(base + o_prep);
-  dp->d_sr_start = reinterpret_cast<int32_t*>(base + o_sr);
+  dp->d_sr_tab = reinterpret_cast<lm::SrBlock*>(base + o_sr);
   dp->d_rd_start = reinterpret_cast<int32_t*>(base + o_rd);
   dp->d_tensor_mat = reinterpret_cast<int32_t*>(base + o_tm);
   for (int pr = 0; pr < 2; ++pr)
@@ -285,11 +285,10 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
     decide = reinterpret_cast<int32_t*>(wsb + p.ws_decide_off);
     lm::SrankLaunch sl;
     sl.mats = dp.d_mats;
-    sl.sr_start = dp.d_sr_start;
+    sl.tab = dp.d_sr_tab;
     sl.rd_start = dp.d_rd_start;
     sl.tensor_mat = dp.d_tensor_mat;
     sl.n_mats = int32_t(p.mats.size());
-    sl.n_blocks = p.sr_start.back();
     sl.n_chunks = p.rd_start.back();
     sl.n_inputs = int32_t(p.tensor_mat.size());
     sl.ws = ws;
@@ -300,7 +299,11 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
     Timer t(stream, LM_PHASE_SRANK);
     const int steps = cfg.adaptive_power_steps;
     for (int i = 0; i <= steps && e == hipSuccess; ++i) {
-      e = lm::launch_srank_pass(sl, i == 0, i == steps, stream);
+      for (const Plan::SrClass& c : p.sr_classes) {
+        e = lm::launch_srank_pass(sl, c.kind, c.bucket, c.first, c.count, i == 0, i == steps,
+                                  stream);
+        if (e != hipSuccess) break;
+      }
       if (e == hipSuccess && i < steps) e = lm::launch_srank_reduce(sl, stream);
     }
     if (e == hipSuccess) e = lm::launch_srank_decide(sl, stream);

@@ -69,11 +69,10 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& a, hipStream_t stream);
 // momentum by power iteration on the Gram matrix of its short side, in fp64.
 struct SrankLaunch {
   const MuonMat* mats;           // device
-  const int32_t* sr_start;       // device, n_mats + 1: pass blocks
+  const SrBlock* tab;            // device: pass workgroups, grouped by class
   const int32_t* rd_start;       // device, n_mats + 1: reduction chunks
   const int32_t* tensor_mat;     // device, n_inputs: candidate index or -1
   int32_t n_mats;
-  int32_t n_blocks;              // sr_start[n_mats]
   int32_t n_chunks;              // rd_start[n_mats]
   int32_t n_inputs;              // length of the caller's tensor list
   void* ws;
@@ -82,10 +81,13 @@ struct SrankLaunch {
   double* srank_out;             // optional, per input tensor (device)
   double alpha;
 };
-// One pass over M per power step: z' = S^T S (z / ||z||) as per-block
-// partials (the first pass starts from the all-ones vector and also sums
-// M^2); `last` passes only sum ||S z / ||z|| ||^2.
-hipError_t launch_srank_pass(const SrankLaunch& a, bool first, bool last, hipStream_t stream);
+// One pass over M per power step for the workgroups tab[first_block ..
+// first_block + n_blocks) of one class (kind, bucket): z' = S^T S (z / ||z||)
+// as per-block partials (the first pass starts from the all-ones vector and
+// writes the sums of M^2); `last` passes only sum ||S z / ||z|| ||^2.
+hipError_t launch_srank_pass(const SrankLaunch& a, int32_t kind, int32_t bucket,
+                             int32_t first_block, int32_t n_blocks, bool first, bool last,
+                             hipStream_t stream);
 // Fixed-order sum of the partials into z' and the chunk sums of z'^2.
 hipError_t launch_srank_reduce(const SrankLaunch& a, hipStream_t stream);
 // r_hat = ||M||_F^2 / sigma_hat^2 and the decision r_hat <= alpha * min(m, n).

@@ -297,14 +297,24 @@ __global__ __launch_bounds__(256) void norm_kernel(PrepArgs a) {
 // Adaptive step: stable rank of the momentum (Appendix G)
 // ---------------------------------------------------------------------------
 // S is the long-side view of M (S = M when rows >= cols, else M^T), so the
-// iterate z has min(m, n) entries. A block of kSrBlock long-side positions
-// (rows of a tall M, columns of a wide M) holds whole rows of S, so one read
-// of the block gives u = S_blk v (v = z / ||z||) and then its share
-// S_blk^T u of z' = S^T S v; the block is read a second time for that share,
-// from cache. All sums are fp64 in a fixed order.
+// iterate z has s = min(m, n) entries, and S^T S is the sum over blocks of
+// long-side positions of S_blk^T S_blk. Per power step one pass reads every
+// block of S once: u = S_blk v with v = z / ||z||, then the block's share
+// S_blk^T u of the next iterate, written as one fp64 partial vector per block;
+// a reduction kernel sums the partials in a fixed order.
+// Register paths (16-byte rows, s <= kSrMaxRegSide), v held in LDS:
+//   tall M: a block is kSrTallRows rows; each wave streams groups of its rows
+//           through registers (lanes along the row, 4 floats each) and keeps
+//           its share of S_blk^T u in fp64 registers;
+//   wide M: a block is a strip of kSrWideCols columns, taken 32 columns at a
+//           time by a 1024-thread workgroup that holds all s rows of those
+//           columns in registers (8 lanes per 128-byte row segment).
+// Generic path (any alignment or short side): blocks of kSrBlock positions,
+// read a second time (from cache) for S_blk^T u.
+// All sums are fp64 in a fixed order.
 struct SrankArgs {
   const MuonMat* mats;
-  const int32_t* sr_start;
+  const SrBlock* tab;
   const int32_t* rd_start;
   const int32_t* tensor_mat;
   int32_t n_mats;
@@ -342,6 +352,227 @@ __device__ __forceinline__ double wave_sum_d(double v) {
   return v;
 }
 
+// 1 / ||z|| from the chunk sums of z^2 (0 for a vanished iterate), or
+// 1 / sqrt(s) for the all-ones start vector.
+__device__ __forceinline__ double sr_inv_norm(const MuonMat& mm, const SrBufs& B, bool first) {
+  if (first) return 1.0 / sqrt(double(mm.s));
+  double n2 = 0.0;
+  for (int i = 0; i < B.nchunks; ++i) n2 += B.nrm[i];
+  return n2 > 0.0 ? 1.0 / sqrt(n2) : 0.0;
+}
+
+// v = z / ||z|| into LDS.
+template <int NT>
+__device__ __forceinline__ void sr_load_v(double* vs, const MuonMat& mm, const SrBufs& B,
+                                          bool first) {
+  const double inv = sr_inv_norm(mm, B, first);
+  for (int c = threadIdx.x; c < mm.s; c += NT) vs[c] = first ? inv : B.z[c] * inv;
+  __syncthreads();
+}
+
+// Block totals of u^2 (uu_wave: the same value in every lane of a wave) and
+// of M^2 (per-lane partials), written by thread 0 in a fixed order.
+template <int NW>
+__device__ __forceinline__ void sr_block_sums(double* red, double uu_wave, double fs_lane,
+                                              bool first, const SrBufs& B, int blk) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const double fs = wave_sum_d(fs_lane);
+  __syncthreads();
+  if (lane == 0) {
+    red[2 * wave] = uu_wave;
+    red[2 * wave + 1] = fs;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double u = 0.0, f = 0.0;
+    for (int w = 0; w < NW; ++w) {
+      u += red[2 * w];
+      f += red[2 * w + 1];
+    }
+    B.usq[blk] = u;
+    if (first) B.fsq[blk] = f;
+  }
+}
+
+template <int NCH>
+__global__ __launch_bounds__(256) void srank_tall_kernel(SrankArgs a, int32_t first_block,
+                                                         int32_t first, int32_t last) {
+  constexpr int kRg = NCH <= 4 ? 4 : 2;           // rows per wave per group
+  constexpr int kGroups = kSrTallRows / (4 * kRg);
+  __shared__ double vs[kSrMaxRegSide];
+  __shared__ double red[4][256];
+  const SrBlock sb = a.tab[first_block + blockIdx.x];
+  const MuonMat& mm = a.mats[sb.mat];
+  const SrBufs B = sr_bufs(a.ws, mm);
+  sr_load_v<256>(vs, mm, B, first != 0);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int s = mm.s;
+  const int64_t r0 = int64_t(sb.blk) * kSrTallRows;
+  const int nr = int(min(int64_t(kSrTallRows), mm.l - r0));
+  // per-lane base; row and chunk offsets below are wave-uniform
+  const float* Ml = mm.m + (r0 + wave * kRg) * s + lane * 4;
+  const int cmax = s - lane * 4;                  // chunk q is in range iff q * 256 < cmax
+  double w[NCH][4];
+#pragma unroll
+  for (int q = 0; q < NCH; ++q)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[q][e] = 0.0;
+  double uu = 0.0, fs[kRg];
+#pragma unroll
+  for (int j = 0; j < kRg; ++j) fs[j] = 0.0;
+#pragma unroll 1
+  for (int g = 0; g < kGroups; ++g) {
+    const int rb = g * 4 * kRg + wave * kRg;      // this wave's first row of the group
+    const float* Mg = Ml + int64_t(g * 4 * kRg) * s;
+    f32x4 x[kRg][NCH];
+#pragma unroll
+    for (int j = 0; j < kRg; ++j)
+#pragma unroll
+      for (int q = 0; q < NCH; ++q) {
+        x[j][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (rb + j < nr && q * 256 < cmax)        // s is a multiple of 4
+          x[j][q] = *reinterpret_cast<const f32x4*>(Mg + j * s + q * 256);
+      }
+    double acc[kRg];
+#pragma unroll
+    for (int j = 0; j < kRg; ++j) acc[j] = 0.0;
+#pragma unroll
+    for (int q = 0; q < NCH; ++q) {
+      double v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = q * 256 < cmax ? vs[q * 256 + lane * 4 + e] : 0.0;
+#pragma unroll
+      for (int j = 0; j < kRg; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const double xe = double(x[j][q][e]);
+          acc[j] = fma(xe, v[e], acc[j]);
+          fs[j] = fma(xe, xe, fs[j]);
+        }
+    }
+    double u[kRg];
+#pragma unroll
+    for (int j = 0; j < kRg; ++j) {
+      u[j] = wave_sum_d(acc[j]);
+      uu = fma(u[j], u[j], uu);
+    }
+    if (!last) {
+#pragma unroll
+      for (int q = 0; q < NCH; ++q)
+#pragma unroll
+        for (int j = 0; j < kRg; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) w[q][e] = fma(double(x[j][q][e]), u[j], w[q][e]);
+    }
+  }
+  if (!last) {
+#pragma unroll
+    for (int q = 0; q < NCH; ++q) {
+      __syncthreads();                            // previous chunk's reads of red
+#pragma unroll
+      for (int e = 0; e < 4; ++e) red[wave][lane * 4 + e] = w[q][e];
+      __syncthreads();
+      const int c = q * 256 + tid;
+      if (c < s)
+        B.part[int64_t(sb.blk) * s + c] = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
+    }
+  }
+  double fsl = 0.0;
+#pragma unroll
+  for (int j = 0; j < kRg; ++j) fsl += fs[j];
+  sr_block_sums<4>(&red[0][0], uu, fsl, first != 0, B, sb.blk);
+}
+
+// SW: columns per sub-strip (32: 128-byte row pieces, 8 lanes per row; 16:
+// 64-byte pieces, 4 lanes per row, twice the rows per pass for larger s).
+template <int NP, int SW>
+__global__ __launch_bounds__(1024) void srank_wide_kernel(SrankArgs a, int32_t first_block,
+                                                          int32_t first, int32_t last) {
+  constexpr int kNw = 16;
+  constexpr int kLpr = SW / 4;                    // lanes per row piece
+  constexpr int kRpw = 64 / kLpr;                 // rows per wave per pass
+  constexpr int kRpp = kNw * kRpw;                // rows per pass
+  __shared__ double vs[kSrMaxRegSide];
+  __shared__ double ured[kNw][SW];
+  __shared__ double us[SW];
+  __shared__ double red[2 * kNw];
+  const SrBlock sb = a.tab[first_block + blockIdx.x];
+  const MuonMat& mm = a.mats[sb.mat];
+  const SrBufs B = sr_bufs(a.ws, mm);
+  sr_load_v<1024>(vs, mm, B, first != 0);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int sub = lane % kLpr, rsub = lane / kLpr;
+  const int s = mm.s;
+  const int64_t l = mm.l;
+  const int r_lane = wave * kRpw + rsub;          // row of pass 0
+  const int rmax = s - r_lane;                    // pass p is in range iff p * kRpp < rmax
+  double w[NP];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) w[p] = 0.0;
+  double uu = 0.0, fs[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 1
+  for (int ss = 0; ss < kSrWideCols / SW; ++ss) {
+    const int64_t c = int64_t(sb.blk) * kSrWideCols + ss * SW + sub * 4;
+    const bool cok = c < l;                       // l is a multiple of 4
+    // per-lane base; pass offsets p * kRpp rows are wave-uniform
+    const float* Ml = mm.m + int64_t(r_lane) * l + c;
+    f32x4 x[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      x[p] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (cok && p * kRpp < rmax) x[p] = *reinterpret_cast<const f32x4*>(Ml + int64_t(p * kRpp) * l);
+    }
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const double vr = p * kRpp < rmax ? vs[r_lane + p * kRpp] : 0.0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double xe = double(x[p][e]);
+        acc[e] = fma(xe, vr, acc[e]);
+        fs[e] = fma(xe, xe, fs[e]);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+#pragma unroll
+      for (int off = kLpr; off < 64; off <<= 1) acc[e] += __shfl_xor(acc[e], off, 64);
+    if (rsub == 0) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ured[wave][sub * 4 + e] = acc[e];
+    }
+    __syncthreads();
+    if (wave == 0) {
+      double uc = 0.0;
+      if (lane < SW) {
+        for (int k = 0; k < kNw; ++k) uc += ured[k][lane];
+        us[lane] = uc;
+      }
+      uu += wave_sum_d(uc * uc);
+    }
+    __syncthreads();
+    if (!last) {
+      double uv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) uv[e] = us[sub * 4 + e];
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[p] = fma(double(x[p][e]), uv[e], w[p]);
+    }
+  }
+  if (!last) {
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      double wr = w[p];
+#pragma unroll
+      for (int off = 1; off < kLpr; off <<= 1) wr += __shfl_xor(wr, off, 64);
+      if (sub == 0 && p * kRpp < rmax) B.part[int64_t(sb.blk) * s + r_lane + p * kRpp] = wr;
+    }
+  }
+  sr_block_sums<kNw>(red, uu, (fs[0] + fs[1]) + (fs[2] + fs[3]), first != 0, B, sb.blk);
+}
+
 template <int VW>
 __device__ __forceinline__ void load_vw(const float* p, bool ok, double x[VW]) {
   if (VW == 4) {
@@ -354,30 +585,11 @@ __device__ __forceinline__ void load_vw(const float* p, bool ok, double x[VW]) {
   }
 }
 
-// Block-level totals of u^2 (same value in every lane of a wave: uu_wave)
-// and M^2 (per-lane partial fs), written by thread 0.
-template <bool FIRST>
-__device__ __forceinline__ void sr_block_sums(double (*red)[256], double uu_wave, double fs,
-                                              const SrBufs& B, int blk) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (FIRST) fs = wave_sum_d(fs);
-  __syncthreads();
-  if (lane == 0) {
-    red[wave][0] = uu_wave;
-    red[wave][1] = fs;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    B.usq[blk] = (red[0][0] + red[1][0]) + (red[2][0] + red[3][0]);
-    if (FIRST) B.fsq[blk] = (red[0][1] + red[1][1]) + (red[2][1] + red[3][1]);
-  }
-}
-
-// Tall M (rows = l >= cols = s): block = kSrBlock rows; wave w owns rows
-// w, w + 4, ... of the block; lanes run along the row, VW floats each.
+// Generic path, tall M (rows = l >= cols = s): block = kSrBlock rows; wave w
+// owns rows w, w + 4, ... of the block; lanes run along the row, VW floats each.
 template <int VW, bool FIRST, bool LAST>
-__device__ void srank_tall(double (*red)[256], const MuonMat& mm, const SrBufs& B, int blk,
-                           double inv) {
+__device__ void srank_generic_tall(double (*red)[256], const MuonMat& mm, const SrBufs& B, int blk,
+                                   double inv) {
   constexpr int kRows = kSrBlock / 4;
   constexpr int kChunk = 64 * VW;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -385,10 +597,9 @@ __device__ void srank_tall(double (*red)[256], const MuonMat& mm, const SrBufs& 
   const int64_t r0 = int64_t(blk) * kSrBlock;
   const int nr = int(min(int64_t(kSrBlock), mm.l - r0));
   const float* M = mm.m + r0 * s;
-  double acc[kRows];
+  double acc[kRows], fs[kRows];
 #pragma unroll
-  for (int j = 0; j < kRows; ++j) acc[j] = 0.0;
-  double fs = 0.0;
+  for (int j = 0; j < kRows; ++j) acc[j] = fs[j] = 0.0;
   for (int c0 = 0; c0 < s; c0 += kChunk) {
     const int c = c0 + lane * VW;
     const bool ok = c < s;                      // VW = 4: s is a multiple of 4
@@ -403,15 +614,16 @@ __device__ void srank_tall(double (*red)[256], const MuonMat& mm, const SrBufs& 
 #pragma unroll
       for (int e = 0; e < VW; ++e) {
         acc[j] = fma(x[e], zc[e], acc[j]);
-        if (FIRST) fs = fma(x[e], x[e], fs);
+        fs[j] = fma(x[e], x[e], fs[j]);
       }
     }
   }
-  double u[kRows], uu = 0.0;
+  double u[kRows], uu = 0.0, fsl = 0.0;
 #pragma unroll
   for (int j = 0; j < kRows; ++j) {
     u[j] = wave_sum_d(acc[j]) * inv;
     uu = fma(u[j], u[j], uu);
+    fsl += fs[j];
   }
   if (!LAST) {
     for (int c0 = 0; c0 < s; c0 += kChunk) {
@@ -438,14 +650,14 @@ __device__ void srank_tall(double (*red)[256], const MuonMat& mm, const SrBufs& 
       }
     }
   }
-  sr_block_sums<FIRST>(red, uu, fs, B, blk);
+  sr_block_sums<4>(&red[0][0], uu, fsl, FIRST, B, blk);
 }
 
-// Wide M (rows = s < cols = l): block = kSrBlock columns; LPR lanes cover
-// one row's kSrBlock columns, VW floats each; a wave covers RPW rows per pass.
+// Generic path, wide M (rows = s < cols = l): block = kSrBlock columns; LPR
+// lanes cover one row's kSrBlock columns, VW floats each.
 template <int VW, bool FIRST, bool LAST>
-__device__ void srank_wide(double (*red)[256], const MuonMat& mm, const SrBufs& B, int blk,
-                           double inv) {
+__device__ void srank_generic_wide(double (*red)[256], const MuonMat& mm, const SrBufs& B, int blk,
+                                   double inv) {
   constexpr int kLpr = kSrBlock / VW;
   constexpr int kRpw = 64 / kLpr;
   constexpr int kRpp = 4 * kRpw;
@@ -457,10 +669,9 @@ __device__ void srank_wide(double (*red)[256], const MuonMat& mm, const SrBufs& 
   const bool cok = c < l;                        // VW = 4: l is a multiple of 4
   const int passes = (s + kRpp - 1) / kRpp;
   const float* Mc = mm.m + c;
-  double acc[VW];
+  double acc[VW], fs[VW];
 #pragma unroll
-  for (int e = 0; e < VW; ++e) acc[e] = 0.0;
-  double fs = 0.0;
+  for (int e = 0; e < VW; ++e) acc[e] = fs[e] = 0.0;
   for (int p = 0; p < passes; ++p) {
     const int r = p * kRpp + wave * kRpw + rsub;
     const bool ok = cok && r < s;
@@ -470,13 +681,16 @@ __device__ void srank_wide(double (*red)[256], const MuonMat& mm, const SrBufs& 
 #pragma unroll
     for (int e = 0; e < VW; ++e) {
       acc[e] = fma(x[e], zr, acc[e]);
-      if (FIRST) fs = fma(x[e], x[e], fs);
+      fs[e] = fma(x[e], x[e], fs[e]);
     }
   }
+  double fsl = 0.0;
 #pragma unroll
-  for (int e = 0; e < VW; ++e)
+  for (int e = 0; e < VW; ++e) {
+    fsl += fs[e];
 #pragma unroll
     for (int off = kLpr; off < 64; off <<= 1) acc[e] += __shfl_xor(acc[e], off, 64);
+  }
   double* ured = &red[0][0];                     // [4][kSrBlock]
   double* us = &red[2][0];                       // kSrBlock
   if (rsub == 0) {
@@ -511,31 +725,22 @@ __device__ void srank_wide(double (*red)[256], const MuonMat& mm, const SrBufs& 
       if (sub == 0 && r < s) B.part[int64_t(blk) * s + r] = wr;
     }
   }
-  sr_block_sums<FIRST>(red, uu, fs, B, blk);
+  sr_block_sums<4>(&red[0][0], uu, fsl, FIRST, B, blk);
 }
 
 template <bool FIRST, bool LAST>
-__global__ __launch_bounds__(256) void srank_pass_kernel(SrankArgs a) {
+__global__ __launch_bounds__(256) void srank_generic_kernel(SrankArgs a, int32_t first_block) {
   __shared__ double red[4][256];
-  const int b = blockIdx.x;
-  const int mi = find_segment(a.sr_start, a.n_mats, b);
-  const MuonMat& mm = a.mats[mi];
+  const SrBlock sb = a.tab[first_block + blockIdx.x];
+  const MuonMat& mm = a.mats[sb.mat];
   const SrBufs B = sr_bufs(a.ws, mm);
-  const int blk = b - a.sr_start[mi];
-  double inv;
-  if (FIRST) {
-    inv = 1.0 / sqrt(double(mm.s));              // v0 = ones / sqrt(s)
-  } else {
-    double n2 = 0.0;
-    for (int i = 0; i < B.nchunks; ++i) n2 += B.nrm[i];
-    inv = n2 > 0.0 ? 1.0 / sqrt(n2) : 0.0;       // a vanished iterate stays zero
-  }
+  const double inv = sr_inv_norm(mm, B, FIRST);
   if (mm.tall) {
-    if (mm.vec_ok) srank_tall<4, FIRST, LAST>(red, mm, B, blk, inv);
-    else srank_tall<1, FIRST, LAST>(red, mm, B, blk, inv);
+    if (mm.vec_ok) srank_generic_tall<4, FIRST, LAST>(red, mm, B, sb.blk, inv);
+    else srank_generic_tall<1, FIRST, LAST>(red, mm, B, sb.blk, inv);
   } else {
-    if (mm.vec_ok) srank_wide<4, FIRST, LAST>(red, mm, B, blk, inv);
-    else srank_wide<1, FIRST, LAST>(red, mm, B, blk, inv);
+    if (mm.vec_ok) srank_generic_wide<4, FIRST, LAST>(red, mm, B, sb.blk, inv);
+    else srank_generic_wide<1, FIRST, LAST>(red, mm, B, sb.blk, inv);
   }
 }
 
@@ -549,8 +754,10 @@ __global__ __launch_bounds__(256) void srank_reduce_kernel(SrankArgs a) {
   const int tid = threadIdx.x, q = tid >> 6;
   const int j = chunk * kSrChunk + (tid & 63);
   double acc = 0.0;
-  if (j < mm.s)
+  if (j < mm.s) {
+#pragma unroll 4
     for (int bb = q; bb < mm.sr_blocks; bb += 4) acc += B.part[int64_t(bb) * mm.s + j];
+  }
   red[q][tid & 63] = acc;
   __syncthreads();
   if (tid < 64) {
@@ -1059,7 +1266,7 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
 static SrankArgs srank_args(const SrankLaunch& l) {
   SrankArgs a;
   a.mats = l.mats;
-  a.sr_start = l.sr_start;
+  a.tab = l.tab;
   a.rd_start = l.rd_start;
   a.tensor_mat = l.tensor_mat;
   a.n_mats = l.n_mats;
@@ -1071,14 +1278,43 @@ static SrankArgs srank_args(const SrankLaunch& l) {
   return a;
 }
 
-hipError_t launch_srank_pass(const SrankLaunch& l, bool first, bool last, hipStream_t stream) {
-  if (l.n_blocks == 0) return hipSuccess;
+hipError_t launch_srank_pass(const SrankLaunch& l, int32_t kind, int32_t bucket,
+                             int32_t first_block, int32_t n_blocks, bool first, bool last,
+                             hipStream_t stream) {
+  if (n_blocks == 0) return hipSuccess;
   const SrankArgs a = srank_args(l);
-  const dim3 grid(unsigned(l.n_blocks)), block(256);
-  if (first && last) hipLaunchKernelGGL((srank_pass_kernel<true, true>), grid, block, 0, stream, a);
-  else if (first) hipLaunchKernelGGL((srank_pass_kernel<true, false>), grid, block, 0, stream, a);
-  else if (last) hipLaunchKernelGGL((srank_pass_kernel<false, true>), grid, block, 0, stream, a);
-  else hipLaunchKernelGGL((srank_pass_kernel<false, false>), grid, block, 0, stream, a);
+  const dim3 grid(static_cast<unsigned>(n_blocks));
+  const int32_t f = first ? 1 : 0, z = last ? 1 : 0;
+  if (kind == kSrTall) {
+    switch (bucket) {
+#define LM_TALL(N) \
+  case N: hipLaunchKernelGGL((srank_tall_kernel<N>), grid, dim3(256), 0, stream, a, first_block, f, z); break;
+      LM_TALL(1) LM_TALL(2) LM_TALL(3) LM_TALL(4) LM_TALL(6) LM_TALL(8)
+#undef LM_TALL
+      default: return hipErrorInvalidValue;
+    }
+  } else if (kind == kSrWide || kind == kSrWideNarrow) {
+#define LM_WIDE(N, SW) \
+  case N: hipLaunchKernelGGL((srank_wide_kernel<N, SW>), grid, dim3(1024), 0, stream, a, first_block, f, z); break;
+    if (kind == kSrWide) {
+      switch (bucket) {
+        LM_WIDE(1, 32) LM_WIDE(2, 32) LM_WIDE(4, 32) LM_WIDE(6, 32) LM_WIDE(8, 32)
+        default: return hipErrorInvalidValue;
+      }
+    } else {
+      switch (bucket) {
+        LM_WIDE(1, 16) LM_WIDE(2, 16) LM_WIDE(4, 16) LM_WIDE(6, 16)
+        default: return hipErrorInvalidValue;
+      }
+    }
+#undef LM_WIDE
+  } else {
+    const dim3 block(256);
+    if (first && last) hipLaunchKernelGGL((srank_generic_kernel<true, true>), grid, block, 0, stream, a, first_block);
+    else if (first) hipLaunchKernelGGL((srank_generic_kernel<true, false>), grid, block, 0, stream, a, first_block);
+    else if (last) hipLaunchKernelGGL((srank_generic_kernel<false, true>), grid, block, 0, stream, a, first_block);
+    else hipLaunchKernelGGL((srank_generic_kernel<false, false>), grid, block, 0, stream, a, first_block);
+  }
   return hipGetLastError();
 }
 

@@ -16,8 +16,23 @@ constexpr int kMinBigTiles = 512;  // a bf16 Gram / polynomial stage uses 256-ti
 constexpr int kPrepTile = 64;    // square tile of the preparation / transpose pass
 constexpr int kLionBlockElems = 4096;  // elements per Lion workgroup (256 x float4 x 4)
 constexpr int kXcds = 8;         // accelerator complex dies of one MI355X
-constexpr int kSrBlock = 32;     // long-side positions per stable-rank block
+// Stable-rank passes (adaptive step). Matrices with 16-byte rows and a short
+// side up to kSrMaxRegSide hold their block in registers (tall: blocks of
+// kSrTallRows rows; wide: strips of kSrWideCols columns, taken 32 columns at a
+// time, or 16 for short sides above 1024); the others take the generic path
+// (blocks of kSrBlock long-side positions, read twice).
+constexpr int kSrBlock = 32;
+constexpr int kSrTallRows = 64;
+constexpr int kSrWideCols = 64;
+constexpr int kSrMaxRegSide = 2048;
 constexpr int kSrChunk = 64;     // short-side entries per stable-rank reduction workgroup
+enum SrKind : int32_t { kSrGeneric = 0, kSrTall = 1, kSrWide = 2, kSrWideNarrow = 3 };
+
+// One workgroup of a stable-rank pass: matrix index and block index.
+struct SrBlock {
+  int32_t mat;
+  int32_t blk;
+};
 
 // One tensor of the elementwise pass: the Lion branch, or AdamW.
 struct LionTensor {
@@ -55,13 +70,15 @@ struct MuonMat {
   int32_t prep_tiles_n;    // preparation tiles along the original columns
   int32_t prep_count;      // preparation tiles of this matrix
   float kappa;             // output scale
-  // adaptive step (stable-rank estimate of M): blocks of kSrBlock long-side
-  // positions, and the byte offset of the matrix's fp64 buffers: the iterate
-  // z (s), per-block partial products (sr_blocks x s), per-block sums of u^2
+  // adaptive step (stable-rank estimate of M): pass blocks along the long
+  // side, and the byte offset of the matrix's fp64 buffers: the iterate z
+  // (s), per-block partial products (sr_blocks x s), per-block sums of u^2
   // and of M^2 (sr_blocks each) and chunk sums of z^2 (ceil(s / kSrChunk)).
   int32_t sr_blocks;
   int32_t tall;            // rows >= cols: blocks of rows, else blocks of columns
   int64_t off_sr;
+  int32_t sr_kind;         // SrKind of the matrix's pass
+  int32_t sr_bucket;       // register bucket of the tall / wide pass
 };
 
 // One output tile of one Newton-Schulz GEMM.

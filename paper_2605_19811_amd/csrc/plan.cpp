@@ -18,6 +18,25 @@ bool finite_nonneg(double v) { return std::isfinite(v) && v >= 0.0; }
 
 }  // namespace
 
+int sr_tall_bucket(int64_t s) {
+  const int64_t n = (s + 255) / 256;
+  for (int b : kSrTallBuckets)
+    if (n <= b) return b;
+  return 0;
+}
+
+int sr_wide_bucket(int64_t s) {
+  if (s <= 1024) {
+    const int64_t n = (s + 127) / 128;
+    for (int b : kSrWideBuckets)
+      if (n <= b) return b;
+  }
+  const int64_t n = (s + 255) / 256;
+  for (int b : kSrNarrowBuckets)
+    if (n <= b) return b;
+  return 0;
+}
+
 bool is_muon_step(int64_t t, int32_t P) { return P >= 1 && t % P == 0; }
 
 bool is_matrix(const TensorIn& x) {
@@ -142,7 +161,6 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
   p->adaptive = kind == StepKind::kAdaptive;
   p->lion_block_start.push_back(0);
   p->prep_start.push_back(0);
-  p->sr_start.push_back(0);
   p->rd_start.push_back(0);
   p->tensor_mat.assign(size_t(n > 0 ? n : 0), -1);
   std::map<std::pair<int64_t, int64_t>, int> classes;
@@ -221,15 +239,25 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
     mm.kappa = kappa_rms02 ? float(0.2 * std::sqrt(double(l))) : 1.0f;
     mm.tensor = i;
     mm.tall = t.rows >= t.cols ? 1 : 0;
-    mm.sr_blocks = int32_t((l + kSrBlock - 1) / kSrBlock);
+    const int bucket = mm.tall ? sr_tall_bucket(s) : sr_wide_bucket(s);
+    if (mm.vec_ok && s <= kSrMaxRegSide && bucket > 0) {
+      mm.sr_kind = mm.tall ? kSrTall : (s <= 1024 ? kSrWide : kSrWideNarrow);
+      mm.sr_bucket = bucket;
+      mm.sr_blocks = int32_t((l + (mm.tall ? kSrTallRows : kSrWideCols) - 1) /
+                             (mm.tall ? kSrTallRows : kSrWideCols));
+    } else {
+      mm.sr_kind = kSrGeneric;
+      mm.sr_bucket = 0;
+      mm.sr_blocks = int32_t((l + kSrBlock - 1) / kSrBlock);
+    }
     if (p->adaptive) {
       const int64_t chunks = (s + kSrChunk - 1) / kSrChunk;
-      if (int64_t(p->sr_start.back()) + mm.sr_blocks > INT32_MAX ||
+      if (int64_t(p->sr_tab.size()) + mm.sr_blocks > INT32_MAX ||
           int64_t(p->rd_start.back()) + chunks > INT32_MAX) {
         *err = "too many elements for the stable-rank passes";
         return Status::kUnsupported;
       }
-      p->sr_start.push_back(p->sr_start.back() + mm.sr_blocks);
+      for (int32_t b = 0; b < mm.sr_blocks; ++b) p->sr_tab.push_back({int32_t(p->mats.size()), b});
       p->rd_start.push_back(p->rd_start.back() + int32_t(chunks));
       p->candidate_elements += t.rows * t.cols;
     }
@@ -288,6 +316,18 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
   p->ws_rscale_off = off;
   off = align256(off + p->mats.size() * sizeof(float));
   if (p->adaptive) {
+    // pass workgroups grouped by (kind, bucket), matrices in list order
+    std::stable_sort(p->sr_tab.begin(), p->sr_tab.end(), [&](const SrBlock& a, const SrBlock& b) {
+      const MuonMat &x = p->mats[size_t(a.mat)], &y = p->mats[size_t(b.mat)];
+      return std::make_pair(x.sr_kind, x.sr_bucket) < std::make_pair(y.sr_kind, y.sr_bucket);
+    });
+    for (size_t i = 0; i < p->sr_tab.size(); ++i) {
+      const MuonMat& mm = p->mats[size_t(p->sr_tab[i].mat)];
+      if (p->sr_classes.empty() || p->sr_classes.back().kind != mm.sr_kind ||
+          p->sr_classes.back().bucket != mm.sr_bucket)
+        p->sr_classes.push_back({mm.sr_kind, mm.sr_bucket, int32_t(i), 0});
+      ++p->sr_classes.back().count;
+    }
     p->ws_decide_off = off;
     off = align256(off + p->mats.size() * sizeof(int32_t));
     for (MuonMat& mm : p->mats) {

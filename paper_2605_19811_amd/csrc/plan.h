@@ -79,7 +79,13 @@ struct Plan {
   // Adaptive step: every candidate sits in `mats` AND in `lion` (gated by its
   // decision); prefix sums of the stable-rank pass blocks and reduction
   // chunks, and the candidate index of each input tensor (-1: none).
-  std::vector<int32_t> sr_start, rd_start;
+  struct SrClass {
+    int32_t kind, bucket;    // SrKind and register bucket
+    int32_t first, count;    // range of sr_tab
+  };
+  std::vector<SrBlock> sr_tab;             // pass workgroups, grouped by class
+  std::vector<SrClass> sr_classes;
+  std::vector<int32_t> rd_start;
   std::vector<int32_t> tensor_mat;
   int64_t candidate_elements = 0;
 
@@ -103,6 +109,16 @@ Status validate_tensors(const TensorIn* x, int32_t n, std::string* err);
 // scaling.
 Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
                   bool kappa_rms02, Plan* out, std::string* err);
+
+// Register buckets of the stable-rank passes: the smallest listed bucket
+// holding ceil(s / 256) column chunks (tall, s <= 2048), ceil(s / 128) row
+// passes (wide, s <= 1024) or ceil(s / 256) row passes (narrow wide,
+// 1024 < s <= 1536); 0 where no bucket fits (generic path).
+constexpr int kSrTallBuckets[] = {1, 2, 3, 4, 6, 8};
+constexpr int kSrWideBuckets[] = {1, 2, 4, 6, 8};
+constexpr int kSrNarrowBuckets[] = {1, 2, 4, 6};
+int sr_tall_bucket(int64_t s);
+int sr_wide_bucket(int64_t s);
 
 // Split an ordered task list (cost = inner dimension of each tile) into one
 // contiguous segment per XCD with near-equal total cost, then order each

@@ -390,7 +390,7 @@ def test_plan_info_adaptive_step(lib):
         if t.lion_only or t.rows == 1:
             continue
         s, l = min(t.rows, t.cols), max(t.rows, t.cols)
-        nb = -(-l // 32)                                         # 32 long-side positions a block
+        nb = -(-l // 64)                      # register paths: 64 long-side positions a block
         blocks += nb
         part += nb * s
         extra += (s + nb * s + 2 * nb + -(-s // 64)) * 8
@@ -399,3 +399,10 @@ def test_plan_info_adaptive_step(lib):
     ws_extra = info["workspace_bytes"] - muon["workspace_bytes"]
     assert extra <= ws_extra < extra + 256 * (48 + 2)
     assert lm.lionmuon_workspace_bytes(specs, cfg) == info["workspace_bytes"]
+    # generic path (rows not a multiple of 4 floats, or a short side beyond the
+    # register paths): blocks of 32 positions
+    for shape, nb in [((97, 61), 4), ((61, 97), 4), ((3000, 2100), 94), ((1600, 1700), 54),
+                      ((1100, 1300), 21), ((1300, 1284), 21), ((700, 900), 15)]:
+        one = lm.lionmuon_plan_info([(*shape, False)], t=0, P=0,
+                                    cfg=lm.config(adaptive_alpha=0.01, adaptive_power_steps=1))
+        assert one["srank_bytes"] == 4.0 * shape[0] * shape[1] * 2 + 16.0 * nb * min(shape), shape

@@ -239,3 +239,46 @@ def test_adaptive_full_set(name):
     del params, moms, grads, tl
     lm.lionmuon_release()
     torch.cuda.empty_cache()
+
+
+# one matrix per pass variant: tall register buckets 1, 2, 3, 4, 6, 8 column
+# chunks; wide 128-row buckets 1, 2, 4, 6, 8; narrow wide (short side above
+# 1024) buckets 6; generic path for wide short sides above 1536, tall short
+# sides above 2048 and rows that are not a multiple of 4 floats
+BUCKET_SHAPES = [(70, 8), (600, 500), (700, 700), (1100, 1000), (1300, 1284), (2100, 2048),
+                 (8, 70), (200, 300), (500, 600), (700, 900), (1000, 1200),
+                 (1100, 1300), (1500, 1600), (1600, 1700), (2200, 2100), (1030, 1027)]
+
+
+@pytest.mark.parametrize("k", [0, 3])
+def test_adaptive_every_pass_variant(k):
+    n = len(BUCKET_SHAPES)
+    rng = np.random.default_rng(95 + k)
+    M0 = [low_rank_momentum([96, i], s, 2, 1e-2) if i % 2 == 0 else
+          (rng.standard_normal(s) * 1e-2).astype(np.float32) for i, s in enumerate(BUCKET_SHAPES)]
+    W0 = [(rng.standard_normal(s) * 0.02).astype(np.float32) for s in BUCKET_SHAPES]
+    G = [(rng.standard_normal(s) * 1e-2).astype(np.float32) for s in BUCKET_SHAPES]
+    W, M = [dev(x) for x in W0], [dev(x) for x in M0]
+    dec = torch.zeros(n, dtype=torch.int32, device=DEV)
+    sr = torch.zeros(n, dtype=torch.float64, device=DEV)
+    alpha = 0.01
+    cfg = lm.config(lr_muon=0.02, lr_lion=1e-3, adaptive_alpha=alpha, adaptive_power_steps=k)
+    print(f"pass variants k={k}", flush=True)
+    lm.lionmuon_step_adaptive(W, [dev(g) for g in G], M, 1, 0.9, 0.99, 0.1, cfg, decisions=dec,
+                              stable_rank=sr)
+    torch.cuda.synchronize()
+    dec, sr = dec.cpu().numpy(), sr.cpu().numpy()
+    check_decisions(M0, set(range(n)), dec, sr, alpha, k)
+    if k == 3:
+        assert dec[[2, 4, 8, 10, 12, 14]].all() and not dec[[0, 1, 3, 5, 6, 7, 9, 11, 13, 15]].any(), dec
+    for i, s in enumerate(BUCKET_SHAPES):
+        if s[0] * s[1] > 1_000_000:        # updates of the large ones: sampled rows, Lion only
+            if not dec[i]:
+                check_lion(W0[i][:64], G[i][:64], M0[i][:64], host(W[i])[:64], host(M[i])[:64],
+                           0.9, 0.99, 1e-3, 0.1)
+            continue
+        if dec[i]:
+            check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 0.02, 0.1, "bf16"
+                       if min(s) >= 64 else "fp32")
+        else:
+            check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 1e-3, 0.1)
