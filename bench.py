@@ -90,9 +90,17 @@ def pmc_summary(wl_name, fetch_csv, write_csv, calib_fetch_csv, calib_write_csv,
     fetch = _counter_means(fetch_csv, "FETCH_SIZE")
     write = _counter_means(write_csv, "WRITE_SIZE")
     kernels = {}
+    # the stable-rank phase is several kernels per step: bytes per step =
+    # all of its dispatches / the decide dispatches (one per step)
+    steps = [len(v) for k, v in fetch.items() if "srank_decide" in k]
+    srank = {"fetch_bytes": 0.0, "write_bytes": 0.0}
     for name in set(fetch) | set(write):
         ph = phase_of(name)
         if ph is None:
+            continue
+        if ph == "srank":
+            srank["fetch_bytes"] += sum(fetch.get(name, [])) * 1024.0 * f_scale / steps[0]
+            srank["write_bytes"] += sum(write.get(name, [])) * 1024.0 * w_scale / steps[0]
             continue
         fv, wv = fetch.get(name, []), write.get(name, [])
         fb = sum(fv) / len(fv) * 1024.0 * f_scale if fv else 0.0
@@ -106,6 +114,9 @@ def pmc_summary(wl_name, fetch_csv, write_csv, calib_fetch_csv, calib_write_csv,
         k["write_bytes"] /= k["launch_kinds"]
         k["bytes_per_launch"] = k["fetch_bytes"] + k["write_bytes"]
         del k["launch_kinds"]
+    if steps:
+        srank["bytes_per_launch"] = srank["fetch_bytes"] + srank["write_bytes"]
+        kernels["srank"] = srank
     out = {"workload": wl_name, "kernel_source_sha256_16": kernel_hash(),
            "fetch_scale": f_scale, "write_scale": w_scale,
            "calibration": f"plain device copy of {calib_mib} MiB (torch copy_)",
@@ -216,12 +227,14 @@ def main():
                     help="write profiles/kernel_trace_<workload>.md from a rocprofv3 stats CSV")
     ap.add_argument("--command", default="", help="profiling command recorded in summaries")
     args = ap.parse_args()
+    # profiles of the adaptive variant are kept apart from the periodic step's
+    prof_name = args.workload + ("-adaptive" if args.adaptive > 0.0 else "")
     if args.pmc_summary:
-        print(pmc_summary(args.workload, *args.pmc_summary, calib_mib=1024,
+        print(pmc_summary(prof_name, *args.pmc_summary, calib_mib=1024,
                           commands=args.command))
         return
     if args.trace_summary:
-        print(trace_summary(args.workload, args.trace_summary, args.command))
+        print(trace_summary(prof_name, args.trace_summary, args.command))
         return
     if args.calib_copy:
         import torch
@@ -374,7 +387,7 @@ def main():
             roof = {"kernel": kernel_names[dom], "bound": "hbm", "achieved": None,
                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": None}
         roof["avg_launch_ms"] = d["avg_ms"]
-        roof["traffic"] = load_traffic(wl.name, dom)
+        roof["traffic"] = load_traffic(prof_name, dom)
         out["roofline"] = roof
     if not args.no_cpu_baseline and not adaptive:
         out["cpu_baseline"] = cpu_baseline(wl, P)
