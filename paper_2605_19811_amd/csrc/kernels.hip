@@ -4,9 +4,9 @@
 //                M = b2*M + (1-b2)*G. Multi-tensor, 16-byte vectors, HBM bound.
 //                Tensors flagged AdamW take the AdamW update in the same launch.
 //  prep_kernel   Muon branch, first pass: the same interpolation and momentum
-//                update, Ghat stored in the NS element type in both the
-//                iteration orientation X (rows <= cols) and its transpose, and
-//                a per-tile partial sum of Ghat^2 (wave shuffles + LDS).
+//                update, Ghat stored in the NS element type in the iteration
+//                orientation X (rows <= cols; an LDS transpose for tall
+//                matrices), and a per-tile partial sum of Ghat^2.
 //  norm_kernel   fixed-order reduction of the partials -> 1/(||Ghat||_F + eps).
 //  srank_*       adaptive step: fp64 power iteration for the stable rank of
 //                each candidate's momentum and the per-matrix Muon / Lion
@@ -14,8 +14,9 @@
 //  ns_*_kernel   the Newton-Schulz products on MFMA with fp32 accumulation:
 //                Gram A = X X^T and polynomial B' = a I + b A + c A A on the
 //                lower triangle of tiles (mirrored on store), then apply
-//                X' = B' X (= a X + (b A + c A A) X) with the W update fused
-//                into the last step's epilogue.
+//                X' = B' X (= a X + (b A + c A A) X), whose X operand is read
+//                from row-major X through LDS transpose reads, with the W
+//                update fused into the last step's epilogue.
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -201,8 +202,10 @@ __device__ __forceinline__ void prep_tile(const PrepArgs& a, const MuonMat& mm, 
   const int64_t rows_pad = mm.transposed ? mm.l_pad : mm.s_pad;
   const int64_t cols_pad = mm.transposed ? mm.s_pad : mm.l_pad;
   char* ws = static_cast<char*>(a.ws);
-  T* S = reinterpret_cast<T*>(ws + (mm.transposed ? mm.off_xt[0] : mm.off_x[0]));   // rows_pad x cols_pad
-  T* Tt = reinterpret_cast<T*>(ws + (mm.transposed ? mm.off_x[0] : mm.off_xt[0]));  // cols_pad x rows_pad
+  // X (s_pad x l_pad): Ghat itself for a wide matrix, Ghat^T (through an LDS
+  // transpose) for a tall one
+  T* X = reinterpret_cast<T*>(ws + mm.off_x[0]);
+  const bool tall = mm.transposed != 0;
   const int tid = threadIdx.x, r0 = tid >> 4, c4 = (tid & 15) * 4;
   float ss = 0.0f;
 #pragma unroll
@@ -247,18 +250,23 @@ __device__ __forceinline__ void prep_tile(const PrepArgs& a, const MuonMat& mm, 
           if (q + e < mm.cols) mm.m[idx + e] = mn[e];
       }
     }
-    store4(S + p * cols_pad + q, c);
+    if (!tall) {
+      store4(X + p * cols_pad + q, c);
+    } else {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) tile[r][c4 + e] = to_elem<T>(c[e]);
+      for (int e = 0; e < 4; ++e) tile[r][c4 + e] = to_elem<T>(c[e]);
+    }
   }
-  __syncthreads();
+  if (tall) {                            // uniform over the workgroup
+    __syncthreads();
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int qq = r0 + 16 * u;          // column of the source tile
-    float v[4];
+    for (int u = 0; u < 4; ++u) {
+      const int qq = r0 + 16 * u;        // column of the source tile
+      float v[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] = float(tile[c4 + e][qq]);
-    store4(Tt + (int64_t(tj) * kPrepTile + qq) * rows_pad + int64_t(ti) * kPrepTile + c4, v);
+      for (int e = 0; e < 4; ++e) v[e] = float(tile[c4 + e][qq]);
+      store4(X + (int64_t(tj) * kPrepTile + qq) * rows_pad + int64_t(ti) * kPrepTile + c4, v);
+    }
   }
   ss = wave_sum(ss);
   if ((tid & 63) == 0) red[tid >> 6] = ss;
@@ -813,13 +821,47 @@ __global__ __launch_bounds__(256) void srank_decide_kernel(SrankArgs a) {
 // direct global->LDS loads (no register staging), double buffered: the loads
 // of stage k+1 are in flight while stage k feeds the MFMAs. Rows are
 // unpadded; their eight 16-byte chunks are XOR-swizzled by row so that the
-// MFMA fragment reads are bank-conflict free.
+// 128-bit fragment reads, served 16 lanes (16 rows) per LDS cycle across 64
+// banks, are bank-conflict free.
 //   BT = 256: 8 waves (2 x 4), each a 128 x 64 sub-tile of 4 x 2 MFMA 32x32
 //             blocks (32 B of operand loads per CU-clock at full MFMA rate);
 //   BT = 128: 4 waves (2 x 2), each a 64 x 64 sub-tile of 2 x 2 blocks, for
 //             stages with too few 256-tiles to fill the chip.
 // Accumulator element r of block (mi, ni) sits at row
 // wm + 32 mi + 8 (r / 4) + 4 (lane / 32) + r % 4, col wn + 32 ni + lane % 32.
+// Workgroup barrier that orders LDS accesses only: unlike __syncthreads it
+// does not wait for this wave's outstanding global stores, so output tiles
+// drain to memory while the workgroup goes on.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Lane exchanges within a quad of lanes through DPP (no LDS traffic).
+__device__ __forceinline__ float dpp_quad_xor1(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1,
+                                                            0xF, 0xF, true));   // [1,0,3,2]
+}
+__device__ __forceinline__ float dpp_quad_xor2(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E,
+                                                            0xF, 0xF, true));   // [2,3,0,1]
+}
+
+// 4 x 4 transpose across the quad: lane b enters with v[e] = C[e][b] and
+// leaves with v[j] = C[b][j]. Two exchange rounds (partners b ^ 2, then
+// b ^ 1), each lane sending two values and receiving two.
+__device__ __forceinline__ void quad_transpose(float v[4], int b) {
+  const bool lo = b < 2;
+  float s0 = dpp_quad_xor2(lo ? v[2] : v[0]);
+  float s1 = dpp_quad_xor2(lo ? v[3] : v[1]);
+  if (lo) { v[2] = s0; v[3] = s1; } else { v[0] = s0; v[1] = s1; }
+  const bool even = (b & 1) == 0;
+  s0 = dpp_quad_xor1(even ? v[1] : v[0]);
+  s1 = dpp_quad_xor1(even ? v[3] : v[2]);
+  if (even) { v[1] = s0; v[3] = s1; } else { v[0] = s0; v[2] = s1; }
+}
+
 template <typename T> struct Mfma;
 
 template <> struct Mfma<bf16> {
@@ -871,14 +913,21 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   constexpr int kEpc = 16 / sizeof(T);           // elements per 16-byte chunk
   constexpr int kLd = kBK;                       // LDS row: 128 bytes, chunks XOR-swizzled
   constexpr int kNT = Geo::kThreads;
-  constexpr int kLoads = BT * 8 / kNT;           // 16-byte chunks per thread per operand
   constexpr int kMI = Geo::kMI, kNI = Geo::kNI;
   // One LDS block: two operand stages during the K loop, then the output tile.
-  constexpr int kSt = BT + kEpc;                 // output staging row stride
-  constexpr int kOperand = 2 * 2 * BT * kLd, kStage = BT * kSt;
+  // Output staging row strides: kStR for row-major staging (16-byte-aligned
+  // rows, 8 or 16 dwords apart modulo the 64 banks, so a quad of lanes
+  // writing 4 consecutive rows never collides), kStC for transposed staging
+  // (4 dwords apart, so 16 lanes writing 16 consecutive rows never collide).
+  constexpr int kStR = BT + 16, kStC = BT + kEpc;
+  constexpr int kOperand = 2 * 2 * BT * kLd, kStage = BT * kStR;
   __shared__ __attribute__((aligned(16))) T smem[kOperand > kStage ? kOperand : kStage];
   T (*sA)[BT][kLd] = reinterpret_cast<T (*)[BT][kLd]>(smem);
   T (*sB)[BT][kLd] = reinterpret_cast<T (*)[BT][kLd]>(smem + 2 * BT * kLd);
+  // apply: the B operand (X, K = s along its rows) is staged k-major as
+  // kBK rows of BT elements (512 bytes) and read transposed
+  constexpr bool kBRows = MODE == kApply;
+  T (*sBr)[kBK][BT] = reinterpret_cast<T (*)[kBK][BT]>(smem + 2 * BT * kLd);
 
   const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
   if (slot >= g.split->count[xcd]) return;
@@ -890,8 +939,6 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // ping-pong buffers chosen without indexing (keeps descriptors out of scratch)
   const int64_t off_x_cur = g.src ? mm.off_x[1] : mm.off_x[0];
   const int64_t off_x_nxt = g.src ? mm.off_x[0] : mm.off_x[1];
-  const int64_t off_xt_cur = g.src ? mm.off_xt[1] : mm.off_xt[0];
-  const int64_t off_xt_nxt = g.src ? mm.off_xt[0] : mm.off_xt[1];
   const T* Aop;
   const T* Bop;
   int64_t lda, ldb;
@@ -906,31 +953,53 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
     K = mm.s_pad;
   } else {
     Aop = at(mm.off_b);
-    Bop = at(off_xt_cur);
-    lda = ldb = mm.s_pad;
+    Bop = at(off_x_cur);
+    lda = mm.s_pad;
+    ldb = mm.l_pad;
     K = mm.s_pad;
   }
   const int row0 = task.tm * BT, col0 = task.tn * BT;
   Aop += row0 * lda;
-  Bop += col0 * ldb;
+  Bop += kBRows ? col0 : col0 * ldb;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
   const int wm = (wave / Geo::kWavesN) * Geo::kWM, wn = (wave % Geo::kWavesN) * Geo::kWN;
-  const int ld_row = tid >> 3, ld_ch = (tid & 7) * kEpc;
 
+  // Physical chunk of logical chunk c in row `row` is c ^ swz(row): among
+  // any 16 consecutive rows the two rows of each parity class (which share a
+  // bank half) get distinct chunks.
+  auto swz = [](int row) { return (row & 7) ^ ((row >> 3) & 1); };
   // Each wave instruction fills 8 rows (1 KB): lane L writes row L/8,
-  // physical chunk L%8, and fetches logical chunk (L%8) ^ (row & 7).
+  // physical chunk L%8, and fetches the logical chunk that lands there.
   constexpr int kWaves = kNT / 64;
   constexpr int kInst = BT / 8 / kWaves;         // wave instructions per operand per stage
+  // k-major B rows (apply): kChunksB 16-byte chunks per row, each wave
+  // instruction fills kRpiB rows; chunks are XOR-swizzled by swb(k) so that
+  // the 4 rows of a transpose read fall into disjoint bank ranges.
+  constexpr int kChunksB = BT * int(sizeof(T)) / 16;
+  constexpr int kRpiB = 64 / kChunksB;
+  constexpr int kInstB = kBK / kRpiB / kWaves;
+  static_assert(!kBRows || kInstB * kRpiB * kWaves == kBK, "B rows split evenly over the waves");
+  auto swb = [](int k) { return (k & 3) * 2; };
   auto dma = [&](int buf, int k0) {
 #pragma unroll
     for (int q = 0; q < kInst; ++q) {
       const int blk = q * kWaves + wave;         // 8-row block
       const int row = blk * 8 + (lane >> 3);
-      const int ch = (lane & 7) ^ (row & 7);
+      const int ch = (lane & 7) ^ swz(row);
       __builtin_amdgcn_global_load_lds(Aop + row * lda + k0 + ch * kEpc, &sA[buf][blk * 8][0], 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(Bop + row * ldb + k0 + ch * kEpc, &sB[buf][blk * 8][0], 16, 0, 0);
+      if constexpr (!kBRows)
+        __builtin_amdgcn_global_load_lds(Bop + row * ldb + k0 + ch * kEpc, &sB[buf][blk * 8][0], 16, 0, 0);
+    }
+    if constexpr (kBRows) {
+#pragma unroll
+      for (int q = 0; q < kInstB; ++q) {
+        const int rr = (q * kWaves + wave) * kRpiB;  // first of the instruction's rows
+        const int k = rr + lane / kChunksB;
+        const int ch = (lane % kChunksB) ^ swb(k);
+        __builtin_amdgcn_global_load_lds(Bop + int64_t(k0 + k) * ldb + ch * kEpc, &sBr[buf][rr][0], 16, 0, 0);
+      }
     }
   };
 
@@ -944,8 +1013,33 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
 
   auto frag = [&](const T* rowp, int row, int kc) {
     const int e = kc + lk * (M::kKStep / 2);
-    const int off = (((e / kEpc) ^ (row & 7)) * kEpc) + (e % kEpc);
+    const int off = (((e / kEpc) ^ swz(row)) * kEpc) + (e % kEpc);
     return M::load(rowp + off, 0);
+  };
+  // B fragment of block column j from k-major rows: the MFMA wants, in lane
+  // (n = lane % 32, half lk), B[kc + lk kKStep/2 + t][n] for t < kKStep/2.
+  auto frag_b_rows = [&](int buf, int j, int kc) -> typename M::Frag {
+    if constexpr (sizeof(T) == 2) {
+      // Two transpose reads of 4 k each. Within each 16-lane group, lane m
+      // points at row kb + (m >> 2), columns n0 + 4 (m & 3) .. +3, and
+      // receives column n0 + m of rows kb .. kb + 3.
+      const int grp = lane >> 4, m = lane & 15;
+      const int n = wn + 32 * j + 16 * (grp & 1) + 4 * (m & 3);
+      const int kb = kc + 8 * (grp >> 1) + (m >> 2);
+      bf16x4 h[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int k = kb + 4 * t;
+        const int off = (((n >> 3) ^ swb(k)) << 3) + (n & 7);
+        // (a C cast: it converts the generic pointer to the LDS address space)
+        h[t] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (__attribute__((address_space(3))) bf16x4*)(&sBr[buf][k][off]));
+      }
+      return typename M::Frag{h[0][0], h[0][1], h[0][2], h[0][3], h[1][0], h[1][1], h[1][2], h[1][3]};
+    } else {
+      const int k = kc + lk, n = wn + 32 * j + lr;
+      return sBr[buf][k][(((n >> 2) ^ swb(k)) << 2) + (n & 3)];
+    }
   };
   auto compute = [&](int buf) {
     // fragments double-buffered in registers: the LDS reads of substep kk+1
@@ -957,7 +1051,10 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
 #pragma unroll
       for (int i = 0; i < kMI; ++i) af[s][i] = frag(&sA[buf][wm + 32 * i + lr][0], wm + 32 * i + lr, kc);
 #pragma unroll
-      for (int j = 0; j < kNI; ++j) bfr[s][j] = frag(&sB[buf][wn + 32 * j + lr][0], wn + 32 * j + lr, kc);
+      for (int j = 0; j < kNI; ++j) {
+        if constexpr (kBRows) bfr[s][j] = frag_b_rows(buf, j, kc);
+        else bfr[s][j] = frag(&sB[buf][wn + 32 * j + lr][0], wn + 32 * j + lr, kc);
+      }
     };
     fetch(0, 0);
 #pragma unroll
@@ -990,32 +1087,39 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // tile (row-major, or transposed with 8-byte writes), then the workgroup
   // stores whole rows with coalesced 16-byte stores.
   const int64_t s_pad = mm.s_pad, l_pad = mm.l_pad;
-  T (*stage)[kSt] = reinterpret_cast<T (*)[kSt]>(smem);
+  T (*stage)[kStR] = reinterpret_cast<T (*)[kStR]>(smem);
+  T (*stage_t)[kStC] = reinterpret_cast<T (*)[kStC]>(smem);
   constexpr int kRowChunks = BT * int(sizeof(T)) / 16;
-  auto flush = [&](T* dst, int64_t ld) {        // stage (BT x BT) -> dst rows
-    __syncthreads();
+  auto flush = [&](T* dst, int64_t ld, const T* stg, int stride) {  // staged tile -> dst rows
+    lds_barrier();
 #pragma unroll 4
     for (int c = tid; c < BT * kRowChunks; c += kNT) {
       const int r = c / kRowChunks, ch = (c % kRowChunks) * kEpc;
-      *reinterpret_cast<u32x4*>(dst + r * ld + ch) = *reinterpret_cast<const u32x4*>(&stage[r][ch]);
+      *reinterpret_cast<u32x4*>(dst + r * ld + ch) = *reinterpret_cast<const u32x4*>(stg + r * stride + ch);
     }
-    __syncthreads();
+    lds_barrier();
   };
   // v(mi, ni, q, e): value of local row wm + 32 mi + 8 q + 4 lk + e, local
-  // column wn + 32 ni + lr.
+  // column wn + 32 ni + lr. Row-major staging first transposes each 4 x 4
+  // block within a quad of lanes (DPP, no LDS traffic), so that every lane
+  // writes 4 consecutive columns of one row in a single store.
   auto stage_rows = [&](auto&& val) {
+    const int b = lane & 3;
 #pragma unroll
     for (int mi = 0; mi < kMI; ++mi)
 #pragma unroll
       for (int ni = 0; ni < kNI; ++ni)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int r = wm + 32 * mi + 8 * q + 4 * lk, c = wn + 32 * ni + lr;
+          float v[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) stage[r + e][c] = to_elem<T>(val(mi, ni, q, e));
+          for (int e = 0; e < 4; ++e) v[e] = val(mi, ni, q, e);
+          quad_transpose(v, b);
+          const int r = wm + 32 * mi + 8 * q + 4 * lk + b, c = wn + 32 * ni + (lr & ~3);
+          store4(&stage[r][c], v);
         }
   };
-  auto stage_cols = [&](auto&& val) {           // transposed: stage[col][row..row+3]
+  auto stage_cols = [&](auto&& val) {           // transposed: stage_t[col][row..row+3]
 #pragma unroll
     for (int mi = 0; mi < kMI; ++mi)
 #pragma unroll
@@ -1026,10 +1130,10 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
           float v[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] = val(mi, ni, q, e);
-          store4(&stage[c][r], v);
+          store4(&stage_t[c][r], v);
         }
   };
-  __syncthreads();                               // operand stages no longer read
+  lds_barrier();                                 // operand stages no longer read
 
   if (MODE == kGram || MODE == kPoly) {
     float alpha = 1.0f;
@@ -1062,10 +1166,10 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
     T* out = at(MODE == kGram ? mm.off_a : mm.off_b);
     auto val = [&](int mi, int ni, int q, int e) { return alpha * acc[mi][ni][4 * q + e]; };
     stage_rows(val);
-    flush(out + row0 * s_pad + col0, s_pad);
+    flush(out + row0 * s_pad + col0, s_pad, &stage[0][0], kStR);
     if (task.tm != task.tn) {                    // mirror into the upper triangle
       stage_cols(val);
-      flush(out + col0 * s_pad + row0, s_pad);
+      flush(out + col0 * s_pad + row0, s_pad, &stage_t[0][0], kStC);
     }
   } else {
     // X' = alpha B' X with B' = a I + b A + c A A from the polynomial step
@@ -1079,9 +1183,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
     if (!g.last) {
       auto val = [&](int mi, int ni, int q, int e) { return acc[mi][ni][4 * q + e]; };
       stage_rows(val);
-      flush(at(off_x_nxt) + row0 * l_pad + col0, l_pad);
-      stage_cols(val);
-      flush(at(off_xt_nxt) + col0 * s_pad + row0, s_pad);
+      flush(at(off_x_nxt) + row0 * l_pad + col0, l_pad, &stage[0][0], kStR);
     } else {
       // last step: W <- W - lr (kappa O + wd W), or O = kappa X_K (NS hook).
       // O is X_K, transposed back for tall matrices. The fp32 O tile goes
@@ -1114,7 +1216,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
                 store4(&fst[c - h * kHalf][r], o);
               }
             }
-        __syncthreads();
+        lds_barrier();
         for (int idx = tid; idx < kHalf * (BT / 4); idx += kNT) {
           const int i = idx / (BT / 4), j = (idx % (BT / 4)) * 4;
           const int64_t gr = wrow0 + h * kHalf + i, gc = wcol0 + j;
@@ -1145,7 +1247,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
             }
           }
         }
-        __syncthreads();
+        lds_barrier();
       }
     }
   }

@@ -62,8 +62,7 @@ struct MuonMat {
   int32_t vec_ok;          // 16-byte vector access legal on w, g, m rows
   int32_t fp32;            // 1: fp32 Newton-Schulz buffers, 0: bf16
   int32_t tensor;          // index of the tensor in the caller's list
-  int64_t off_x[2];        // X  (s_pad x l_pad), ping-pong
-  int64_t off_xt[2];       // X^T (l_pad x s_pad), ping-pong
+  int64_t off_x[2];        // X (s_pad x l_pad, row-major), ping-pong
   int64_t off_a;           // A = X X^T (s_pad x s_pad)
   int64_t off_b;           // B' = a I + b A + c A A (s_pad x s_pad)
   int32_t prep_first;      // first preparation tile of this matrix

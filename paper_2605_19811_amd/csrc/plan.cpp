@@ -223,8 +223,6 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
     const int64_t sl = int64_t(mm.s_pad) * mm.l_pad * eb, ss = int64_t(mm.s_pad) * mm.s_pad * eb;
     mm.off_x[0] = ns_off;  ns_off += sl;
     mm.off_x[1] = ns_off;  ns_off += sl;
-    mm.off_xt[0] = ns_off; ns_off += sl;
-    mm.off_xt[1] = ns_off; ns_off += sl;
     mm.off_a = ns_off;     ns_off += ss;
     mm.off_b = ns_off;     ns_off += ss;
     const int64_t rows_pad = mm.transposed ? mm.l_pad : mm.s_pad;
