@@ -127,6 +127,37 @@ def pmc_summary(wl_name, fetch_csv, write_csv, calib_fetch_csv, calib_write_csv,
     return path
 
 
+def sq_summary(wl_name, sq_csv, command):
+    """MFMA and LDS occupancy of each library kernel from one rocprofv3 SQ
+    counter pass (sums over all dispatches of the kernel)."""
+    import collections
+    import csv
+    tot = collections.defaultdict(lambda: collections.defaultdict(float))
+    for r in csv.DictReader(open(sq_csv)):
+        if phase_of(r["Kernel_Name"]) is None:
+            continue
+        tot[r["Kernel_Name"]][r["Counter_Name"]] += float(r["Counter_Value"])
+    lines = [f"# SQ counters: {wl_name}", "", f"Command: `{command}`", "",
+             "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x SQ_BUSY_CU_CYCLES): the fraction of "
+             "SIMD cycles, while the CU is busy, in which the matrix core is executing (a "
+             "32x32x16 bf16 MFMA occupies its SIMD for 32 cycles; 1024 flop per SIMD-cycle is "
+             "the nominal peak). Wait = SQ_WAIT_ANY / SQ_WAVE_CYCLES. LDS conflict = "
+             "SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE.", "",
+             "| kernel | phase | MFMA busy | wait | LDS conflict |", "|---|---|---|---|---|"]
+    for name, c in sorted(tot.items(), key=lambda kv: phase_of(kv[0])):
+        busy = c.get("SQ_BUSY_CU_CYCLES", 0.0)
+        mf = c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (4.0 * busy) if busy else 0.0
+        wt = c.get("SQ_WAIT_ANY", 0.0) / c["SQ_WAVE_CYCLES"] if c.get("SQ_WAVE_CYCLES") else 0.0
+        lc = (c.get("SQ_LDS_BANK_CONFLICT", 0.0) / c["SQ_LDS_IDX_ACTIVE"]
+              if c.get("SQ_LDS_IDX_ACTIVE") else 0.0)
+        short = name if len(name) < 70 else name[:67] + "..."
+        lines.append(f"| `{short}` | {phase_of(name)} | {mf:.3f} | {wt:.3f} | {lc:.3f} |")
+    path = os.path.join(TRAFFIC_DIR, f"sq_{wl_name}.md")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    return path
+
+
 def trace_summary(wl_name, stats_csv, command):
     """Text summary of a rocprofv3 --kernel-trace --stats run."""
     import csv
@@ -225,6 +256,8 @@ def main():
                     help="write profiles/traffic_<workload>.json from rocprofv3 counter CSVs")
     ap.add_argument("--trace-summary", metavar="KERNEL_STATS_CSV",
                     help="write profiles/kernel_trace_<workload>.md from a rocprofv3 stats CSV")
+    ap.add_argument("--sq-summary", metavar="SQ_CSV",
+                    help="write profiles/sq_<workload>.md from a rocprofv3 SQ counter CSV")
     ap.add_argument("--command", default="", help="profiling command recorded in summaries")
     args = ap.parse_args()
     # profiles of the adaptive variant are kept apart from the periodic step's
@@ -235,6 +268,9 @@ def main():
         return
     if args.trace_summary:
         print(trace_summary(prof_name, args.trace_summary, args.command))
+        return
+    if args.sq_summary:
+        print(sq_summary(prof_name, args.sq_summary, args.command))
         return
     if args.calib_copy:
         import torch
@@ -367,7 +403,31 @@ def main():
         if n_muon_steps:
             out["ns_tflops"] = round(info_muon["ns_flops"] * n_muon_steps / (ns_ms * 1e-3) / 1e12, 1)
             out["ns_frac_bf16_peak"] = round(out["ns_tflops"] / BF16_PEAK_TFLOPS, 4)
+            out["ns_tflops_dense_convention"] = round(
+                info_muon["ns_flops_dense"] * n_muon_steps / (ns_ms * 1e-3) / 1e12, 1)
             out["ns_ms_per_muon_step"] = round(ns_ms / n_muon_steps, 4)
+        if not adaptive:
+            # time split of the two step kinds and the amortisation cross-check
+            # ((P-1) T_lion + T_muon) / P against the measured ms/step
+            lion_ms = phases["lion"]["ms"]
+            muon_ms = sum(phases[p]["ms"] for p in ("prep", "norm", "gram", "poly", "apply"))
+            split = {}
+            if n_lion_steps:
+                lion_only_ms = 0.0
+                if n_muon_steps and info_muon["lion_elements"] and phases["lion"]["launches"]:
+                    # Lion-only tensors on Muon steps: pro rata by element count
+                    per_elem = lion_ms / (n_lion_steps * info_lion["lion_elements"]
+                                          + n_muon_steps * info_muon["lion_elements"])
+                    lion_only_ms = per_elem * n_muon_steps * info_muon["lion_elements"]
+                split["t_lion_ms"] = round((lion_ms - lion_only_ms) / n_lion_steps, 4)
+                muon_ms += lion_only_ms
+            if n_muon_steps:
+                split["t_muon_ms"] = round(muon_ms / n_muon_steps, 4)
+            if len(split) == 2 or P in (0, 1):
+                tl, tm = split.get("t_lion_ms", 0.0), split.get("t_muon_ms", 0.0)
+                split["amortised_from_split_ms"] = round(
+                    tl if P == 0 else ((P - 1) * tl + tm) / P, 4)
+            out["split"] = split
         if "lion" in ph and "gbps" in ph["lion"]:
             out["lion_gbps"] = ph["lion"]["gbps"]
             out["lion_frac_hbm_peak"] = ph["lion"]["frac_hbm_peak"]

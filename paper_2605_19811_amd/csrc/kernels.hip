@@ -976,12 +976,13 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   constexpr int kInst = BT / 8 / kWaves;         // wave instructions per operand per stage
   // k-major B rows (apply): kChunksB 16-byte chunks per row, each wave
   // instruction fills kRpiB rows; chunks are XOR-swizzled by swb(k) so that
-  // the 4 rows of a transpose read fall into disjoint bank ranges.
+  // the 4 rows x 64 bytes a transpose read serves per LDS cycle (32 lanes)
+  // fall into disjoint bank ranges.
   constexpr int kChunksB = BT * int(sizeof(T)) / 16;
   constexpr int kRpiB = 64 / kChunksB;
   constexpr int kInstB = kBK / kRpiB / kWaves;
   static_assert(!kBRows || kInstB * kRpiB * kWaves == kBK, "B rows split evenly over the waves");
-  auto swb = [](int k) { return (k & 3) * 2; };
+  auto swb = [](int k) { return (k & 3) * 4; };
   auto dma = [&](int buf, int k0) {
 #pragma unroll
     for (int q = 0; q < kInst; ++q) {
