@@ -862,6 +862,27 @@ __device__ __forceinline__ void quad_transpose(float v[4], int b) {
   if (even) { v[1] = s0; v[3] = s1; } else { v[0] = s0; v[2] = s1; }
 }
 
+// Scheduling directives for the MFMA k-steps of one stage: NM MFMAs with the
+// next k-step's NR LDS fragment reads placed one after each of the first NR
+// MFMAs, so the matrix core is not left waiting for a whole batch of reads.
+template <int I, int NM, int NR>
+__device__ __forceinline__ void sched_mfma_reads() {
+  if constexpr (I < NM) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if constexpr (I < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    sched_mfma_reads<I + 1, NM, NR>();
+  } else if constexpr (NR > NM) {
+    __builtin_amdgcn_sched_group_barrier(0x100, NR - NM, 0);
+  }
+}
+template <int S, int NM, int NR>
+__device__ __forceinline__ void sched_interleave() {
+  if constexpr (S > 0) {
+    sched_mfma_reads<0, NM, NR>();
+    sched_interleave<S - 1, NM, NR>();
+  }
+}
+
 template <typename T> struct Mfma;
 
 template <> struct Mfma<bf16> {
@@ -1042,10 +1063,23 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
       return sBr[buf][k][(((n >> 2) ^ swb(k)) << 2) + (n & 3)];
     }
   };
+  constexpr int kSub = kBK / M::kKStep;
+  // bf16 apply: the transpose-read B fragments of a whole stage are read
+  // into registers before the next stage's loads are issued. The compiler
+  // cannot tell those reads from the in-flight global->LDS copies and would
+  // otherwise wait for the copies to land before each transpose read,
+  // serialising loads and MFMAs.
+  constexpr bool kTrB = kBRows && sizeof(T) == 2;
+  typename M::Frag bq[kTrB ? kSub : 1][kNI];
+  auto preload_b = [&](int buf) {
+#pragma unroll
+    for (int kk = 0; kk < kSub; ++kk)
+#pragma unroll
+      for (int j = 0; j < kNI; ++j) bq[kTrB ? kk : 0][j] = frag_b_rows(buf, j, kk * M::kKStep);
+  };
   auto compute = [&](int buf) {
     // fragments double-buffered in registers: the LDS reads of substep kk+1
     // are issued before the MFMAs of substep kk
-    constexpr int kSub = kBK / M::kKStep;
     typename M::Frag af[2][kMI], bfr[2][kNI];
     auto fetch = [&](int s, int kk) {
       const int kc = kk * M::kKStep;
@@ -1053,7 +1087,8 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
       for (int i = 0; i < kMI; ++i) af[s][i] = frag(&sA[buf][wm + 32 * i + lr][0], wm + 32 * i + lr, kc);
 #pragma unroll
       for (int j = 0; j < kNI; ++j) {
-        if constexpr (kBRows) bfr[s][j] = frag_b_rows(buf, j, kc);
+        if constexpr (kTrB) bfr[s][j] = bq[kk][j];
+        else if constexpr (kBRows) bfr[s][j] = frag_b_rows(buf, j, kc);
         else bfr[s][j] = frag(&sB[buf][wn + 32 * j + lr][0], wn + 32 * j + lr, kc);
       }
     };
@@ -1065,7 +1100,12 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
       for (int i = 0; i < kMI; ++i)
 #pragma unroll
         for (int j = 0; j < kNI; ++j) acc[i][j] = M::mma(af[kk & 1][i], bfr[kk & 1][j], acc[i][j]);
-    }
+    }    // region order: the first fragment reads, then per k-step the MFMAs
+    // interleaved with the next k-step's reads, then the last k-step's MFMAs
+    constexpr int kReads = kMI + (kTrB ? 0 : kNI * (kBRows ? 2 : 1));
+    __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+    sched_interleave<kSub - 1, kMI * kNI, kReads>();
+    __builtin_amdgcn_sched_group_barrier(0x008, kMI * kNI, 0);
   };
 
   // The barrier after each stage both publishes the stage just loaded (every
@@ -1075,6 +1115,10 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
+    if constexpr (kTrB) {
+      preload_b(kt & 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     if (kt + 1 < nk) dma((kt + 1) & 1, (kt + 1) * kBK);
     __builtin_amdgcn_sched_barrier(0);
     compute(kt & 1);
