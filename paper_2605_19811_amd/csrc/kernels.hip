@@ -1187,8 +1187,9 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
       alpha = r * r;
     }
     if (MODE == kPoly) {
-      // B' = a I + b A + c A A (the a X term of the apply step folded into B;
-      // A is symmetric, so A[R][C] is read as A[C][R..R+3] with one 8-byte load)
+      // B' = a I + b A + c A A (the a X term of the apply step folded into
+      // B'). The old A is read in the accumulator layout: for each of a
+      // lane's rows, the 32 lanes of a half-wave read 32 consecutive columns.
       const T* aold = at(mm.off_a);
       const bool diag = task.tm == task.tn;
 #pragma unroll
@@ -1199,7 +1200,8 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
           for (int q = 0; q < 4; ++q) {
             const int r = wm + 32 * mi + 8 * q + 4 * lk, c = wn + 32 * ni + lr;
             float old[4];
-            load4(aold + int64_t(col0 + c) * s_pad + row0 + r, old);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) old[e] = float(aold[int64_t(row0 + r + e) * s_pad + col0 + c]);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               float v = fmaf(g.b, old[e], g.c * acc[mi][ni][4 * q + e]);
