@@ -55,8 +55,8 @@ struct DevicePlan {
   lm::SrBlock* d_sr_tab = nullptr;
   int32_t* d_rd_start = nullptr;
   int32_t* d_tensor_mat = nullptr;
-  lm::GemmTask* d_tasks[2][3] = {};   // [precision][gram, poly, apply]
-  lm::XcdSplit* d_splits = nullptr;   // [precision * 3 + stage]
+  lm::GemmTask* d_tasks[2][4] = {};   // [precision][gram, poly, apply, apply tail]
+  lm::XcdSplit* d_splits = nullptr;   // [precision * 4 + list]
 
   ~DevicePlan() {
     if (uploaded) (void)hipEventDestroy(uploaded);
@@ -146,15 +146,17 @@ lm_status get_plan(const TensorIn* x, int32_t n, lm::StepKind kind, lm::NsPrecis
   const size_t o_sr = off;         place(p.sr_tab, &off, &parts);
   const size_t o_rd = off;         place(p.rd_start, &off, &parts);
   const size_t o_tm = off;         place(p.tensor_mat, &off, &parts);
-  size_t o_tasks[2][3];
+  size_t o_tasks[2][4];
   std::vector<lm::XcdSplit> splits;
   for (int pr = 0; pr < 2; ++pr) {
     o_tasks[pr][0] = off; place(p.gram[pr], &off, &parts);
     o_tasks[pr][1] = off; place(p.poly[pr], &off, &parts);
     o_tasks[pr][2] = off; place(p.apply[pr], &off, &parts);
+    o_tasks[pr][3] = off; place(p.apply_tail[pr], &off, &parts);
     splits.push_back(p.gram_split[pr]);
     splits.push_back(p.poly_split[pr]);
     splits.push_back(p.apply_split[pr]);
+    splits.push_back(p.apply_tail_split[pr]);
   }
   const size_t o_splits = off;     place(splits, &off, &parts);
   const size_t total = std::max<size_t>(off, 256);
@@ -182,8 +184,8 @@ lm_status get_plan(const TensorIn* x, int32_t n, lm::StepKind kind, lm::NsPrecis
   dp->d_rd_start = reinterpret_cast<int32_t*>(base + o_rd);
   dp->d_tensor_mat = reinterpret_cast<int32_t*>(base + o_tm);
   for (int pr = 0; pr < 2; ++pr)
-    for (int st3 = 0; st3 < 3; ++st3)
-      dp->d_tasks[pr][st3] = reinterpret_cast<lm::GemmTask*>(base + o_tasks[pr][st3]);
+    for (int st4 = 0; st4 < 4; ++st4)
+      dp->d_tasks[pr][st4] = reinterpret_cast<lm::GemmTask*>(base + o_tasks[pr][st4]);
   dp->d_splits = reinterpret_cast<lm::XcdSplit*>(base + o_splits);
   g_plans.push_front(dp);
   while (g_plans.size() > kMaxPlans) g_plans.pop_back();   // hipFree waits for the device
@@ -382,12 +384,20 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
                                                                           : p.apply_split[pr]);
         if (sp.max_count == 0) continue;
         gl.tasks = dp.d_tasks[pr][st3];
-        gl.split = dp.d_splits + pr * 3 + st3;
+        gl.split = dp.d_splits + pr * 4 + st3;
         gl.max_count = sp.max_count;
         gl.fp32 = pr;
         gl.tile = p.tile[pr][st3];
         e = lm::launch_gemm(modes[st3], gl, stream);
         if (e != hipSuccess) return hip_fail(e, "Newton-Schulz kernel launch");
+        if (st3 == 2 && p.apply_tail_split[pr].max_count > 0) {   // the last round, as 128-tiles
+          gl.tasks = dp.d_tasks[pr][3];
+          gl.split = dp.d_splits + pr * 4 + 3;
+          gl.max_count = p.apply_tail_split[pr].max_count;
+          gl.tile = lm::kTileSmall;
+          e = lm::launch_gemm(modes[st3], gl, stream);
+          if (e != hipSuccess) return hip_fail(e, "Newton-Schulz kernel launch");
+        }
       }
       t.done();
     }
@@ -634,7 +644,8 @@ lm_status lionmuon_plan_info(const lm_shape* shapes, int32_t n, int64_t t, int32
   out->muon_elements = p.muon_elements;
   out->gram_tiles = int64_t(p.gram[0].size() + p.gram[1].size());
   out->poly_tiles = int64_t(p.poly[0].size() + p.poly[1].size());
-  out->apply_tiles = int64_t(p.apply[0].size() + p.apply[1].size());
+  out->apply_tiles = int64_t(p.apply[0].size() + p.apply[1].size() + p.apply_tail[0].size() +
+                             p.apply_tail[1].size());
   out->ns_flops = lm::ns_flops_symmetric(p, cfg->ns_steps);
   out->ns_flops_dense = lm::ns_flops_dense(p, cfg->ns_steps);
   out->lion_bytes = 20.0 * double(p.lion_elements) + 28.0 * double(p.adamw_elements);

@@ -16,6 +16,7 @@ constexpr int kMinBigTiles = 512;  // a bf16 Gram / polynomial stage uses 256-ti
 constexpr int kPrepTile = 64;    // square tile of the preparation / transpose pass
 constexpr int kLionBlockElems = 4096;  // elements per Lion workgroup (256 x float4 x 4)
 constexpr int kXcds = 8;         // accelerator complex dies of one MI355X
+constexpr int kComputeUnits = 256;  // CUs of one MI355X: workgroups of one full round
 // Stable-rank passes (adaptive step). Matrices with 16-byte rows and a short
 // side up to kSrMaxRegSide hold their block in registers (tall: blocks of
 // kSrTallRows rows; wide: strips of kSrWideCols columns, taken 32 columns at a

@@ -303,9 +303,27 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
         }
       }
     }
+    // a nearly empty last round of 256-tiles runs as 128-tiles instead
+    std::vector<int64_t> ct;
+    if (t_app == kTileBig) {
+      const size_t n = p->apply[pr].size(), rem = n % kComputeUnits;
+      if (n > rem && rem > 0 && 2 * rem <= size_t(kComputeUnits)) {
+        for (size_t i = n - rem; i < n; ++i) {
+          const GemmTask t = p->apply[pr][i];
+          for (int a = 0; a < 2; ++a)
+            for (int b = 0; b < 2; ++b) {
+              p->apply_tail[pr].push_back({t.mat, int16_t(2 * t.tm + a), int16_t(2 * t.tn + b)});
+              ct.push_back(ca[i]);
+            }
+        }
+        p->apply[pr].resize(n - rem);
+        ca.resize(n - rem);
+      }
+    }
     split_by_xcd(&p->gram[pr], cg, &p->gram_split[pr]);
     split_by_xcd(&p->poly[pr], cp, &p->poly_split[pr]);
     split_by_xcd(&p->apply[pr], ca, &p->apply_split[pr]);
+    split_by_xcd(&p->apply_tail[pr], ct, &p->apply_tail_split[pr]);
   }
 
   size_t off = align256(size_t(ns_off));

@@ -72,6 +72,11 @@ struct Plan {
   // grouped per XCD segment
   std::vector<GemmTask> gram[2], poly[2], apply[2];
   XcdSplit gram_split[2]{}, poly_split[2]{}, apply_split[2]{};
+  // bf16 apply tiles past the last full round of kComputeUnits 256-tiles,
+  // when they fill at most half a round, each split into four 128-tiles
+  // (a second launch after `apply`)
+  std::vector<GemmTask> apply_tail[2];
+  XcdSplit apply_tail_split[2]{};
   int32_t tile[2][3] = {{kTileBig, kTileBig, kTileBig}, {kTileSmall, kTileSmall, kTileSmall}};
   int64_t muon_elements = 0;
   int32_t n_shape_classes = 0;

@@ -148,10 +148,12 @@ def test_plan_info_tiles_span_ragged_shapes(lib):
     assert info["gram_tiles"] == 20 and info["poly_tiles"] == 20 and info["apply_tiles"] == 12
 
 
+# apply: 256-tiles; a last round of at most 128 of them (of 256 CUs) runs as
+# four 128-tiles each: 124M 1296 = 5 x 256 + 16, 720M 10800 = 42 x 256 + 48
 @pytest.mark.parametrize("name,sym_tiles,apply_tiles", [
-    ("gpt2-124m", 48 * 21, 12 * 27 + 12 * 9 + 24 * 36),   # 128-tiles for Gram/poly
-    ("gpt2-355m", 96 * 10, 24 * 48 + 24 * 16 + 48 * 64),  # 256-tiles everywhere
-    ("gpt2-720m", 144 * 15, 36 * 75 + 36 * 25 + 72 * 100)])
+    ("gpt2-124m", 48 * 21, 1280 + 4 * 16),                 # 128-tiles for Gram/poly
+    ("gpt2-355m", 96 * 10, 24 * 48 + 24 * 16 + 48 * 64),   # 4608 = 18 x 256: no tail
+    ("gpt2-720m", 144 * 15, 10752 + 4 * 48)])
 def test_plan_tile_choice_for_benchmark_sets(lib, name, sym_tiles, apply_tiles):
     info = lm.lionmuon_plan_info(_specs(workloads.get(name)), t=0, P=1)
     assert info["gram_tiles"] == sym_tiles and info["poly_tiles"] == sym_tiles

@@ -380,12 +380,18 @@ def test_profiling_counts_every_launch():
 # Full benchmark sets, sampled tensors, same launch as the benchmark
 # --------------------------------------------------------------------------
 def _sample_indices(wl):
+    """One tensor of every distinct shape, plus the last matrix of the list
+    (its last apply tiles are the ones a nearly empty final round of 256-tiles
+    hands to the 128-tile launch)."""
     seen, out = set(), []
     for i, t in enumerate(wl.tensors):
         key = (t.rows, t.cols, t.lion_only)
         if key not in seen:
             seen.add(key)
             out.append(i)
+    last = max(i for i, t in enumerate(wl.tensors) if not t.lion_only and t.rows > 1)
+    if last not in out:
+        out.append(last)
     return out
 
 
