@@ -1235,8 +1235,12 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
       // last step: W <- W - lr (kappa O + wd W), or O = kappa X_K (NS hook).
       // O is X_K, transposed back for tall matrices. The fp32 O tile goes
       // through LDS in two halves of W rows so that W is read and written in
-      // whole 16-byte pieces of its rows.
+      // whole 16-byte pieces of its rows. Each thread's W pieces of a half
+      // are requested before that half of O is staged, so their latency
+      // overlaps the staging instead of being paid once per piece.
       constexpr int kHalf = BT / 2, kFs = BT + 4;
+      constexpr int kIter = kHalf * (BT / 4) / kNT;   // 16-byte W pieces per thread per half
+      static_assert(kIter * kNT == kHalf * (BT / 4), "W pieces split evenly over the threads");
       float (*fst)[kFs] = reinterpret_cast<float (*)[kFs]>(smem);
       const bool tall = mm.transposed != 0;
       const int64_t wrow0 = tall ? col0 : row0, wcol0 = tall ? row0 : col0;
@@ -1244,6 +1248,18 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
       const float kappa = mm.kappa;
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
+        f32x4 wv[kIter];
+        if (!g.store_o) {
+#pragma unroll
+          for (int it = 0; it < kIter; ++it) {
+            const int idx = tid + it * kNT;
+            const int i = idx / (BT / 4), j = (idx % (BT / 4)) * 4;
+            const int64_t gr = wrow0 + h * kHalf + i, gc = wcol0 + j;
+            wv[it] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (mm.vec_ok && gr < wrows && gc + 3 < wcols)
+              wv[it] = *reinterpret_cast<const f32x4*>(mm.w + gr * wcols + gc);
+          }
+        }
 #pragma unroll
         for (int mi = 0; mi < kMI; ++mi)
 #pragma unroll
@@ -1264,7 +1280,9 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
               }
             }
         lds_barrier();
-        for (int idx = tid; idx < kHalf * (BT / 4); idx += kNT) {
+#pragma unroll
+        for (int it = 0; it < kIter; ++it) {
+          const int idx = tid + it * kNT;
           const int i = idx / (BT / 4), j = (idx % (BT / 4)) * 4;
           const int64_t gr = wrow0 + h * kHalf + i, gc = wcol0 + j;
           if (gr >= wrows || gc >= wcols) continue;
@@ -1272,13 +1290,12 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
           float o[4];
           load4(&fst[i][j], o);
           if (mm.vec_ok && gc + 3 < wcols) {
-            float w[4];
             if (g.store_o) {
               store4(wp, o);
             } else {
-              load4(wp, w);
+              float w[4];
 #pragma unroll
-              for (int e = 0; e < 4; ++e) w[e] = fmaf(-g.lr, fmaf(g.wd, w[e], o[e]), w[e]);
+              for (int e = 0; e < 4; ++e) w[e] = fmaf(-g.lr, fmaf(g.wd, wv[it][e], o[e]), wv[it][e]);
               store4(wp, w);
             }
           } else {
