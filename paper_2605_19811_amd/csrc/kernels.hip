@@ -1004,23 +1004,31 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   constexpr int kInstB = kBK / kRpiB / kWaves;
   static_assert(!kBRows || kInstB * kRpiB * kWaves == kBK, "B rows split evenly over the waves");
   auto swb = [](int k) { return (k & 3) * 4; };
+  // Copy addresses: a wave-uniform base (operand, K offset, instruction)
+  // plus one loop-invariant 32-bit byte offset per lane and operand. Because
+  // kWaves (and kWaves * kRpiB) is even (a multiple of 4), the swizzle of a
+  // lane's row does not depend on the instruction index.
+  static_assert(kWaves % 2 == 0 && (kWaves * kRpiB) % 4 == 0, "swizzle independent of the instruction");
+  const uint32_t a_off = uint32_t(((wave * 8 + (lane >> 3)) * lda + ((lane & 7) ^ swz(wave * 8 + (lane >> 3))) * kEpc) * sizeof(T));
+  const uint32_t b_off = kBRows
+      ? uint32_t(((wave * kRpiB + lane / kChunksB) * ldb + ((lane % kChunksB) ^ swb(wave * kRpiB + lane / kChunksB)) * kEpc) * sizeof(T))
+      : uint32_t(((wave * 8 + (lane >> 3)) * ldb + ((lane & 7) ^ swz(wave * 8 + (lane >> 3))) * kEpc) * sizeof(T));
+  auto gsrc = [](const T* base, uint32_t off) {
+    return reinterpret_cast<const void*>(reinterpret_cast<const char*>(base) + off);
+  };
   auto dma = [&](int buf, int k0) {
 #pragma unroll
     for (int q = 0; q < kInst; ++q) {
       const int blk = q * kWaves + wave;         // 8-row block
-      const int row = blk * 8 + (lane >> 3);
-      const int ch = (lane & 7) ^ swz(row);
-      __builtin_amdgcn_global_load_lds(Aop + row * lda + k0 + ch * kEpc, &sA[buf][blk * 8][0], 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(gsrc(Aop + int64_t(q * kWaves * 8) * lda + k0, a_off), &sA[buf][blk * 8][0], 16, 0, 0);
       if constexpr (!kBRows)
-        __builtin_amdgcn_global_load_lds(Bop + row * ldb + k0 + ch * kEpc, &sB[buf][blk * 8][0], 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(gsrc(Bop + int64_t(q * kWaves * 8) * ldb + k0, b_off), &sB[buf][blk * 8][0], 16, 0, 0);
     }
     if constexpr (kBRows) {
 #pragma unroll
       for (int q = 0; q < kInstB; ++q) {
         const int rr = (q * kWaves + wave) * kRpiB;  // first of the instruction's rows
-        const int k = rr + lane / kChunksB;
-        const int ch = (lane % kChunksB) ^ swb(k);
-        __builtin_amdgcn_global_load_lds(Bop + int64_t(k0 + k) * ldb + ch * kEpc, &sBr[buf][rr][0], 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(gsrc(Bop + int64_t(k0 + q * kWaves * kRpiB) * ldb, b_off), &sBr[buf][rr][0], 16, 0, 0);
       }
     }
   };
@@ -1100,7 +1108,8 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
       for (int i = 0; i < kMI; ++i)
 #pragma unroll
         for (int j = 0; j < kNI; ++j) acc[i][j] = M::mma(af[kk & 1][i], bfr[kk & 1][j], acc[i][j]);
-    }    // region order: the first fragment reads, then per k-step the MFMAs
+    }
+    // region order: the first fragment reads, then per k-step the MFMAs
     // interleaved with the next k-step's reads, then the last k-step's MFMAs
     constexpr int kReads = kMI + (kTrB ? 0 : kNI * (kBRows ? 2 : 1));
     __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
