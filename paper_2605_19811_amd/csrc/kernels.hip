@@ -31,6 +31,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 
 // sign with sign(+-0) = 0 and NaN propagated.
 __device__ __forceinline__ float sign_f(float x) {
@@ -832,6 +833,26 @@ __global__ __launch_bounds__(256) void srank_decide_kernel(SrankArgs a) {
 // Workgroup barrier that orders LDS accesses only: unlike __syncthreads it
 // does not wait for this wave's outstanding global stores, so output tiles
 // drain to memory while the workgroup goes on.
+// Wait until at most N vector-memory operations of this wave are outstanding
+// (they complete in the order they were issued).
+// (the builtin, not inline assembly: the compiler then knows which
+// operations have completed and adds no waits of its own for them)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // s_waitcnt fields: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in 15:14; expcnt
+  // (6:4) and lgkmcnt (11:8) at their maxima, i.e. not waited for
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Descriptor tables are read through the constant address space: they are
+// never written while a kernel runs, so the compiler may fetch them with
+// scalar loads even after the kernel's own stores.
+template <class U>
+__device__ __forceinline__ const __attribute__((address_space(4))) U* kconst(const U* p) {
+  return (const __attribute__((address_space(4))) U*)(p);
+}
+
 __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   __builtin_amdgcn_s_barrier();
@@ -926,7 +947,10 @@ struct GemmArgs {
   float a, b, c, lr, wd;
 };
 
-template <typename T, int MODE, int BT>
+// LAST (apply only): the last Newton-Schulz step, whose epilogue updates W
+// (its own instantiation: that epilogue's registers would otherwise weigh
+// on every other apply step).
+template <typename T, int MODE, int BT, bool LAST = false>
 __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   using M = Mfma<T>;
   using Geo = TileGeom<BT>;
@@ -950,40 +974,38 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   constexpr bool kBRows = MODE == kApply;
   T (*sBr)[kBK][BT] = reinterpret_cast<T (*)[kBK][BT]>(smem + 2 * BT * kLd);
 
-  const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
-  if (slot >= g.split->count[xcd]) return;
-  const GemmTask task = g.tasks[g.split->start[xcd] + slot];
-  if (g.decide && g.decide[task.mat] == 0) return;
-  const MuonMat& mm = g.mats[task.mat];
+  // The workgroups of an XCD walk that XCD's tile list with a stride of
+  // their number, skipping the tiles of matrices whose adaptive decision
+  // went the other way. Only the non-final apply is persistent (a grid of
+  // one round, several tiles per workgroup): its epilogue stores from
+  // registers, so the next tile's loads overlap them. The other products
+  // stage their results through the whole LDS and run one tile per
+  // workgroup, so a finished workgroup's successor starts at once.
+  constexpr bool kPersistent = MODE == kApply && !LAST;
+  const int xcd = blockIdx.x % kXcds;
+  const int count = kconst(g.split)->count[xcd];
+  const auto* tasks = kconst(g.tasks) + kconst(g.split)->start[xcd];
+  const int step = int(gridDim.x) / kXcds;
+  auto live = [&](int s) {
+    while (s < count && g.decide && kconst(g.decide)[tasks[s].mat] == 0) s += step;
+    return s;
+  };
   char* wsb = static_cast<char*>(g.ws);
   auto at = [&](int64_t off) { return reinterpret_cast<T*>(wsb + off); };
-  // ping-pong buffers chosen without indexing (keeps descriptors out of scratch)
-  const int64_t off_x_cur = g.src ? mm.off_x[1] : mm.off_x[0];
-  const int64_t off_x_nxt = g.src ? mm.off_x[0] : mm.off_x[1];
-  const T* Aop;
-  const T* Bop;
-  int64_t lda, ldb;
-  int K;
-  if (MODE == kGram) {
-    Aop = Bop = at(off_x_cur);
-    lda = ldb = mm.l_pad;
-    K = mm.l_pad;
-  } else if (MODE == kPoly) {
-    Aop = Bop = at(mm.off_a);
-    lda = ldb = mm.s_pad;
-    K = mm.s_pad;
-  } else {
-    Aop = at(mm.off_b);
-    Bop = at(off_x_cur);
-    lda = mm.s_pad;
-    ldb = mm.l_pad;
-    K = mm.s_pad;
-  }
-  const int row0 = task.tm * BT, col0 = task.tn * BT;
-  Aop += row0 * lda;
-  Bop += kBRows ? col0 : col0 * ldb;
+  // Non-final apply steps store X' straight from registers; the next tile's
+  // first stage is then requested before those stores, so it loads while
+  // they drain. kDirect is the number of those stores per lane.
+  constexpr int kDirect = Geo::kMI * Geo::kNI * 4;
+  bool prefetched = false;
+  for (int slot = live(blockIdx.x / kXcds); slot < count;) {
+  // Lane-derived values are recomputed for every tile (the empty asm keeps
+  // the compiler from hoisting them out of the tile loop, where they would
+  // stay live, in registers, through the epilogue).
+  int tid = threadIdx.x;
+  if constexpr (kPersistent) asm volatile("" : "+v"(tid));
+  __builtin_assume(tid >= 0 && tid < kNT);
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
   const int wm = (wave / Geo::kWavesN) * Geo::kWM, wn = (wave % Geo::kWavesN) * Geo::kWN;
 
@@ -1004,34 +1026,73 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   constexpr int kInstB = kBK / kRpiB / kWaves;
   static_assert(!kBRows || kInstB * kRpiB * kWaves == kBK, "B rows split evenly over the waves");
   auto swb = [](int k) { return (k & 3) * 4; };
-  // Copy addresses: a wave-uniform base (operand, K offset, instruction)
-  // plus one loop-invariant 32-bit byte offset per lane and operand. Because
-  // kWaves (and kWaves * kRpiB) is even (a multiple of 4), the swizzle of a
-  // lane's row does not depend on the instruction index.
+  // Operands of one tile. Copy addresses are a wave-uniform base (operand,
+  // K offset, instruction) plus one loop-invariant 32-bit byte offset per
+  // lane and operand. Because kWaves (and kWaves * kRpiB) is even (a
+  // multiple of 4), the swizzle of a lane's row does not depend on the
+  // instruction index.
   static_assert(kWaves % 2 == 0 && (kWaves * kRpiB) % 4 == 0, "swizzle independent of the instruction");
-  const uint32_t a_off = uint32_t(((wave * 8 + (lane >> 3)) * lda + ((lane & 7) ^ swz(wave * 8 + (lane >> 3))) * kEpc) * sizeof(T));
-  const uint32_t b_off = kBRows
-      ? uint32_t(((wave * kRpiB + lane / kChunksB) * ldb + ((lane % kChunksB) ^ swb(wave * kRpiB + lane / kChunksB)) * kEpc) * sizeof(T))
-      : uint32_t(((wave * 8 + (lane >> 3)) * ldb + ((lane & 7) ^ swz(wave * 8 + (lane >> 3))) * kEpc) * sizeof(T));
+  struct Ops {
+    const T* a;
+    const T* b;
+    int64_t lda, ldb;
+    int K;
+    uint32_t a_off, b_off;
+  };
+  auto make_ops = [&](const __attribute__((address_space(4))) GemmTask& t) {
+    const auto& m = kconst(g.mats)[t.mat];
+    // ping-pong buffers chosen without indexing (keeps descriptors out of scratch)
+    const int64_t xcur = g.src ? m.off_x[1] : m.off_x[0];
+    Ops o;
+    if (MODE == kGram) {
+      o.a = o.b = at(xcur);
+      o.lda = o.ldb = m.l_pad;
+      o.K = int(m.l_pad);
+    } else if (MODE == kPoly) {
+      o.a = o.b = at(m.off_a);
+      o.lda = o.ldb = m.s_pad;
+      o.K = int(m.s_pad);
+    } else {
+      o.a = at(m.off_b);
+      o.b = at(xcur);
+      o.lda = m.s_pad;
+      o.ldb = m.l_pad;
+      o.K = int(m.s_pad);
+    }
+    o.a += int64_t(t.tm) * BT * o.lda;
+    o.b += kBRows ? int64_t(t.tn) * BT : int64_t(t.tn) * BT * o.ldb;
+    o.a_off = uint32_t(((wave * 8 + (lane >> 3)) * o.lda + ((lane & 7) ^ swz(wave * 8 + (lane >> 3))) * kEpc) * sizeof(T));
+    o.b_off = kBRows
+        ? uint32_t(((wave * kRpiB + lane / kChunksB) * o.ldb + ((lane % kChunksB) ^ swb(wave * kRpiB + lane / kChunksB)) * kEpc) * sizeof(T))
+        : uint32_t(((wave * 8 + (lane >> 3)) * o.ldb + ((lane & 7) ^ swz(wave * 8 + (lane >> 3))) * kEpc) * sizeof(T));
+    return o;
+  };
   auto gsrc = [](const T* base, uint32_t off) {
     return reinterpret_cast<const void*>(reinterpret_cast<const char*>(base) + off);
   };
-  auto dma = [&](int buf, int k0) {
+  auto dma = [&](const Ops& o, int buf, int k0) {
 #pragma unroll
     for (int q = 0; q < kInst; ++q) {
       const int blk = q * kWaves + wave;         // 8-row block
-      __builtin_amdgcn_global_load_lds(gsrc(Aop + int64_t(q * kWaves * 8) * lda + k0, a_off), &sA[buf][blk * 8][0], 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(gsrc(o.a + int64_t(q * kWaves * 8) * o.lda + k0, o.a_off), &sA[buf][blk * 8][0], 16, 0, 0);
       if constexpr (!kBRows)
-        __builtin_amdgcn_global_load_lds(gsrc(Bop + int64_t(q * kWaves * 8) * ldb + k0, b_off), &sB[buf][blk * 8][0], 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(gsrc(o.b + int64_t(q * kWaves * 8) * o.ldb + k0, o.b_off), &sB[buf][blk * 8][0], 16, 0, 0);
     }
     if constexpr (kBRows) {
 #pragma unroll
       for (int q = 0; q < kInstB; ++q) {
         const int rr = (q * kWaves + wave) * kRpiB;  // first of the instruction's rows
-        __builtin_amdgcn_global_load_lds(gsrc(Bop + int64_t(k0 + q * kWaves * kRpiB) * ldb, b_off), &sBr[buf][rr][0], 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(gsrc(o.b + int64_t(k0 + q * kWaves * kRpiB) * o.ldb, o.b_off), &sBr[buf][rr][0], 16, 0, 0);
       }
     }
   };
+  static_assert(kDirect + 2 * kInst + kInstB < 64, "outstanding vector memory operations fit the counter");
+  const auto& task = tasks[slot];
+  const auto& mm = kconst(g.mats)[task.mat];
+  const int64_t off_x_nxt = g.src ? mm.off_x[0] : mm.off_x[1];
+  const Ops ops = make_ops(task);
+  const int K = ops.K;
+  const int row0 = task.tm * BT, col0 = task.tn * BT;
 
   f32x16 acc[kMI][kNI];
 #pragma unroll
@@ -1079,11 +1140,82 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // serialising loads and MFMAs.
   constexpr bool kTrB = kBRows && sizeof(T) == 2;
   typename M::Frag bq[kTrB ? kSub : 1][kNI];
+  // The 16 transpose reads of a stage are one assembly block that ends by
+  // waiting for them: the compiler's own form of the read counts as touching
+  // memory it cannot see and would first wait for every outstanding global
+  // access, including the previous tile's stores still draining. Read
+  // (kk, j, t) is at the lane's address for column block j plus
+  // (16 kk + 4 t) rows of BT elements.
   auto preload_b = [&](int buf) {
+    if constexpr (kTrB) {
+      static_assert(kSub == 4 && kNI == 2 && (BT == 256 || BT == 128), "transpose-read block layout");
+      uint32_t base[2];
 #pragma unroll
-    for (int kk = 0; kk < kSub; ++kk)
+      for (int j = 0; j < 2; ++j) {
+        const int grp = lane >> 4, m = lane & 15;
+        const int n = wn + 32 * j + 16 * (grp & 1) + 4 * (m & 3);
+        const int k = 8 * (grp >> 1) + (m >> 2);
+        const int off = (((n >> 3) ^ swb(k)) << 3) + (n & 7);
+        // (a C cast: it converts the generic pointer to the LDS address space)
+        base[j] = uint32_t(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) T*)(&sBr[buf][k][off])));
+      }
+      u32x2 h[16];
+      if constexpr (BT == 256) {
+        asm volatile(
+            "ds_read_b64_tr_b16 %0, %16\n"
+            "ds_read_b64_tr_b16 %1, %16 offset:2048\n"
+            "ds_read_b64_tr_b16 %2, %17\n"
+            "ds_read_b64_tr_b16 %3, %17 offset:2048\n"
+            "ds_read_b64_tr_b16 %4, %16 offset:8192\n"
+            "ds_read_b64_tr_b16 %5, %16 offset:10240\n"
+            "ds_read_b64_tr_b16 %6, %17 offset:8192\n"
+            "ds_read_b64_tr_b16 %7, %17 offset:10240\n"
+            "ds_read_b64_tr_b16 %8, %16 offset:16384\n"
+            "ds_read_b64_tr_b16 %9, %16 offset:18432\n"
+            "ds_read_b64_tr_b16 %10, %17 offset:16384\n"
+            "ds_read_b64_tr_b16 %11, %17 offset:18432\n"
+            "ds_read_b64_tr_b16 %12, %16 offset:24576\n"
+            "ds_read_b64_tr_b16 %13, %16 offset:26624\n"
+            "ds_read_b64_tr_b16 %14, %17 offset:24576\n"
+            "ds_read_b64_tr_b16 %15, %17 offset:26624\n"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(h[0]), "=&v"(h[1]), "=&v"(h[2]), "=&v"(h[3]), "=&v"(h[4]), "=&v"(h[5]), "=&v"(h[6]), "=&v"(h[7]),
+              "=&v"(h[8]), "=&v"(h[9]), "=&v"(h[10]), "=&v"(h[11]), "=&v"(h[12]), "=&v"(h[13]), "=&v"(h[14]), "=&v"(h[15])
+            : "v"(base[0]), "v"(base[1])
+            : "memory");
+      } else {
+        asm volatile(
+            "ds_read_b64_tr_b16 %0, %16\n"
+            "ds_read_b64_tr_b16 %1, %16 offset:1024\n"
+            "ds_read_b64_tr_b16 %2, %17\n"
+            "ds_read_b64_tr_b16 %3, %17 offset:1024\n"
+            "ds_read_b64_tr_b16 %4, %16 offset:4096\n"
+            "ds_read_b64_tr_b16 %5, %16 offset:5120\n"
+            "ds_read_b64_tr_b16 %6, %17 offset:4096\n"
+            "ds_read_b64_tr_b16 %7, %17 offset:5120\n"
+            "ds_read_b64_tr_b16 %8, %16 offset:8192\n"
+            "ds_read_b64_tr_b16 %9, %16 offset:9216\n"
+            "ds_read_b64_tr_b16 %10, %17 offset:8192\n"
+            "ds_read_b64_tr_b16 %11, %17 offset:9216\n"
+            "ds_read_b64_tr_b16 %12, %16 offset:12288\n"
+            "ds_read_b64_tr_b16 %13, %16 offset:13312\n"
+            "ds_read_b64_tr_b16 %14, %17 offset:12288\n"
+            "ds_read_b64_tr_b16 %15, %17 offset:13312\n"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(h[0]), "=&v"(h[1]), "=&v"(h[2]), "=&v"(h[3]), "=&v"(h[4]), "=&v"(h[5]), "=&v"(h[6]), "=&v"(h[7]),
+              "=&v"(h[8]), "=&v"(h[9]), "=&v"(h[10]), "=&v"(h[11]), "=&v"(h[12]), "=&v"(h[13]), "=&v"(h[14]), "=&v"(h[15])
+            : "v"(base[0]), "v"(base[1])
+            : "memory");
+      }
 #pragma unroll
-      for (int j = 0; j < kNI; ++j) bq[kTrB ? kk : 0][j] = frag_b_rows(buf, j, kk * M::kKStep);
+      for (int kk = 0; kk < kSub; ++kk)
+#pragma unroll
+        for (int j = 0; j < kNI; ++j) {
+          const bf16x4 lo = __builtin_bit_cast(bf16x4, h[(kk * 2 + j) * 2]);
+          const bf16x4 hi = __builtin_bit_cast(bf16x4, h[(kk * 2 + j) * 2 + 1]);
+          bq[kk][j] = typename M::Frag{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        }
+    }
   };
   auto compute = [&](int buf) {
     // fragments double-buffered in registers: the LDS reads of substep kk+1
@@ -1120,21 +1252,29 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // The barrier after each stage both publishes the stage just loaded (every
   // wave has waited for its own loads) and frees the buffer just read.
   const int nk = K / kBK;
-  dma(0, 0);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
+  if (prefetched) {
+    wait_vmcnt<kDirect>();                       // this tile's first stage; stores may still drain
+  } else {
+    dma(ops, 0, 0);
+    wait_vmcnt<0>();
+  }
+  prefetched = false;
+  lds_barrier();
   for (int kt = 0; kt < nk; ++kt) {
     if constexpr (kTrB) {
       preload_b(kt & 1);
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (kt + 1 < nk) dma((kt + 1) & 1, (kt + 1) * kBK);
+    if (kt + 1 < nk) dma(ops, (kt + 1) & 1, (kt + 1) * kBK);
     __builtin_amdgcn_sched_barrier(0);
     compute(kt & 1);
     __builtin_amdgcn_sched_barrier(0);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
+    wait_vmcnt<0>();
+    lds_barrier();
   }
+  // (the barrier after the last stage means no wave reads the operand
+  // buffers any more)
+  const int nslot = live(slot + step);
 
   // ---- epilogues ----------------------------------------------------------
   // Results leave through LDS: each lane writes its values into the staging
@@ -1187,12 +1327,11 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
           store4(&stage_t[c][r], v);
         }
   };
-  lds_barrier();                                 // operand stages no longer read
 
   if (MODE == kGram || MODE == kPoly) {
     float alpha = 1.0f;
     if (MODE == kGram && g.first) {
-      const float r = g.rscale[task.mat];
+      const float r = kconst(g.rscale)[task.mat];
       alpha = r * r;
     }
     if (MODE == kPoly) {
@@ -1229,17 +1368,35 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
     }
   } else {
     // X' = alpha B' X with B' = a I + b A + c A A from the polynomial step
-    const float alpha = g.first ? g.rscale[task.mat] : 1.0f;
+    const float alpha = g.first ? kconst(g.rscale)[task.mat] : 1.0f;
 #pragma unroll
     for (int mi = 0; mi < kMI; ++mi)
 #pragma unroll
       for (int ni = 0; ni < kNI; ++ni)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[mi][ni][r] *= alpha;
-    if (!g.last) {
-      auto val = [&](int mi, int ni, int q, int e) { return acc[mi][ni][4 * q + e]; };
-      stage_rows(val);
-      flush(at(off_x_nxt) + row0 * l_pad + col0, l_pad, &stage[0][0], kStR);
+    if constexpr (!LAST) {
+      if (nslot < count) {
+        dma(make_ops(tasks[nslot]), 0, 0);
+        prefetched = true;
+      }
+      // each quad of lanes transposes its 4 x 4 blocks (DPP) so that every
+      // lane stores 4 consecutive columns of one row
+      T* out = at(off_x_nxt) + row0 * l_pad + col0;
+      const int b = lane & 3;
+#pragma unroll
+      for (int mi = 0; mi < kMI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < kNI; ++ni)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = acc[mi][ni][4 * q + e];
+            quad_transpose(v, b);
+            const int r = wm + 32 * mi + 8 * q + 4 * lk + b, c = wn + 32 * ni + (lr & ~3);
+            store4(out + r * l_pad + c, v);
+          }
     } else {
       // last step: W <- W - lr (kappa O + wd W), or O = kappa X_K (NS hook).
       // O is X_K, transposed back for tall matrices. The fp32 O tile goes
@@ -1324,6 +1481,9 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
       }
     }
   }
+  if constexpr (!kPersistent) break;            // one tile per workgroup (full grid)
+  slot = nslot;
+  }
 }
 
 // One entry point per Newton-Schulz product, so profiles name each stage.
@@ -1338,6 +1498,10 @@ __global__ __launch_bounds__(TileGeom<BT>::kThreads) void ns_poly_kernel(GemmArg
 template <typename T, int BT>
 __global__ __launch_bounds__(TileGeom<BT>::kThreads) void ns_apply_kernel(GemmArgs g) {
   gemm_body<T, kApply, BT>(g);
+}
+template <typename T, int BT>
+__global__ __launch_bounds__(TileGeom<BT>::kThreads) void ns_apply_last_kernel(GemmArgs g) {
+  gemm_body<T, kApply, BT, true>(g);
 }
 
 }  // namespace
@@ -1415,14 +1579,20 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
   a.lr = l.lr;
   a.wd = l.wd;
   a.decide = l.decide;
-  const dim3 grid(unsigned(l.max_count) * kXcds);
+  // persistent: at most as many workgroups per XCD as its CUs hold at once
+  // (one 256-tile or two 128-tiles per CU, limited by LDS)
+  // (only the non-final apply is persistent; the others keep one workgroup
+  // per tile)
+  const int per_xcd = (mode != kApply || l.last) ? l.max_count : (kComputeUnits / kXcds) * (l.tile == 256 ? 1 : 2);
+  const dim3 grid(unsigned(l.max_count < per_xcd ? l.max_count : per_xcd) * kXcds);
 #define LM_LAUNCH(KERNEL, T, BT) \
   hipLaunchKernelGGL((KERNEL<T, BT>), grid, dim3(TileGeom<BT>::kThreads), 0, stream, a)
 #define LM_LAUNCH_MODE(T, BT)                                   \
   do {                                                          \
     if (mode == kGram) LM_LAUNCH(ns_gram_kernel, T, BT);        \
     else if (mode == kPoly) LM_LAUNCH(ns_poly_kernel, T, BT);   \
-    else LM_LAUNCH(ns_apply_kernel, T, BT);                     \
+    else if (!l.last) LM_LAUNCH(ns_apply_kernel, T, BT);        \
+    else LM_LAUNCH(ns_apply_last_kernel, T, BT);                \
   } while (0)
   if (l.fp32) {
     if (l.tile != 128) return hipErrorInvalidValue;
