@@ -52,7 +52,7 @@ def load_traffic(workload, kernel):
 
 PHASE_OF_KERNEL = (("lion_kernel", "lion"), ("prep_kernel", "prep"), ("norm_kernel", "norm"),
                    ("ns_gram_kernel", "gram"), ("ns_poly_kernel", "poly"),
-                   ("ns_apply_kernel", "apply"), ("srank_", "srank"))
+                   ("ns_apply_", "apply"), ("srank_", "srank"))   # apply: ns_apply_kernel, ns_apply_last_kernel
 
 
 def phase_of(kernel_name):
@@ -94,26 +94,30 @@ def pmc_summary(wl_name, fetch_csv, write_csv, calib_fetch_csv, calib_write_csv,
     # all of its dispatches / the decide dispatches (one per step)
     steps = [len(v) for k, v in fetch.items() if "srank_decide" in k]
     srank = {"fetch_bytes": 0.0, "write_bytes": 0.0}
+    # a Newton-Schulz phase launch is one main-list launch plus, for the
+    # apply, an optional launch of its last round as 128-tiles (and the last
+    # apply is its own kernel): bytes per launch = all of the phase's
+    # dispatches / its 256-tile dispatches (all dispatches where there are none)
+    tot = {}
     for name in set(fetch) | set(write):
         ph = phase_of(name)
         if ph is None:
             continue
-        if ph == "srank":
-            srank["fetch_bytes"] += sum(fetch.get(name, [])) * 1024.0 * f_scale / steps[0]
-            srank["write_bytes"] += sum(write.get(name, [])) * 1024.0 * w_scale / steps[0]
-            continue
         fv, wv = fetch.get(name, []), write.get(name, [])
-        fb = sum(fv) / len(fv) * 1024.0 * f_scale if fv else 0.0
-        wb = sum(wv) / len(wv) * 1024.0 * w_scale if wv else 0.0
-        k = kernels.setdefault(ph, {"fetch_bytes": 0.0, "write_bytes": 0.0, "launch_kinds": 0})
-        k["fetch_bytes"] += fb
-        k["write_bytes"] += wb
-        k["launch_kinds"] += 1
-    for k in kernels.values():
-        k["fetch_bytes"] /= k["launch_kinds"]
-        k["write_bytes"] /= k["launch_kinds"]
-        k["bytes_per_launch"] = k["fetch_bytes"] + k["write_bytes"]
-        del k["launch_kinds"]
+        if ph == "srank":
+            srank["fetch_bytes"] += sum(fv) * 1024.0 * f_scale / steps[0]
+            srank["write_bytes"] += sum(wv) * 1024.0 * w_scale / steps[0]
+            continue
+        t = tot.setdefault(ph, {"fetch": 0.0, "write": 0.0, "n_all": 0, "n_256": 0})
+        t["fetch"] += sum(fv) * 1024.0 * f_scale
+        t["write"] += sum(wv) * 1024.0 * w_scale
+        t["n_all"] += len(fv)
+        if "Li256" in name:
+            t["n_256"] += len(fv)
+    for ph, t in tot.items():
+        n = t["n_256"] or t["n_all"]
+        kernels[ph] = {"fetch_bytes": t["fetch"] / n, "write_bytes": t["write"] / n,
+                       "bytes_per_launch": (t["fetch"] + t["write"]) / n}
     if steps:
         srank["bytes_per_launch"] = srank["fetch_bytes"] + srank["write_bytes"]
         kernels["srank"] = srank
@@ -170,6 +174,26 @@ def trace_summary(wl_name, stats_csv, command):
         short = name if len(name) < 70 else name[:67] + "..."
         lines.append(f"| `{short}` | {ph} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
                      f"{float(r['TotalDurationNs']) / 1e3:.1f} | {float(r['Percentage']):.2f} |")
+    # per phase launch, as bench.py times a phase (main list plus the apply's
+    # 128-tile tail and last-step kernels; the stable-rank phase per step)
+    tot = {}
+    for r in rows:
+        ph = phase_of(r["Name"])
+        if ph is None:
+            continue
+        t = tot.setdefault(ph, {"ns": 0.0, "n_all": 0, "n_256": 0, "n_decide": 0})
+        t["ns"] += float(r["TotalDurationNs"])
+        t["n_all"] += int(r["Calls"])
+        if "Li256" in r["Name"]:
+            t["n_256"] += int(r["Calls"])
+        if "srank_decide" in r["Name"]:
+            t["n_decide"] += int(r["Calls"])
+    lines += ["", "Per phase launch (all of a phase's kernels; launches = its 256-tile dispatches "
+              "where there are any, the decide dispatches for srank):", "",
+              "| phase | launches | avg us per launch |", "|---|---|---|"]
+    for ph, t in sorted(tot.items(), key=lambda kv: -kv[1]["ns"]):
+        n = t["n_decide"] if ph == "srank" else (t["n_256"] or t["n_all"])
+        lines.append(f"| {ph} | {n} | {t['ns'] / n / 1e3:.1f} |")
     path = os.path.join(TRAFFIC_DIR, f"kernel_trace_{wl_name}.md")
     with open(path, "w") as f:
         f.write("\n".join(lines) + "\n")
@@ -436,7 +460,7 @@ def main():
         d = ph[dom]
         kernel_names = {"lion": "lion_kernel", "prep": "prep_kernel", "norm": "norm_kernel",
                         "gram": "ns_gram_kernel<bf16>", "poly": "ns_poly_kernel<bf16>",
-                        "apply": "ns_apply_kernel<bf16>", "srank": "srank_pass+reduce+decide"}
+                        "apply": "ns_apply_kernel<bf16> (+ ns_apply_last_kernel)", "srank": "srank_pass+reduce+decide"}
         if "tflops" in d:
             roof = {"kernel": kernel_names[dom], "bound": "mfma", "achieved": d["tflops"],
                     "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": d["frac_bf16_peak"]}
