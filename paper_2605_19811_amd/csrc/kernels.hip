@@ -193,20 +193,80 @@ __device__ __forceinline__ void load4(const float* p, float v[4]) {
   v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3];
 }
 
+// Wide matrix (X = Ghat, same layout): a strip of kPrepElems elements, TC
+// columns wide, so that each wave reads and writes whole TC-element pieces
+// of rows (1 KB of fp32 for TC = 256).
+template <typename T, int TC>
+__device__ __forceinline__ void prep_wide(const PrepArgs& a, const MuonMat& mm, int b) {
+  constexpr int kChunks = TC / 4, kRowsPass = 256 / kChunks, kRows = kPrepElems / TC;
+  static_assert(kRows == 4 * kRowsPass, "four passes per strip");
+  __shared__ float red[4];
+  const int local = b - mm.prep_first;
+  const int ti = local / mm.prep_tiles_n, tj = local - ti * mm.prep_tiles_n;
+  T* X = reinterpret_cast<T*>(static_cast<char*>(a.ws) + mm.off_x[0]);
+  const int64_t cols_pad = mm.l_pad;
+  const int tid = threadIdx.x, r0 = tid / kChunks, c4 = (tid % kChunks) * 4;
+  float ss = 0.0f;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int64_t p = int64_t(ti) * kRows + r0 + kRowsPass * u;
+    const int64_t q = int64_t(tj) * TC + c4;
+    float gv[4] = {0.f, 0.f, 0.f, 0.f}, mv[4] = {0.f, 0.f, 0.f, 0.f};
+    const bool row_in = p < mm.rows;
+    const bool vec = row_in && mm.vec_ok && q + 3 < mm.cols;
+    const int64_t idx = p * mm.cols + q;
+    if (vec) {
+      const f32x4 g = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(mm.g + idx));
+      gv[0] = g[0]; gv[1] = g[1]; gv[2] = g[2]; gv[3] = g[3];
+      if (mm.m) {
+        const f32x4 m = *reinterpret_cast<const f32x4*>(mm.m + idx);
+        mv[0] = m[0]; mv[1] = m[1]; mv[2] = m[2]; mv[3] = m[3];
+      }
+    } else if (row_in) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (q + e < mm.cols) {
+          gv[e] = mm.g[idx + e];
+          if (mm.m) mv[e] = mm.m[idx + e];
+        }
+      }
+    }
+    float c[4], mn[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      c[e] = fmaf(a.b1, mv[e], a.omb1 * gv[e]);
+      mn[e] = fmaf(a.b2, mv[e], a.omb2 * gv[e]);
+      ss = fmaf(c[e], c[e], ss);
+    }
+    if (mm.m) {
+      if (vec) {
+        const f32x4 mv4 = {mn[0], mn[1], mn[2], mn[3]};
+        *reinterpret_cast<f32x4*>(mm.m + idx) = mv4;
+      } else if (row_in) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (q + e < mm.cols) mm.m[idx + e] = mn[e];
+      }
+    }
+    store4(X + p * cols_pad + q, c);
+  }
+  ss = wave_sum(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  if (tid == 0) a.partials[mm.prep_first + local] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// Tall matrix: a 64 x 64 tile of Ghat, stored transposed (X = Ghat^T)
+// through LDS.
 template <typename T>
-__device__ __forceinline__ void prep_tile(const PrepArgs& a, const MuonMat& mm, int b) {
+__device__ __forceinline__ void prep_tall(const PrepArgs& a, const MuonMat& mm, int b) {
   constexpr int kPad = 4 / sizeof(T) + 1;        // odd word stride per LDS row
   __shared__ T tile[kPrepTile][kPrepTile + kPad];
   __shared__ float red[4];
   const int local = b - mm.prep_first;
   const int ti = local / mm.prep_tiles_n, tj = local - ti * mm.prep_tiles_n;
-  const int64_t rows_pad = mm.transposed ? mm.l_pad : mm.s_pad;
-  const int64_t cols_pad = mm.transposed ? mm.s_pad : mm.l_pad;
-  char* ws = static_cast<char*>(a.ws);
-  // X (s_pad x l_pad): Ghat itself for a wide matrix, Ghat^T (through an LDS
-  // transpose) for a tall one
-  T* X = reinterpret_cast<T*>(ws + mm.off_x[0]);
-  const bool tall = mm.transposed != 0;
+  const int64_t rows_pad = mm.l_pad;           // of the original (tall) matrix
+  T* X = reinterpret_cast<T*>(static_cast<char*>(a.ws) + mm.off_x[0]);
   const int tid = threadIdx.x, r0 = tid >> 4, c4 = (tid & 15) * 4;
   float ss = 0.0f;
 #pragma unroll
@@ -251,14 +311,10 @@ __device__ __forceinline__ void prep_tile(const PrepArgs& a, const MuonMat& mm, 
           if (q + e < mm.cols) mm.m[idx + e] = mn[e];
       }
     }
-    if (!tall) {
-      store4(X + p * cols_pad + q, c);
-    } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) tile[r][c4 + e] = to_elem<T>(c[e]);
-    }
+    for (int e = 0; e < 4; ++e) tile[r][c4 + e] = to_elem<T>(c[e]);
   }
-  if (tall) {                            // uniform over the workgroup
+  {
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -280,10 +336,16 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
   const int mi = find_segment(a.prep_start, a.n_mats, b);
   if (a.decide && a.decide[mi] == 0) return;          // the candidate took Lion
   const MuonMat& mm = a.mats[mi];
-  if (mm.fp32)
-    prep_tile<float>(a, mm, b);
-  else
-    prep_tile<bf16>(a, mm, b);
+  if (mm.transposed) {
+    if (mm.fp32) prep_tall<float>(a, mm, b);
+    else prep_tall<bf16>(a, mm, b);
+  } else if (mm.l_pad == mm.prep_tiles_n * 256) {
+    if (mm.fp32) prep_wide<float, 256>(a, mm, b);
+    else prep_wide<bf16, 256>(a, mm, b);
+  } else {
+    if (mm.fp32) prep_wide<float, 128>(a, mm, b);
+    else prep_wide<bf16, 128>(a, mm, b);
+  }
 }
 
 __global__ __launch_bounds__(256) void norm_kernel(PrepArgs a) {
