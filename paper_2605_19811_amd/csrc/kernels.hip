@@ -1171,35 +1171,16 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   };
   // B fragment of block column j from k-major rows: the MFMA wants, in lane
   // (n = lane % 32, half lk), B[kc + lk kKStep/2 + t][n] for t < kKStep/2.
+  // fp32 apply: B fragment of block column j from the k-major rows (one
+  // element per lane: B[kc + lk][n]); the bf16 apply reads its fragments
+  // with transpose reads (preload_b below)
   auto frag_b_rows = [&](int buf, int j, int kc) -> typename M::Frag {
-    if constexpr (sizeof(T) == 2) {
-      // Two transpose reads of 4 k each. Within each 16-lane group, lane m
-      // points at row kb + (m >> 2), columns n0 + 4 (m & 3) .. +3, and
-      // receives column n0 + m of rows kb .. kb + 3.
-      const int grp = lane >> 4, m = lane & 15;
-      const int n = wn + 32 * j + 16 * (grp & 1) + 4 * (m & 3);
-      const int kb = kc + 8 * (grp >> 1) + (m >> 2);
-      bf16x4 h[2];
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int k = kb + 4 * t;
-        const int off = (((n >> 3) ^ swb(k)) << 3) + (n & 7);
-        // (a C cast: it converts the generic pointer to the LDS address space)
-        h[t] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (__attribute__((address_space(3))) bf16x4*)(&sBr[buf][k][off]));
-      }
-      return typename M::Frag{h[0][0], h[0][1], h[0][2], h[0][3], h[1][0], h[1][1], h[1][2], h[1][3]};
-    } else {
-      const int k = kc + lk, n = wn + 32 * j + lr;
-      return sBr[buf][k][(((n >> 2) ^ swb(k)) << 2) + (n & 3)];
-    }
+    const int k = kc + lk, n = wn + 32 * j + lr;
+    return sBr[buf][k][(((n >> 2) ^ swb(k)) << 2) + (n & 3)];
   };
   constexpr int kSub = kBK / M::kKStep;
-  // bf16 apply: the transpose-read B fragments of a whole stage are read
-  // into registers before the next stage's loads are issued. The compiler
-  // cannot tell those reads from the in-flight global->LDS copies and would
-  // otherwise wait for the copies to land before each transpose read,
-  // serialising loads and MFMAs.
+  // bf16 apply: the B fragments of a whole stage are read into registers
+  // (transpose reads) before the next stage's copies are issued.
   constexpr bool kTrB = kBRows && sizeof(T) == 2;
   typename M::Frag bq[kTrB ? kSub : 1][kNI];
   // The 16 transpose reads of a stage are one assembly block that ends by
@@ -1207,7 +1188,11 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // memory it cannot see and would first wait for every outstanding global
   // access, including the previous tile's stores still draining. Read
   // (kk, j, t) is at the lane's address for column block j plus
-  // (16 kk + 4 t) rows of BT elements.
+  // (16 kk + 4 t) rows of BT elements. The MFMA wants, in lane (n =
+  // lane % 32, half lk), B[kc + 8 lk + t][n] for t < 8: two transpose reads
+  // of 4 k each. Within each 16-lane group, lane m points at row
+  // kb + (m >> 2), columns n0 + 4 (m & 3) .. +3, and receives column n0 + m
+  // of rows kb .. kb + 3.
   auto preload_b = [&](int buf) {
     if constexpr (kTrB) {
       static_assert(kSub == 4 && kNI == 2 && (BT == 256 || BT == 128), "transpose-read block layout");
