@@ -282,3 +282,35 @@ def test_adaptive_every_pass_variant(k):
                        if min(s) >= 64 else "fp32")
         else:
             check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 1e-3, 0.1)
+
+
+def test_adaptive_gated_tiles_every_tensor_checked():
+    """Muon and Lion candidates alternate over a set large enough that each
+    persistent Newton-Schulz workgroup walks several tiles, with the tiles of
+    Lion-branch matrices skipped between live ones, and the apply's last
+    round split into 128-tiles. Every tensor's update is checked: a live tile
+    left out or a skipped tile processed shows in its matrix."""
+    shapes = [(768, 1536) if i % 4 < 2 else (1536, 768) for i in range(32)]
+    rng = np.random.default_rng(97)
+    M0 = [low_rank_momentum([98, i], s, 2, 1e-3) if i % 2 == 0 else
+          (rng.standard_normal(s) * 1e-2).astype(np.float32) for i, s in enumerate(shapes)]
+    W0 = [(rng.standard_normal(s) * 0.02).astype(np.float32) for s in shapes]
+    G = [(rng.standard_normal(s) * 1e-2).astype(np.float32) for s in shapes]
+    W, M = [dev(x) for x in W0], [dev(x) for x in M0]
+    n = len(shapes)
+    dec = torch.zeros(n, dtype=torch.int32, device=DEV)
+    sr = torch.zeros(n, dtype=torch.float64, device=DEV)
+    alpha, k = 0.05, 5
+    cfg = lm.config(lr_muon=0.02, lr_lion=1e-3, adaptive_alpha=alpha, adaptive_power_steps=k)
+    print(f"gated tiles: {n} tensors", flush=True)
+    lm.lionmuon_step_adaptive(W, [dev(g) for g in G], M, 4, 0.9, 0.99, 0.1, cfg, decisions=dec,
+                              stable_rank=sr)
+    torch.cuda.synchronize()
+    dec, sr = dec.cpu().numpy(), sr.cpu().numpy()
+    check_decisions(M0, set(range(n)), dec, sr, alpha, k)
+    assert dec[0::2].all() and not dec[1::2].any(), dec
+    for i in range(n):
+        if dec[i]:
+            check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 0.02, 0.1, "bf16")
+        else:
+            check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 1e-3, 0.1)
