@@ -300,10 +300,16 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
     sl.alpha = cfg.adaptive_alpha;
     Timer t(stream, LM_PHASE_SRANK);
     const int steps = cfg.adaptive_power_steps;
+    // Every pass reads all candidate momenta; odd passes walk them in
+    // reverse (classes and blocks), so a pass starts with the data the
+    // previous one read last, which the last-level cache still holds.
+    const size_t nc = p.sr_classes.size();
     for (int i = 0; i <= steps && e == hipSuccess; ++i) {
-      for (const Plan::SrClass& c : p.sr_classes) {
+      const bool rev = (i & 1) != 0;
+      for (size_t j = 0; j < nc; ++j) {
+        const Plan::SrClass& c = p.sr_classes[rev ? nc - 1 - j : j];
         e = lm::launch_srank_pass(sl, c.kind, c.bucket, c.first, c.count, i == 0, i == steps,
-                                  stream);
+                                  rev, stream);
         if (e != hipSuccess) break;
       }
       if (e == hipSuccess && i < steps) e = lm::launch_srank_reduce(sl, stream);

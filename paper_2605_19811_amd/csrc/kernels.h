@@ -85,9 +85,11 @@ struct SrankLaunch {
 // first_block + n_blocks) of one class (kind, bucket): z' = S^T S (z / ||z||)
 // as per-block partials (the first pass starts from the all-ones vector and
 // writes the sums of M^2); `last` passes only sum ||S z / ||z|| ||^2.
+// `reverse` walks the blocks from the last to the first (same results: each
+// block writes its own partials).
 hipError_t launch_srank_pass(const SrankLaunch& a, int32_t kind, int32_t bucket,
                              int32_t first_block, int32_t n_blocks, bool first, bool last,
-                             hipStream_t stream);
+                             bool reverse, hipStream_t stream);
 // Fixed-order sum of the partials into z' and the chunk sums of z'^2.
 hipError_t launch_srank_reduce(const SrankLaunch& a, hipStream_t stream);
 // r_hat = ||M||_F^2 / sigma_hat^2 and the decision r_hat <= alpha * min(m, n).

@@ -394,6 +394,8 @@ struct SrankArgs {
   int32_t* decisions_out;
   double* srank_out;
   double alpha;
+  int32_t reverse;   // pass blocks in reverse order (alternate passes: the
+                     // blocks read last are still in the last-level cache)
 };
 
 struct SrBufs {
@@ -472,7 +474,7 @@ __global__ __launch_bounds__(256) void srank_tall_kernel(SrankArgs a, int32_t fi
   constexpr int kGroups = kSrTallRows / (4 * kRg);
   __shared__ double vs[kSrMaxRegSide];
   __shared__ double red[4][256];
-  const SrBlock sb = a.tab[first_block + blockIdx.x];
+  const SrBlock sb = a.tab[first_block + (a.reverse ? int(gridDim.x) - 1 - int(blockIdx.x) : int(blockIdx.x))];
   const MuonMat& mm = a.mats[sb.mat];
   const SrBufs B = sr_bufs(a.ws, mm);
   sr_load_v<256>(vs, mm, B, first != 0);
@@ -567,7 +569,7 @@ __global__ __launch_bounds__(1024) void srank_wide_kernel(SrankArgs a, int32_t f
   __shared__ double ured[kNw][SW];
   __shared__ double us[SW];
   __shared__ double red[2 * kNw];
-  const SrBlock sb = a.tab[first_block + blockIdx.x];
+  const SrBlock sb = a.tab[first_block + (a.reverse ? int(gridDim.x) - 1 - int(blockIdx.x) : int(blockIdx.x))];
   const MuonMat& mm = a.mats[sb.mat];
   const SrBufs B = sr_bufs(a.ws, mm);
   sr_load_v<1024>(vs, mm, B, first != 0);
@@ -802,7 +804,7 @@ __device__ void srank_generic_wide(double (*red)[256], const MuonMat& mm, const 
 template <bool FIRST, bool LAST>
 __global__ __launch_bounds__(256) void srank_generic_kernel(SrankArgs a, int32_t first_block) {
   __shared__ double red[4][256];
-  const SrBlock sb = a.tab[first_block + blockIdx.x];
+  const SrBlock sb = a.tab[first_block + (a.reverse ? int(gridDim.x) - 1 - int(blockIdx.x) : int(blockIdx.x))];
   const MuonMat& mm = a.mats[sb.mat];
   const SrBufs B = sr_bufs(a.ws, mm);
   const double inv = sr_inv_norm(mm, B, FIRST);
@@ -1667,14 +1669,16 @@ static SrankArgs srank_args(const SrankLaunch& l) {
   a.decisions_out = l.decisions_out;
   a.srank_out = l.srank_out;
   a.alpha = l.alpha;
+  a.reverse = 0;
   return a;
 }
 
 hipError_t launch_srank_pass(const SrankLaunch& l, int32_t kind, int32_t bucket,
                              int32_t first_block, int32_t n_blocks, bool first, bool last,
-                             hipStream_t stream) {
+                             bool reverse, hipStream_t stream) {
   if (n_blocks == 0) return hipSuccess;
-  const SrankArgs a = srank_args(l);
+  SrankArgs a = srank_args(l);
+  a.reverse = reverse ? 1 : 0;
   const dim3 grid(static_cast<unsigned>(n_blocks));
   const int32_t f = first ? 1 : 0, z = last ? 1 : 0;
   if (kind == kSrTall) {
