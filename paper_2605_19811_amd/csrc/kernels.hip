@@ -882,7 +882,8 @@ __global__ __launch_bounds__(256) void srank_decide_kernel(SrankArgs a) {
 // Newton-Schulz GEMMs
 // ---------------------------------------------------------------------------
 // C[BT x BT] = sum_k Aop[row0 + i][k] * Bop[col0 + j][k]: both operands are
-// K-contiguous ("NT"). K is staged through LDS 128 bytes per row at a time by
+// K-contiguous ("NT"), except the apply's X, which is staged k-major and read
+// with transpose reads. K is staged through LDS 128 bytes per row at a time by
 // direct global->LDS loads (no register staging), double buffered: the loads
 // of stage k+1 are in flight while stage k feeds the MFMAs. Rows are
 // unpadded; their eight 16-byte chunks are XOR-swizzled by row so that the
@@ -894,9 +895,6 @@ __global__ __launch_bounds__(256) void srank_decide_kernel(SrankArgs a) {
 //             stages with too few 256-tiles to fill the chip.
 // Accumulator element r of block (mi, ni) sits at row
 // wm + 32 mi + 8 (r / 4) + 4 (lane / 32) + r % 4, col wn + 32 ni + lane % 32.
-// Workgroup barrier that orders LDS accesses only: unlike __syncthreads it
-// does not wait for this wave's outstanding global stores, so output tiles
-// drain to memory while the workgroup goes on.
 // Wait until at most N vector-memory operations of this wave are outstanding
 // (they complete in the order they were issued).
 // (the builtin, not inline assembly: the compiler then knows which
@@ -917,6 +915,9 @@ __device__ __forceinline__ const __attribute__((address_space(4))) U* kconst(con
   return (const __attribute__((address_space(4))) U*)(p);
 }
 
+// Workgroup barrier that orders LDS accesses only: unlike __syncthreads it
+// does not wait for this wave's outstanding global stores, so output tiles
+// drain to memory while the workgroup goes on.
 __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   __builtin_amdgcn_s_barrier();
@@ -1326,9 +1327,11 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   const int nslot = live(slot + step);
 
   // ---- epilogues ----------------------------------------------------------
-  // Results leave through LDS: each lane writes its values into the staging
-  // tile (row-major, or transposed with 8-byte writes), then the workgroup
-  // stores whole rows with coalesced 16-byte stores.
+  // The Gram and polynomial results leave through LDS: each lane writes its
+  // values into the staging tile (row-major, or transposed with 8-byte
+  // writes), then the workgroup stores whole rows with coalesced 16-byte
+  // stores. The non-final apply stores from registers; the last one stages
+  // its fp32 direction through LDS to update W.
   const int64_t s_pad = mm.s_pad, l_pad = mm.l_pad;
   T (*stage)[kStR] = reinterpret_cast<T (*)[kStR]>(smem);
   T (*stage_t)[kStC] = reinterpret_cast<T (*)[kStC]>(smem);
