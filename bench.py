@@ -32,8 +32,15 @@ TRAFFIC_DIR = os.path.join(ROOT, "profiles")
 
 
 def kernel_hash():
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the kernel source with comments and blank lines removed, so a
+    comment-only edit keeps the counters taken with the same code valid."""
+    import re
+    with open(KERNEL_SOURCE) as f:
+        src = f.read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    lines = [re.sub(r"//.*$", "", ln).rstrip() for ln in src.splitlines()]
+    code = "\n".join(ln for ln in lines if ln.strip())
+    return hashlib.sha256(code.encode()).hexdigest()[:16]
 
 
 def load_traffic(workload, kernel):
