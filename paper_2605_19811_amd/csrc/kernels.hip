@@ -193,6 +193,9 @@ __device__ __forceinline__ void load4(const float* p, float v[4]) {
   v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3];
 }
 
+// LDS block of the transpose tile (bf16 64 x 131 or fp32 64 x 66 elements)
+constexpr int kPrepLdsBytes = 64 * 66 * 4;
+
 // Wide matrix (X = Ghat, same layout): a strip of kPrepElems elements, TC
 // columns wide, so that each wave reads and writes whole TC-element pieces
 // of rows (1 KB of fp32 for TC = 256).
@@ -256,24 +259,30 @@ __device__ __forceinline__ void prep_wide(const PrepArgs& a, const MuonMat& mm, 
   if (tid == 0) a.partials[mm.prep_first + local] = (red[0] + red[1]) + (red[2] + red[3]);
 }
 
-// Tall matrix: a 64 x 64 tile of Ghat, stored transposed (X = Ghat^T)
-// through LDS.
-template <typename T>
-__device__ __forceinline__ void prep_tall(const PrepArgs& a, const MuonMat& mm, int b) {
+// Tall matrix: a kPrepTile x TC tile of Ghat (rows read as 4 TC-byte
+// pieces), stored transposed (X = Ghat^T) through LDS as 64-element pieces of
+// TC rows of X. TC = kPrepTallCols (bf16 X) or kPrepTile (fp32 X), so both
+// tiles fit the same LDS block.
+template <typename T, int TC>
+__device__ __forceinline__ void prep_tall(const PrepArgs& a, const MuonMat& mm, int b,
+                                          char* lds) {
+  constexpr int kTR = kPrepTile, kTC = TC;
   constexpr int kPad = 4 / sizeof(T) + 1;        // odd word stride per LDS row
-  __shared__ T tile[kPrepTile][kPrepTile + kPad];
+  constexpr int kChunks = kTC / 4, kRowsPass = 256 / kChunks, kPasses = kTR / kRowsPass;
+  static_assert(kTR * (kTC + kPad) * sizeof(T) <= kPrepLdsBytes, "tile fits the LDS block");
+  T (*tile)[kTC + kPad] = reinterpret_cast<T (*)[kTC + kPad]>(lds);
   __shared__ float red[4];
   const int local = b - mm.prep_first;
   const int ti = local / mm.prep_tiles_n, tj = local - ti * mm.prep_tiles_n;
   const int64_t rows_pad = mm.l_pad;           // of the original (tall) matrix
   T* X = reinterpret_cast<T*>(static_cast<char*>(a.ws) + mm.off_x[0]);
-  const int tid = threadIdx.x, r0 = tid >> 4, c4 = (tid & 15) * 4;
+  const int tid = threadIdx.x, r0 = tid / kChunks, c4 = (tid % kChunks) * 4;
   float ss = 0.0f;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int r = r0 + 16 * u;
-    const int64_t p = int64_t(ti) * kPrepTile + r;
-    const int64_t q = int64_t(tj) * kPrepTile + c4;
+  for (int u = 0; u < kPasses; ++u) {
+    const int r = r0 + kRowsPass * u;
+    const int64_t p = int64_t(ti) * kTR + r;
+    const int64_t q = int64_t(tj) * kTC + c4;
     float gv[4] = {0.f, 0.f, 0.f, 0.f}, mv[4] = {0.f, 0.f, 0.f, 0.f};
     const bool row_in = p < mm.rows;
     const bool vec = row_in && mm.vec_ok && q + 3 < mm.cols;
@@ -314,16 +323,17 @@ __device__ __forceinline__ void prep_tall(const PrepArgs& a, const MuonMat& mm, 
 #pragma unroll
     for (int e = 0; e < 4; ++e) tile[r][c4 + e] = to_elem<T>(c[e]);
   }
-  {
-    __syncthreads();
+  __syncthreads();
+  // X^T rows: kTC of them, kTR elements each, 4 per thread
+  constexpr int kLpr = kTR / 4, kXRowsPass = 256 / kLpr;
+  const int xr0 = tid / kLpr, xc4 = (tid % kLpr) * 4;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int qq = r0 + 16 * u;        // column of the source tile
-      float v[4];
+  for (int u = 0; u < kTC / kXRowsPass; ++u) {
+    const int qq = xr0 + kXRowsPass * u;          // column of the source tile
+    float v[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = float(tile[c4 + e][qq]);
-      store4(X + (int64_t(tj) * kPrepTile + qq) * rows_pad + int64_t(ti) * kPrepTile + c4, v);
-    }
+    for (int e = 0; e < 4; ++e) v[e] = float(tile[xc4 + e][qq]);
+    store4(X + (int64_t(tj) * kTC + qq) * rows_pad + int64_t(ti) * kTR + xc4, v);
   }
   ss = wave_sum(ss);
   if ((tid & 63) == 0) red[tid >> 6] = ss;
@@ -332,13 +342,14 @@ __device__ __forceinline__ void prep_tall(const PrepArgs& a, const MuonMat& mm, 
 }
 
 __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
+  __shared__ __attribute__((aligned(16))) char lds[kPrepLdsBytes];
   const int b = blockIdx.x;
   const int mi = find_segment(a.prep_start, a.n_mats, b);
   if (a.decide && a.decide[mi] == 0) return;          // the candidate took Lion
   const MuonMat& mm = a.mats[mi];
   if (mm.transposed) {
-    if (mm.fp32) prep_tall<float>(a, mm, b);
-    else prep_tall<bf16>(a, mm, b);
+    if (mm.fp32) prep_tall<float, kPrepTile>(a, mm, b, lds);
+    else prep_tall<bf16, kPrepTallCols>(a, mm, b, lds);
   } else if (mm.l_pad == mm.prep_tiles_n * 256) {
     if (mm.fp32) prep_wide<float, 256>(a, mm, b);
     else prep_wide<bf16, 256>(a, mm, b);

@@ -13,7 +13,8 @@ constexpr int kTileSmall = 128;  // MFMA output tile edges; fp32 buffers are pad
 constexpr int kTileBig = 256;    // to 128, bf16 buffers to 256
 constexpr int kMinBigTiles = 512;  // a bf16 Gram / polynomial stage uses 256-tiles
                                    // only with at least this many (two per CU)
-constexpr int kPrepTile = 64;    // square tile of the preparation / transpose pass (tall)
+constexpr int kPrepTile = 64;    // rows of a tall matrix's preparation / transpose tile
+constexpr int kPrepTallCols = 128;  // its columns with bf16 X (64 with fp32 X)
 constexpr int kPrepElems = 4096; // elements of every preparation tile (wide: 16 x 256 or 32 x 128)
 constexpr int kLionBlockElems = 4096;  // elements per Lion workgroup (256 x float4 x 4)
 constexpr int kXcds = 8;         // accelerator complex dies of one MI355X

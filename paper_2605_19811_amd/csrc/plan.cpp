@@ -227,10 +227,11 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
     mm.off_b = ns_off;     ns_off += ss;
     const int64_t rows_pad = mm.transposed ? mm.l_pad : mm.s_pad;
     const int64_t cols_pad = mm.transposed ? mm.s_pad : mm.l_pad;
-    // preparation tiles: 64 x 64 through the LDS transpose for a tall
-    // matrix; kPrepElems-element strips of whole 1 KB (or 512 B) row pieces
-    // for a wide one
-    const int64_t tile_c = mm.transposed ? kPrepTile : (cols_pad % 256 == 0 ? 256 : 128);
+    // preparation tiles: 64 x 128 (64 x 64 for fp32 X) through the LDS
+    // transpose for a tall matrix; kPrepElems-element strips of whole 1 KB
+    // (or 512 B) row pieces for a wide one
+    const int64_t tile_c = mm.transposed ? (mm.fp32 ? kPrepTile : kPrepTallCols)
+                                         : (cols_pad % 256 == 0 ? 256 : 128);
     const int64_t tile_r = mm.transposed ? kPrepTile : kPrepElems / tile_c;
     mm.prep_tiles_n = int32_t(cols_pad / tile_c);
     mm.prep_count = int32_t((rows_pad / tile_r) * (cols_pad / tile_c));
