@@ -202,7 +202,8 @@ constexpr int kPrepLdsBytes = 64 * 66 * 4;
 template <typename T, int TC>
 __device__ __forceinline__ void prep_wide(const PrepArgs& a, const MuonMat& mm, int b) {
   constexpr int kChunks = TC / 4, kRowsPass = 256 / kChunks, kRows = kPrepElems / TC;
-  static_assert(kRows == 4 * kRowsPass, "four passes per strip");
+  constexpr int kPasses = kRows / kRowsPass;
+  static_assert(kPasses * kRowsPass == kRows, "whole passes per strip");
   __shared__ float red[4];
   const int local = b - mm.prep_first;
   const int ti = local / mm.prep_tiles_n, tj = local - ti * mm.prep_tiles_n;
@@ -211,7 +212,7 @@ __device__ __forceinline__ void prep_wide(const PrepArgs& a, const MuonMat& mm, 
   const int tid = threadIdx.x, r0 = tid / kChunks, c4 = (tid % kChunks) * 4;
   float ss = 0.0f;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
+  for (int u = 0; u < kPasses; ++u) {
     const int64_t p = int64_t(ti) * kRows + r0 + kRowsPass * u;
     const int64_t q = int64_t(tj) * TC + c4;
     float gv[4] = {0.f, 0.f, 0.f, 0.f}, mv[4] = {0.f, 0.f, 0.f, 0.f};
