@@ -92,7 +92,10 @@ hipError_t get_event(hipEvent_t* e) {
     g_event_pool.pop_back();
     return hipSuccess;
   }
-  return hipEventCreate(e);
+  // device-scope only: a system-scope release on every phase boundary costs
+  // several microseconds per event, and the timestamps are read back only
+  // after the stream has been synchronised
+  return hipEventCreateWithFlags(e, hipEventDisableSystemFence);
 }
 
 void append_key(std::vector<uint8_t>* k, const void* p, size_t n) {
