@@ -437,3 +437,30 @@ def test_full_set_sampled(name):
     del params, moms, grads, tl
     lm.lionmuon_release()
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", ["gpt2-124m", "gpt2-355m"])
+def test_full_set_every_matrix(name):
+    """The set's Muon step in the benchmark's launch configuration, with every
+    matrix compared with the oracle (at 124M the persistent apply walks five
+    tiles per workgroup and the last round goes to the 128-tile launch; at
+    355M eighteen)."""
+    wl = workloads.get(name)
+    params, moms, grads = workloads.device_state(torch, wl, DEV, seed=8, warm=True, n_grad=1)
+    grads = grads[0]
+    before = [(p.cpu().numpy(), m.cpu().numpy(), g.cpu().numpy())
+              for p, m, g in zip(params, moms, grads)]
+    cfg = lm.config(ns_precision="bf16", lr_muon=wl.lr_muon, lr_lion=wl.lr_lion)
+    tl = lm.TensorList(params, grads, moms, [t.lion_only for t in wl.tensors])
+    print(f"{name}: Muon step, every matrix checked", flush=True)
+    lm.lionmuon_step_ex(None, None, None, 2, wl.P, wl.beta1, wl.beta2, wl.wd, cfg, tensors=tl)
+    sync()
+    errs = []
+    for i, (W0, M0, G) in enumerate(before):
+        errs.append(check_muon(W0, G, M0, params[i].cpu().numpy(), moms[i].cpu().numpy(),
+                               wl.beta1, wl.beta2, wl.lr_muon, wl.wd, "bf16"))
+    print(f"{name}: max Muon direction error {max(errs):.2e} over {len(errs)} matrices",
+          flush=True)
+    del params, moms, grads, tl
+    lm.lionmuon_release()
+    torch.cuda.empty_cache()
