@@ -32,20 +32,26 @@ import workloads  # noqa: E402
 HBM_PEAK_GBPS = 8000.0            # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2516.6         # dense MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
 FP32_MFMA_PEAK_TFLOPS = 157.3
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2605_19811_amd", "csrc", "kernels.hip")
+# the kernels and the planner that sets their tiles and grids: traffic per
+# launch depends on both
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2605_19811_amd", "csrc", f)
+                  for f in ("kernels.hip", "plan.cpp")]
 TRAFFIC_DIR = os.path.join(ROOT, "profiles")
 
 
 def kernel_hash():
-    """Hash of the kernel source with comments and blank lines removed, so a
-    comment-only edit keeps the counters taken with the same code valid."""
+    """Hash of the kernel and planner sources with comments and blank lines
+    removed, so a comment-only edit keeps the counters taken with the same
+    code valid."""
     import re
-    with open(KERNEL_SOURCE) as f:
-        src = f.read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    lines = [re.sub(r"//.*$", "", ln).rstrip() for ln in src.splitlines()]
-    code = "\n".join(ln for ln in lines if ln.strip())
-    return hashlib.sha256(code.encode()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path) as f:
+            src = f.read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        lines = [re.sub(r"//.*$", "", ln).rstrip() for ln in src.splitlines()]
+        h.update("\n".join(ln for ln in lines if ln.strip()).encode())
+    return h.hexdigest()[:16]
 
 
 def load_traffic(workload, kernel):

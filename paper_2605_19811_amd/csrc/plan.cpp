@@ -16,6 +16,73 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 bool finite_nonneg(double v) { return std::isfinite(v) && v >= 0.0; }
 
+// Lower-triangle output tiles of one matrix's s x s product, each with its
+// inner dimension as cost.
+void sym_tiles(const MuonMat& mm, int32_t mi, int tile, int64_t inner,
+               std::vector<GemmTask>* tasks, std::vector<int64_t>* cost) {
+  const int ts = int(mm.s_pad / tile);
+  for (int tm = 0; tm < ts; ++tm) {
+    for (int tn = 0; tn <= tm; ++tn) {
+      tasks->push_back({mi, int16_t(tm), int16_t(tn)});
+      cost->push_back(inner);
+    }
+  }
+}
+
+// Estimated duration of a one-tile-per-workgroup symmetric product launch,
+// in quarters of a 256-tile K stage: each XCD's tiles, longest first, go to
+// whichever of its workgroup slots frees first (as the dispatcher hands out
+// a full grid), one slot per CU for 256-tiles and two for 128-tiles (LDS).
+// Per tile: a K stage of a 256-tile takes 4 units; two 128-tiles sharing a
+// CU take 3 units each per stage (a quarter of the work at two thirds of the
+// 256-tile rate, measured on the benchmark sets); set-up and epilogue cost
+// 7 and 5 units.
+int64_t sym_launch_estimate(const std::vector<GemmTask>& tasks, const std::vector<int64_t>& inner,
+                            const XcdSplit& split, int tile) {
+  const bool big = tile == kTileBig;
+  const int slots = kComputeUnits / kXcds * (big ? 1 : 2);
+  const int64_t per_stage = big ? 4 : 3, fixed = big ? 7 : 5;
+  const int64_t kbk = 64;
+  int64_t worst = 0;
+  std::vector<int64_t> free_at(size_t(slots), 0);
+  for (int x = 0; x < kXcds; ++x) {
+    std::fill(free_at.begin(), free_at.end(), 0);
+    for (int32_t i = split.start[x]; i < split.start[x] + split.count[x]; ++i) {
+      auto it = std::min_element(free_at.begin(), free_at.end());
+      *it += fixed + per_stage * ((inner[size_t(i)] + kbk - 1) / kbk);
+    }
+    worst = std::max(worst, *std::max_element(free_at.begin(), free_at.end()));
+  }
+  return worst;
+}
+
+// Tile edge for a bf16 symmetric product (Gram if `gram`, else the
+// polynomial): 256 unless 128-tiles are estimated to finish sooner (too few
+// 256-tiles to fill the chip, or too uneven a last round).
+int32_t pick_sym_tile(const std::vector<MuonMat>& mats, bool gram) {
+  int64_t est[2] = {0, 0};
+  const int32_t sizes[2] = {kTileBig, kTileSmall};
+  for (int k = 0; k < 2; ++k) {
+    std::vector<GemmTask> tasks;
+    std::vector<int64_t> cost;
+    for (int32_t mi = 0; mi < int32_t(mats.size()); ++mi) {
+      const MuonMat& mm = mats[size_t(mi)];
+      if (mm.fp32) continue;
+      sym_tiles(mm, mi, sizes[k], gram ? mm.l_pad : mm.s_pad, &tasks, &cost);
+    }
+    if (tasks.empty()) return kTileBig;
+    XcdSplit split;
+    split_by_xcd(&tasks, cost, &split);
+    std::vector<int64_t> inner(tasks.size());
+    for (size_t i = 0; i < tasks.size(); ++i) {
+      const MuonMat& mm = mats[size_t(tasks[i].mat)];
+      inner[i] = gram ? mm.l_pad : mm.s_pad;
+    }
+    est[k] = sym_launch_estimate(tasks, inner, split, sizes[k]);
+  }
+  return est[0] <= est[1] ? kTileBig : kTileSmall;
+}
+
 }  // namespace
 
 int sr_tall_bucket(int64_t s) {
@@ -276,31 +343,21 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
   // GEMM work lists in canonical order (matrix, then tiles), cost = inner
   // dimension, one list per Newton-Schulz precision.
   // bf16: apply on 256-tiles; Gram and polynomial (s x s outputs, lower
-  // triangle) on 256-tiles only when there are enough of them. fp32: 128.
-  int64_t big_sym = 0;
-  for (const MuonMat& mm : p->mats) {
-    if (mm.fp32) continue;
-    const int64_t ts = mm.s_pad / kTileBig;
-    big_sym += ts * (ts + 1) / 2;
+  // triangle) each on whichever of 256- and 128-tiles the launch estimate
+  // below favours. fp32: 128.
+  if (p->mats.size() > 0) {
+    p->tile[0][0] = pick_sym_tile(p->mats, true);
+    p->tile[0][1] = pick_sym_tile(p->mats, false);
   }
-  const int32_t sym_tile = big_sym >= kMinBigTiles ? kTileBig : kTileSmall;
-  p->tile[0][0] = p->tile[0][1] = sym_tile;
   p->tile[0][2] = kTileBig;
   for (int pr = 0; pr < 2; ++pr) {
     std::vector<int64_t> cg, cp, ca;
-    const int t_sym = p->tile[pr][0], t_app = p->tile[pr][2];
+    const int t_app = p->tile[pr][2];
     for (int32_t mi = 0; mi < int32_t(p->mats.size()); ++mi) {
       const MuonMat& mm = p->mats[mi];
       if (mm.fp32 != pr) continue;
-      const int ts = mm.s_pad / t_sym;
-      for (int tm = 0; tm < ts; ++tm) {
-        for (int tn = 0; tn <= tm; ++tn) {      // symmetric: lower triangle
-          p->gram[pr].push_back({mi, int16_t(tm), int16_t(tn)});
-          cg.push_back(mm.l_pad);
-          p->poly[pr].push_back({mi, int16_t(tm), int16_t(tn)});
-          cp.push_back(mm.s_pad);
-        }
-      }
+      sym_tiles(mm, mi, p->tile[pr][0], mm.l_pad, &p->gram[pr], &cg);
+      sym_tiles(mm, mi, p->tile[pr][1], mm.s_pad, &p->poly[pr], &cp);
       const int ts_a = mm.s_pad / t_app, tl_a = mm.l_pad / t_app;
       for (int tn = 0; tn < tl_a; ++tn) {
         for (int tm = 0; tm < ts_a; ++tm) {
