@@ -904,7 +904,9 @@ __global__ __launch_bounds__(256) void srank_decide_kernel(SrankArgs a) {
 //   BT = 256: 8 waves (2 x 4), each a 128 x 64 sub-tile of 4 x 2 MFMA 32x32
 //             blocks (32 B of operand loads per CU-clock at full MFMA rate);
 //   BT = 128: 4 waves (2 x 2), each a 64 x 64 sub-tile of 2 x 2 blocks, for
-//             stages with too few 256-tiles to fill the chip.
+//             stages with too few 256-tiles to fill the chip;
+//   BT = 64:  4 waves (2 x 2), each one 32 x 32 block (fp32 products with
+//             too few 128-tiles to fill the chip).
 // Accumulator element r of block (mi, ni) sits at row
 // wm + 32 mi + 8 (r / 4) + 4 (lane / 32) + r % 4, col wn + 32 ni + lane % 32.
 // Wait until at most N vector-memory operations of this wave are outstanding
@@ -1006,8 +1008,8 @@ template <> struct Mfma<float> {
 };
 
 template <int BT> struct TileGeom {
-  static constexpr int kWM = BT == 256 ? 128 : 64;   // wave sub-tile rows
-  static constexpr int kWN = 64;                      // wave sub-tile cols
+  static constexpr int kWM = BT == 256 ? 128 : BT / 2;   // wave sub-tile rows
+  static constexpr int kWN = BT == 64 ? 32 : 64;          // wave sub-tile cols
   static constexpr int kWavesN = BT / kWN;
   static constexpr int kThreads = (BT / kWM) * kWavesN * 64;
   static constexpr int kMI = kWM / 32, kNI = kWN / 32;
@@ -1644,10 +1646,11 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
   a.wd = l.wd;
   a.decide = l.decide;
   // persistent: at most as many workgroups per XCD as its CUs hold at once
-  // (one 256-tile or two 128-tiles per CU, limited by LDS)
+  // (one 256-tile, two 128-tiles or four 64-tiles per CU, limited by LDS)
   // (only the non-final apply is persistent; the others keep one workgroup
   // per tile)
-  const int per_xcd = (mode != kApply || l.last) ? l.max_count : (kComputeUnits / kXcds) * (l.tile == 256 ? 1 : 2);
+  const int per_cu = l.tile == 256 ? 1 : (l.tile == 128 ? 2 : 4);
+  const int per_xcd = (mode != kApply || l.last) ? l.max_count : (kComputeUnits / kXcds) * per_cu;
   const dim3 grid(unsigned(l.max_count < per_xcd ? l.max_count : per_xcd) * kXcds);
 #define LM_LAUNCH(KERNEL, T, BT) \
   hipLaunchKernelGGL((KERNEL<T, BT>), grid, dim3(TileGeom<BT>::kThreads), 0, stream, a)
@@ -1659,8 +1662,9 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
     else LM_LAUNCH(ns_apply_last_kernel, T, BT);                \
   } while (0)
   if (l.fp32) {
-    if (l.tile != 128) return hipErrorInvalidValue;
-    LM_LAUNCH_MODE(float, 128);
+    if (l.tile == 64) LM_LAUNCH_MODE(float, 64);
+    else if (l.tile == 128) LM_LAUNCH_MODE(float, 128);
+    else return hipErrorInvalidValue;
   } else if (l.tile == 256) {
     LM_LAUNCH_MODE(bf16, 256);
   } else {

@@ -11,6 +11,7 @@ namespace lm {
 // Tile sizes of the Newton-Schulz GEMMs and of the Muon preparation pass.
 constexpr int kTileSmall = 128;  // MFMA output tile edges; fp32 buffers are padded
 constexpr int kTileBig = 256;    // to 128, bf16 buffers to 256
+constexpr int kTileTiny = 64;    // fp32 products with too few 128-tiles to fill the chip
                                    // only with at least this many (two per CU)
 constexpr int kPrepTile = 64;    // rows of a tall matrix's preparation / transpose tile
 constexpr int kPrepTallCols = 128;  // its columns with bf16 X (64 with fp32 X)

@@ -344,12 +344,24 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
   // dimension, one list per Newton-Schulz precision.
   // bf16: apply on 256-tiles; Gram and polynomial (s x s outputs, lower
   // triangle) each on whichever of 256- and 128-tiles the launch estimate
-  // below favours. fp32: 128.
+  // below favours. fp32: 128-tiles, or 64-tiles for a product whose
+  // 128-tiles would not give every CU one.
   if (p->mats.size() > 0) {
     p->tile[0][0] = pick_sym_tile(p->mats, true);
     p->tile[0][1] = pick_sym_tile(p->mats, false);
   }
   p->tile[0][2] = kTileBig;
+  {
+    int64_t sym = 0, app = 0;
+    for (const MuonMat& mm : p->mats) {
+      if (!mm.fp32) continue;
+      const int64_t ts = mm.s_pad / kTileSmall;
+      sym += ts * (ts + 1) / 2;
+      app += ts * (mm.l_pad / kTileSmall);
+    }
+    p->tile[1][0] = p->tile[1][1] = sym < kComputeUnits ? kTileTiny : kTileSmall;
+    p->tile[1][2] = app < kComputeUnits ? kTileTiny : kTileSmall;
+  }
   for (int pr = 0; pr < 2; ++pr) {
     std::vector<int64_t> cg, cp, ca;
     const int t_app = p->tile[pr][2];

@@ -132,16 +132,20 @@ def test_plan_info_vectors_and_lion_only_never_muon(lib):
     # 64 x 96 runs bf16 (short side >= 64): padded to 256; the symmetric stages
     # use 128-tiles (too few 256-tiles), apply one 256-tile
     assert info["gram_tiles"] == 3 and info["poly_tiles"] == 3 and info["apply_tiles"] == 1
+    # fp32 (short side below 65): padded to 128; too few 128-tiles to give
+    # every CU one, so 64-tiles: 2 x 2 (lower triangle 3), apply 2 x 2
     info = lm.lionmuon_plan_info(specs, t=0, P=1, cfg=lm.config(ns_bf16_min_side=65))
-    assert info["gram_tiles"] == 1 and info["poly_tiles"] == 1 and info["apply_tiles"] == 1
+    assert info["gram_tiles"] == 3 and info["poly_tiles"] == 3 and info["apply_tiles"] == 4
 
 
 def test_plan_info_tiles_span_ragged_shapes(lib):
     specs = [(300, 520, False), (520, 300, False)]
-    # fp32: padded to 128, s -> 3 tiles, l -> 5 tiles; lower triangle 6; apply 15
+    # fp32: padded to 128 (384 x 640); 12 lower 128-tiles and 30 apply ones
+    # would leave most CUs idle, so 64-tiles: s -> 6, l -> 10; lower
+    # triangle 21, apply 60, per matrix
     info = lm.lionmuon_plan_info(specs, t=0, P=1, cfg=lm.config(ns_precision="fp32"))
     assert info["n_shape_classes"] == 1
-    assert info["gram_tiles"] == 12 and info["poly_tiles"] == 12 and info["apply_tiles"] == 30
+    assert info["gram_tiles"] == 42 and info["poly_tiles"] == 42 and info["apply_tiles"] == 120
     # bf16: padded to 256 (512 x 768); symmetric stages on 128-tiles (4 -> 10
     # lower), apply on 256-tiles (2 x 3)
     info = lm.lionmuon_plan_info(specs, t=0, P=1)
@@ -162,6 +166,17 @@ def test_plan_tile_choice_for_benchmark_sets(lib, name, gram_tiles, poly_tiles, 
     info = lm.lionmuon_plan_info(_specs(workloads.get(name)), t=0, P=1)
     assert info["gram_tiles"] == gram_tiles and info["poly_tiles"] == poly_tiles
     assert info["apply_tiles"] == apply_tiles
+
+
+def test_plan_fp32_tile_choice(lib):
+    """fp32 products run on 64-tiles when their 128-tiles would not give
+    every one of the 256 CUs one, else on 128-tiles."""
+    fp32 = lm.config(ns_precision="fp32")
+    info = lm.lionmuon_plan_info([(768, 768, False)], t=0, P=1, cfg=fp32)
+    assert (info["gram_tiles"], info["poly_tiles"], info["apply_tiles"]) == (78, 78, 144)
+    info = lm.lionmuon_plan_info(_specs(workloads.get("gpt2-124m")), t=0, P=1, cfg=fp32)
+    assert (info["gram_tiles"], info["poly_tiles"]) == (48 * 21, 48 * 21)
+    assert info["apply_tiles"] == 12 * 6 * (18 + 6 + 24 + 24)
 
 
 def test_workspace_bytes_matches_plan_info(lib):
