@@ -1038,20 +1038,25 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   constexpr int kLd = kBK;                       // LDS row: 128 bytes, chunks XOR-swizzled
   constexpr int kNT = Geo::kThreads;
   constexpr int kMI = Geo::kMI, kNI = Geo::kNI;
-  // One LDS block: two operand stages during the K loop, then the output tile.
+  // One LDS block: kNBuf operand stages during the K loop, then the output
+  // tile. Two stages, except for the bf16 apply on 128-tiles (a nearly empty
+  // last round of 256-tiles, one such workgroup per CU and too few of them
+  // to hide load latency with other workgroups): four, three of them in
+  // flight while one feeds the MFMAs.
   // Output staging row strides: kStR for row-major staging (16-byte-aligned
   // rows, 8 or 16 dwords apart modulo the 64 banks, so a quad of lanes
   // writing 4 consecutive rows never collides), kStC for transposed staging
   // (4 dwords apart, so 16 lanes writing 16 consecutive rows never collide).
   constexpr int kStR = BT + 16, kStC = BT + kEpc;
-  constexpr int kOperand = 2 * 2 * BT * kLd, kStage = BT * kStR;
+  constexpr int kNBuf = (MODE == kApply && BT == 128 && sizeof(T) == 2) ? 4 : 2;
+  constexpr int kOperand = kNBuf * 2 * BT * kLd, kStage = BT * kStR;
   __shared__ __attribute__((aligned(16))) T smem[kOperand > kStage ? kOperand : kStage];
   T (*sA)[BT][kLd] = reinterpret_cast<T (*)[BT][kLd]>(smem);
-  T (*sB)[BT][kLd] = reinterpret_cast<T (*)[BT][kLd]>(smem + 2 * BT * kLd);
+  T (*sB)[BT][kLd] = reinterpret_cast<T (*)[BT][kLd]>(smem + kNBuf * BT * kLd);
   // apply: the B operand (X, K = s along its rows) is staged k-major as
   // kBK rows of BT elements (512 bytes) and read transposed
   constexpr bool kBRows = MODE == kApply;
-  T (*sBr)[kBK][BT] = reinterpret_cast<T (*)[kBK][BT]>(smem + 2 * BT * kLd);
+  T (*sBr)[kBK][BT] = reinterpret_cast<T (*)[kBK][BT]>(smem + kNBuf * BT * kLd);
 
   // The workgroups of an XCD walk that XCD's tile list with a stride of
   // their number, skipping the tiles of matrices whose adaptive decision
@@ -1165,7 +1170,8 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
       }
     }
   };
-  static_assert(kDirect + 2 * kInst + kInstB < 64, "outstanding vector memory operations fit the counter");
+  constexpr int kOps = kInst + (kBRows ? kInstB : kInst);   // copies per wave per stage
+  static_assert(kDirect + (kNBuf - 1) * kOps < 64, "outstanding vector memory operations fit the counter");
   const auto& task = tasks[slot];
   const auto& mm = kconst(g.mats)[task.mat];
   const int64_t off_x_nxt = g.src ? mm.off_x[0] : mm.off_x[1];
@@ -1316,24 +1322,49 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // The barrier after each stage both publishes the stage just loaded (every
   // wave has waited for its own loads) and frees the buffer just read.
   const int nk = K / kBK;
-  if (prefetched) {
-    wait_vmcnt<kDirect>();                       // this tile's first stage; stores may still drain
-  } else {
-    dma(ops, 0, 0);
-    wait_vmcnt<0>();
-  }
+  // Wait until stage `s` has landed when `later` stages were requested after
+  // it (and, for a prefetched first stage, this wave's stores in between).
+  auto wait_stage = [&](int later, bool stores) {
+    if constexpr (kNBuf == 2) {
+      if (stores) wait_vmcnt<kDirect>();
+      else wait_vmcnt<0>();
+    } else {
+      static_assert(kNBuf == 4, "stage waits written out for 2 or 4 buffers");
+      const int n = later < kNBuf - 2 ? later : kNBuf - 2;
+      if (stores) {
+        if (n >= 2) wait_vmcnt<kDirect + 2 * kOps>();
+        else if (n == 1) wait_vmcnt<kDirect + kOps>();
+        else wait_vmcnt<kDirect>();
+      } else {
+        if (n >= 2) wait_vmcnt<2 * kOps>();
+        else if (n == 1) wait_vmcnt<kOps>();
+        else wait_vmcnt<0>();
+      }
+    }
+  };
+  // stages 0 .. kNBuf - 2 in flight before the first MFMA (stage 0 may have
+  // been requested already, before the previous tile's stores)
+  if (!prefetched) dma(ops, 0, 0);
+#pragma unroll
+  for (int st = 1; st < kNBuf - 1; ++st)
+    if (st < nk) dma(ops, st, st * kBK);
+  wait_stage(nk - 1, prefetched);
   prefetched = false;
   lds_barrier();
   for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & (kNBuf - 1);
     if constexpr (kTrB) {
-      preload_b(kt & 1);
+      preload_b(buf);
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (kt + 1 < nk) dma(ops, (kt + 1) & 1, (kt + 1) * kBK);
+    // the buffer of stage kt - 1, which every wave finished before the
+    // barrier that ended the previous step
+    const int nxt = kt + kNBuf - 1;
+    if (nxt < nk) dma(ops, nxt & (kNBuf - 1), nxt * kBK);
     __builtin_amdgcn_sched_barrier(0);
-    compute(kt & 1);
+    compute(buf);
     __builtin_amdgcn_sched_barrier(0);
-    wait_vmcnt<0>();
+    wait_stage(nk - 2 - kt, false);              // stage kt + 1
     lds_barrier();
   }
   // (the barrier after the last stage means no wave reads the operand
@@ -1646,10 +1677,11 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
   a.wd = l.wd;
   a.decide = l.decide;
   // persistent: at most as many workgroups per XCD as its CUs hold at once
-  // (one 256-tile, two 128-tiles or four 64-tiles per CU, limited by LDS)
+  // (one 256-tile, two 128-tiles (one for the four-stage bf16 apply) or four
+  // 64-tiles per CU, limited by LDS)
   // (only the non-final apply is persistent; the others keep one workgroup
   // per tile)
-  const int per_cu = l.tile == 256 ? 1 : (l.tile == 128 ? 2 : 4);
+  const int per_cu = l.tile == 256 ? 1 : (l.tile == 128 ? (l.fp32 ? 2 : 1) : 4);
   const int per_xcd = (mode != kApply || l.last) ? l.max_count : (kComputeUnits / kXcds) * per_cu;
   const dim3 grid(unsigned(l.max_count < per_xcd ? l.max_count : per_xcd) * kXcds);
 #define LM_LAUNCH(KERNEL, T, BT) \
