@@ -32,17 +32,17 @@ import workloads  # noqa: E402
 HBM_PEAK_GBPS = 8000.0            # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2516.6         # dense MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
 FP32_MFMA_PEAK_TFLOPS = 157.3
-# the kernels and the planner that sets their tiles and grids: traffic per
-# launch depends on both
+# the kernels, the planner that sets their tiles and grids, and the constants
+# both share: traffic per launch depends on all three
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2605_19811_amd", "csrc", f)
-                  for f in ("kernels.hip", "plan.cpp")]
+                  for f in ("kernels.hip", "plan.cpp", "lm_desc.h")]
 TRAFFIC_DIR = os.path.join(ROOT, "profiles")
 
 
 def kernel_hash():
-    """Hash of the kernel and planner sources with comments and blank lines
-    removed, so a comment-only edit keeps the counters taken with the same
-    code valid."""
+    """Hash of the kernel, planner and shared-constant sources with comments
+    and blank lines removed, so a comment-only edit keeps the counters taken
+    with the same code valid."""
     import re
     h = hashlib.sha256()
     for path in KERNEL_SOURCES:

@@ -25,8 +25,8 @@ constexpr int kComputeUnits = 256;  // CUs of one MI355X: workgroups of one full
 // time, or 16 for short sides above 1024); the others take the generic path
 // (blocks of kSrBlock long-side positions, read twice).
 constexpr int kSrBlock = 32;
-constexpr int kSrTallRows = 64;
-constexpr int kSrWideCols = 64;
+constexpr int kSrTallRows = 128;
+constexpr int kSrWideCols = 256;
 constexpr int kSrMaxRegSide = 2048;
 constexpr int kSrChunk = 64;     // short-side entries per stable-rank reduction workgroup
 enum SrKind : int32_t { kSrGeneric = 0, kSrTall = 1, kSrWide = 2, kSrWideNarrow = 3 };

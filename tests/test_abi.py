@@ -411,7 +411,8 @@ def test_plan_info_adaptive_step(lib):
         if t.lion_only or t.rows == 1:
             continue
         s, l = min(t.rows, t.cols), max(t.rows, t.cols)
-        nb = -(-l // 64)                      # register paths: 64 long-side positions a block
+        # register paths: blocks of 128 rows (tall) or 256 columns (wide)
+        nb = -(-l // (128 if t.rows >= t.cols else 256))
         blocks += nb
         part += nb * s
         extra += (s + nb * s + 2 * nb + -(-s // 64)) * 8
@@ -421,9 +422,10 @@ def test_plan_info_adaptive_step(lib):
     assert extra <= ws_extra < extra + 256 * (48 + 2)
     assert lm.lionmuon_workspace_bytes(specs, cfg) == info["workspace_bytes"]
     # generic path (rows not a multiple of 4 floats, or a short side beyond the
-    # register paths): blocks of 32 positions
+    # register paths): blocks of 32 positions; register paths: 128 rows (tall)
+    # or 256 columns (wide)
     for shape, nb in [((97, 61), 4), ((61, 97), 4), ((3000, 2100), 94), ((1600, 1700), 54),
-                      ((1100, 1300), 21), ((1300, 1284), 21), ((700, 900), 15)]:
+                      ((1100, 1300), 6), ((1300, 1284), 11), ((700, 900), 4)]:
         one = lm.lionmuon_plan_info([(*shape, False)], t=0, P=0,
                                     cfg=lm.config(adaptive_alpha=0.01, adaptive_power_steps=1))
         assert one["srank_bytes"] == 4.0 * shape[0] * shape[1] * 2 + 16.0 * nb * min(shape), shape
