@@ -230,7 +230,7 @@ typedef struct lm_plan_info {
   int64_t muon_elements;    /* elements on the Muon branch                     */
   int64_t gram_tiles, poly_tiles, apply_tiles; /* MFMA output tiles per NS step
                                (a nearly empty last round of 256x256 apply tiles
-                               is counted as the 128x128 tiles it runs as)      */
+                               is counted as the smaller tiles it runs as)      */
   double ns_flops;          /* algorithmic NS flops, symmetric products counted
                                once: K * sum s(s+1)l + s^2(s+1) + 2 s^2 l       */
   double ns_flops_dense;    /* dense convention K * sum 4 s^2 l + 2 s^3        */

@@ -399,11 +399,11 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
         gl.tile = p.tile[pr][st3];
         e = lm::launch_gemm(modes[st3], gl, stream);
         if (e != hipSuccess) return hip_fail(e, "Newton-Schulz kernel launch");
-        if (st3 == 2 && p.apply_tail_split[pr].max_count > 0) {   // the last round, as 128-tiles
+        if (st3 == 2 && p.apply_tail_split[pr].max_count > 0) {   // the last round, as smaller tiles
           gl.tasks = dp.d_tasks[pr][3];
           gl.split = dp.d_splits + pr * 4 + 3;
           gl.max_count = p.apply_tail_split[pr].max_count;
-          gl.tile = lm::kTileSmall;
+          gl.tile = p.tail_tile[pr];
           e = lm::launch_gemm(modes[st3], gl, stream);
           if (e != hipSuccess) return hip_fail(e, "Newton-Schulz kernel launch");
         }

@@ -1039,16 +1039,16 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   constexpr int kNT = Geo::kThreads;
   constexpr int kMI = Geo::kMI, kNI = Geo::kNI;
   // One LDS block: kNBuf operand stages during the K loop, then the output
-  // tile. Two stages, except for the bf16 apply on 128-tiles (a nearly empty
-  // last round of 256-tiles, one such workgroup per CU and too few of them
-  // to hide load latency with other workgroups): four, three of them in
-  // flight while one feeds the MFMAs.
+  // tile. Two stages, except for the bf16 apply on 128- or 64-tiles (a nearly
+  // empty last round of 256-tiles, one or two such workgroups per CU and too
+  // few of them to hide load latency with other workgroups): four, three of
+  // them in flight while one feeds the MFMAs.
   // Output staging row strides: kStR for row-major staging (16-byte-aligned
   // rows, 8 or 16 dwords apart modulo the 64 banks, so a quad of lanes
   // writing 4 consecutive rows never collides), kStC for transposed staging
   // (4 dwords apart, so 16 lanes writing 16 consecutive rows never collide).
   constexpr int kStR = BT + 16, kStC = BT + kEpc;
-  constexpr int kNBuf = (MODE == kApply && BT == 128 && sizeof(T) == 2) ? 4 : 2;
+  constexpr int kNBuf = (MODE == kApply && BT <= 128 && sizeof(T) == 2) ? 4 : 2;
   constexpr int kOperand = kNBuf * 2 * BT * kLd, kStage = BT * kStR;
   __shared__ __attribute__((aligned(16))) T smem[kOperand > kStage ? kOperand : kStage];
   T (*sA)[BT][kLd] = reinterpret_cast<T (*)[BT][kLd]>(smem);
@@ -1109,7 +1109,10 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   constexpr int kRpiB = 64 / kChunksB;
   constexpr int kInstB = kBK / kRpiB / kWaves;
   static_assert(!kBRows || kInstB * kRpiB * kWaves == kBK, "B rows split evenly over the waves");
-  auto swb = [](int k) { return (k & 3) * 4; };
+  // (bf16 rows of 64 elements are only 8 chunks: there the 4 rows of a read
+  // take chunk offsets 0, 0, 4, 4, which with the 128-byte row stride puts
+  // them in 4 distinct quarters of the banks)
+  auto swb = [](int k) { return (sizeof(T) == 2 && BT == 64) ? ((k >> 1) & 1) * 4 : (k & 3) * 4; };
   // Operands of one tile. Copy addresses are a wave-uniform base (operand,
   // K offset, instruction) plus one loop-invariant 32-bit byte offset per
   // lane and operand. Because kWaves (and kWaves * kRpiB) is even (a
@@ -1206,7 +1209,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // (transpose reads) before the next stage's copies are issued.
   constexpr bool kTrB = kBRows && sizeof(T) == 2;
   typename M::Frag bq[kTrB ? kSub : 1][kNI];
-  // The 16 transpose reads of a stage are one assembly block that ends by
+  // The 16 (64-tiles: 8) transpose reads of a stage are one assembly block that ends by
   // waiting for them: the compiler's own form of the read counts as touching
   // memory it cannot see and would first wait for every outstanding global
   // access, including the previous tile's stores still draining. Read
@@ -1218,10 +1221,11 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // of rows kb .. kb + 3.
   auto preload_b = [&](int buf) {
     if constexpr (kTrB) {
-      static_assert(kSub == 4 && kNI == 2 && (BT == 256 || BT == 128), "transpose-read block layout");
-      uint32_t base[2];
+      static_assert(kSub == 4 && ((kNI == 2 && (BT == 256 || BT == 128)) || (kNI == 1 && BT == 64)),
+                    "transpose-read block layout");
+      uint32_t base[kNI];
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
+      for (int j = 0; j < kNI; ++j) {
         const int grp = lane >> 4, m = lane & 15;
         const int n = wn + 32 * j + 16 * (grp & 1) + 4 * (m & 3);
         const int k = 8 * (grp >> 1) + (m >> 2);
@@ -1229,7 +1233,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
         // (a C cast: it converts the generic pointer to the LDS address space)
         base[j] = uint32_t(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) T*)(&sBr[buf][k][off])));
       }
-      u32x2 h[16];
+      u32x2 h[8 * kNI];
       if constexpr (BT == 256) {
         asm volatile(
             "ds_read_b64_tr_b16 %0, %16\n"
@@ -1253,7 +1257,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
               "=&v"(h[8]), "=&v"(h[9]), "=&v"(h[10]), "=&v"(h[11]), "=&v"(h[12]), "=&v"(h[13]), "=&v"(h[14]), "=&v"(h[15])
             : "v"(base[0]), "v"(base[1])
             : "memory");
-      } else {
+      } else if constexpr (BT == 128) {
         asm volatile(
             "ds_read_b64_tr_b16 %0, %16\n"
             "ds_read_b64_tr_b16 %1, %16 offset:1024\n"
@@ -1276,13 +1280,27 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
               "=&v"(h[8]), "=&v"(h[9]), "=&v"(h[10]), "=&v"(h[11]), "=&v"(h[12]), "=&v"(h[13]), "=&v"(h[14]), "=&v"(h[15])
             : "v"(base[0]), "v"(base[1])
             : "memory");
+      } else {
+        asm volatile(
+            "ds_read_b64_tr_b16 %0, %8\n"
+            "ds_read_b64_tr_b16 %1, %8 offset:512\n"
+            "ds_read_b64_tr_b16 %2, %8 offset:2048\n"
+            "ds_read_b64_tr_b16 %3, %8 offset:2560\n"
+            "ds_read_b64_tr_b16 %4, %8 offset:4096\n"
+            "ds_read_b64_tr_b16 %5, %8 offset:4608\n"
+            "ds_read_b64_tr_b16 %6, %8 offset:6144\n"
+            "ds_read_b64_tr_b16 %7, %8 offset:6656\n"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(h[0]), "=&v"(h[1]), "=&v"(h[2]), "=&v"(h[3]), "=&v"(h[4]), "=&v"(h[5]), "=&v"(h[6]), "=&v"(h[7])
+            : "v"(base[0])
+            : "memory");
       }
 #pragma unroll
       for (int kk = 0; kk < kSub; ++kk)
 #pragma unroll
         for (int j = 0; j < kNI; ++j) {
-          const bf16x4 lo = __builtin_bit_cast(bf16x4, h[(kk * 2 + j) * 2]);
-          const bf16x4 hi = __builtin_bit_cast(bf16x4, h[(kk * 2 + j) * 2 + 1]);
+          const bf16x4 lo = __builtin_bit_cast(bf16x4, h[(kk * kNI + j) * 2]);
+          const bf16x4 hi = __builtin_bit_cast(bf16x4, h[(kk * kNI + j) * 2 + 1]);
           bq[kk][j] = typename M::Frag{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         }
     }
@@ -1676,12 +1694,12 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
   a.lr = l.lr;
   a.wd = l.wd;
   a.decide = l.decide;
-  // persistent: at most as many workgroups per XCD as its CUs hold at once
-  // (one 256-tile, two 128-tiles (one for the four-stage bf16 apply) or four
-  // 64-tiles per CU, limited by LDS)
+  // persistent: at most as many workgroups per XCD as its CUs hold at once,
+  // limited by LDS (256-tiles: one per CU; 128-tiles: two, or one for the
+  // four-stage bf16 apply; 64-tiles: four, or two for the bf16 apply)
   // (only the non-final apply is persistent; the others keep one workgroup
   // per tile)
-  const int per_cu = l.tile == 256 ? 1 : (l.tile == 128 ? (l.fp32 ? 2 : 1) : 4);
+  const int per_cu = l.tile == 256 ? 1 : (l.tile == 128 ? (l.fp32 ? 2 : 1) : (l.fp32 ? 4 : 2));
   const int per_xcd = (mode != kApply || l.last) ? l.max_count : (kComputeUnits / kXcds) * per_cu;
   const dim3 grid(unsigned(l.max_count < per_xcd ? l.max_count : per_xcd) * kXcds);
 #define LM_LAUNCH(KERNEL, T, BT) \
@@ -1699,9 +1717,13 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
     else return hipErrorInvalidValue;
   } else if (l.tile == 256) {
     LM_LAUNCH_MODE(bf16, 256);
-  } else {
-    if (l.tile != 128) return hipErrorInvalidValue;
+  } else if (l.tile == 128) {
     LM_LAUNCH_MODE(bf16, 128);
+  } else {
+    // bf16 64-tiles exist for the apply only (the last round of 256-tiles)
+    if (l.tile != 64 || mode != kApply) return hipErrorInvalidValue;
+    if (!l.last) LM_LAUNCH(ns_apply_kernel, bf16, 64);
+    else LM_LAUNCH(ns_apply_last_kernel, bf16, 64);
   }
 #undef LM_LAUNCH_MODE
 #undef LM_LAUNCH

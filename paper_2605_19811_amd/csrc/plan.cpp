@@ -2,6 +2,7 @@
 #include "plan.h"
 
 #include <algorithm>
+#include <cstdint>
 #include <cmath>
 #include <map>
 #include <numeric>
@@ -378,16 +379,22 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
         }
       }
     }
-    // a nearly empty last round of 256-tiles runs as 128-tiles instead
+    // A nearly empty last round of 256-tiles runs as smaller tiles instead:
+    // 64-tiles (16 per 256-tile) when they fit one round of the CUs (and
+    // their indices fit the task fields), else 128-tiles (4 per 256-tile).
     std::vector<int64_t> ct;
     if (t_app == kTileBig) {
       const size_t n = p->apply[pr].size(), rem = n % kComputeUnits;
       if (n > rem && rem > 0 && 2 * rem <= size_t(kComputeUnits)) {
+        int64_t max_tl = 0;
+        for (size_t i = n - rem; i < n; ++i) max_tl = std::max<int64_t>(max_tl, p->apply[pr][i].tn);
+        const int split = (16 * rem <= size_t(kComputeUnits) && 4 * (max_tl + 1) <= INT16_MAX) ? 4 : 2;
+        p->tail_tile[pr] = kTileBig / split;
         for (size_t i = n - rem; i < n; ++i) {
           const GemmTask t = p->apply[pr][i];
-          for (int a = 0; a < 2; ++a)
-            for (int b = 0; b < 2; ++b) {
-              p->apply_tail[pr].push_back({t.mat, int16_t(2 * t.tm + a), int16_t(2 * t.tn + b)});
+          for (int a = 0; a < split; ++a)
+            for (int b = 0; b < split; ++b) {
+              p->apply_tail[pr].push_back({t.mat, int16_t(split * t.tm + a), int16_t(split * t.tn + b)});
               ct.push_back(ca[i]);
             }
         }

@@ -78,6 +78,7 @@ struct Plan {
   std::vector<GemmTask> apply_tail[2];
   XcdSplit apply_tail_split[2]{};
   int32_t tile[2][3] = {{kTileBig, kTileBig, kTileBig}, {kTileSmall, kTileSmall, kTileSmall}};
+  int32_t tail_tile[2] = {kTileSmall, kTileSmall};   // tile edge of apply_tail
   int64_t muon_elements = 0;
   int32_t n_shape_classes = 0;
 

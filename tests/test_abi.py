@@ -153,13 +153,14 @@ def test_plan_info_tiles_span_ragged_shapes(lib):
 
 
 # apply: 256-tiles; a last round of at most 128 of them (of 256 CUs) runs as
-# four 128-tiles each: 124M 1296 = 5 x 256 + 16, 720M 10800 = 42 x 256 + 48
+# sixteen 64-tiles each when those fit one round, else four 128-tiles each:
+# 124M 1296 = 5 x 256 + 16 (16 x 16 = 256 64-tiles), 720M 10800 = 42 x 256 + 48
 # Gram / polynomial: 256-tiles unless 128-tiles are estimated to finish
 # sooner. At 124M the Gram (K = l up to 3072) keeps 256-tiles (288 of them,
 # the longest first), the polynomial (K = 768) takes 128-tiles: 288 short
 # 256-tiles would leave a second round 12% full.
 @pytest.mark.parametrize("name,gram_tiles,poly_tiles,apply_tiles", [
-    ("gpt2-124m", 48 * 6, 48 * 21, 1280 + 4 * 16),
+    ("gpt2-124m", 48 * 6, 48 * 21, 1280 + 16 * 16),
     ("gpt2-355m", 96 * 10, 96 * 10, 24 * 48 + 24 * 16 + 48 * 64),   # 4608 = 18 x 256: no tail
     ("gpt2-720m", 144 * 15, 144 * 15, 10752 + 4 * 48)])
 def test_plan_tile_choice_for_benchmark_sets(lib, name, gram_tiles, poly_tiles, apply_tiles):
