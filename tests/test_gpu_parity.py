@@ -443,7 +443,7 @@ def test_full_set_sampled(name):
 def test_full_set_every_matrix(name):
     """The set's Muon step in the benchmark's launch configuration, with every
     matrix compared with the oracle (at 124M the persistent apply walks five
-    tiles per workgroup and the last round goes to the 128-tile launch; at
+    tiles per workgroup and the last round goes to the 64-tile launch; at
     355M eighteen)."""
     wl = workloads.get(name)
     params, moms, grads = workloads.device_state(torch, wl, DEV, seed=8, warm=True, n_grad=1)
