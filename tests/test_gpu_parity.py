@@ -382,7 +382,7 @@ def test_profiling_counts_every_launch():
 def _sample_indices(wl):
     """One tensor of every distinct shape, plus the last matrix of the list
     (its last apply tiles are the ones a nearly empty final round of 256-tiles
-    hands to the 128-tile launch)."""
+    hands to the launch of smaller tiles)."""
     seen, out = set(), []
     for i, t in enumerate(wl.tensors):
         key = (t.rows, t.cols, t.lion_only)
