@@ -897,7 +897,8 @@ __global__ __launch_bounds__(256) void srank_decide_kernel(SrankArgs a) {
 // K-contiguous ("NT"), except the apply's X, which is staged k-major and read
 // with transpose reads. K is staged through LDS 128 bytes per row at a time by
 // direct global->LDS loads (no register staging), double buffered: the loads
-// of stage k+1 are in flight while stage k feeds the MFMAs. Rows are
+// of stage k+1 are in flight while stage k feeds the MFMAs (the bf16 apply
+// on 128- and 64-tiles keeps four stages, three in flight). Rows are
 // unpadded; their eight 16-byte chunks are XOR-swizzled by row so that the
 // 128-bit fragment reads, served 16 lanes (16 rows) per LDS cycle across 64
 // banks, are bank-conflict free.
@@ -906,7 +907,8 @@ __global__ __launch_bounds__(256) void srank_decide_kernel(SrankArgs a) {
 //   BT = 128: 4 waves (2 x 2), each a 64 x 64 sub-tile of 2 x 2 blocks, for
 //             stages with too few 256-tiles to fill the chip;
 //   BT = 64:  4 waves (2 x 2), each one 32 x 32 block (fp32 products with
-//             too few 128-tiles to fill the chip).
+//             too few 128-tiles to fill the chip, and the bf16 apply's last
+//             round when sixteen times its leftover 256-tiles fit one round).
 // Accumulator element r of block (mi, ni) sits at row
 // wm + 32 mi + 8 (r / 4) + 4 (lane / 32) + r % 4, col wn + 32 ni + lane % 32.
 // Wait until at most N vector-memory operations of this wave are outstanding
