@@ -174,6 +174,26 @@ def test_mixed_list_muon_step(precision):
             check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_m, wd, precision)
 
 
+@pytest.mark.parametrize("last", ["wide", "tall"])
+def test_apply_small_tile_round_on_ragged_matrices(last):
+    """264 apply 256-tiles: the 8 of the last round run as 128 64-tiles, all
+    of them from the last matrix, whose W edges (300 of 512 padded rows,
+    3000 of 3072 padded columns) fall inside those tiles; the tall variant
+    also writes O transposed back. Every matrix is checked."""
+    shapes = [(700, 5000)] * 4 + [(300, 3000) if last == "wide" else (3000, 300)]
+    info = lm.lionmuon_plan_info([(*sh, False) for sh in shapes], t=0, P=1)
+    assert info["apply_tiles"] == 256 + 8 * 16
+    W0, M0, G = _state(shapes, 77)
+    W, M, Gd = [dev(x) for x in W0], [dev(x) for x in M0], [dev(x) for x in G]
+    lr_m, wd = 0.02, 0.1
+    cfg = lm.config(ns_precision="bf16", lr_muon=lr_m, lr_lion=1e-3)
+    print(f"small-tile last round, last matrix {last}", flush=True)
+    lm.lionmuon_step_ex(W, Gd, M, 0, 1, 0.9, 0.99, wd, cfg)
+    sync()
+    for i in range(len(shapes)):
+        check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_m, wd, "bf16")
+
+
 @pytest.mark.parametrize("t,P", [(0, 2), (1, 2), (5, 0)])
 def test_adamw_tensors_in_mixed_list(t, P):
     """1-D tensors (and a matrix) flagged AdamW take AdamW every step
