@@ -230,10 +230,11 @@ def ns_flops_per_launch(wl):
     return {"gram": gram, "poly": poly, "apply": apply}
 
 
-def cpu_baseline(wl, P):
+def cpu_baseline(wl, P, budget_s=10.0):
     """fp64 oracle on a bounded sample: one Lion step and one Muon step on one
-    tensor of every distinct shape, scaled to the whole set by element count
-    (Lion) and by Newton-Schulz flops (Muon), amortised over P."""
+    tensor of every distinct shape, scaled to the whole set by tensor count,
+    repeated until about `budget_s` seconds of CPU work (at least once) and
+    averaged over the repetitions, amortised over P."""
     import numpy as np
     import oracle
     try:
@@ -248,23 +249,33 @@ def cpu_baseline(wl, P):
         if seen[key] == 1:
             sample.append(i)
     count = {k: v for k, v in seen.items()}
-    t_lion = t_muon = 0.0
     rng = np.random.default_rng(0)
+    inputs = []
     for i in sample:
         t = wl.tensors[i]
-        reps = count[(t.rows, t.cols, t.lion_only)]
         W = rng.standard_normal(t.shape).astype(np.float32) * 0.02
         M = rng.standard_normal(t.shape).astype(np.float32) * wl.grad_std
         G = rng.standard_normal(t.shape).astype(np.float32) * wl.grad_std
-        t0 = time.perf_counter()
-        oracle.lionmuon_update(W, G, M, 1, P, wl.beta1, wl.beta2, wl.lr_muon, wl.lr_lion,
-                               wl.wd, lion_only=True)
-        t1 = time.perf_counter()
-        oracle.lionmuon_update(W, G, M, 0, 1, wl.beta1, wl.beta2, wl.lr_muon, wl.lr_lion,
-                               wl.wd, lion_only=t.lion_only)
-        t2 = time.perf_counter()
-        t_lion += (t1 - t0) * reps
-        t_muon += (t2 - t1) * reps
+        inputs.append((t, W, M, G))
+    t_lion = t_muon = 0.0
+    rounds = 0
+    start = time.perf_counter()
+    while rounds == 0 or time.perf_counter() - start < budget_s:
+        for t, W, M, G in inputs:
+            reps = count[(t.rows, t.cols, t.lion_only)]
+            t0 = time.perf_counter()
+            oracle.lionmuon_update(W, G, M, 1, P, wl.beta1, wl.beta2, wl.lr_muon, wl.lr_lion,
+                                   wl.wd, lion_only=True)
+            t1 = time.perf_counter()
+            oracle.lionmuon_update(W, G, M, 0, 1, wl.beta1, wl.beta2, wl.lr_muon, wl.lr_lion,
+                                   wl.wd, lion_only=t.lion_only)
+            t2 = time.perf_counter()
+            t_lion += (t1 - t0) * reps
+            t_muon += (t2 - t1) * reps
+        rounds += 1
+    spent = time.perf_counter() - start
+    t_lion /= rounds
+    t_muon /= rounds
     if P == 0:
         amort = t_lion
     else:
@@ -272,7 +283,8 @@ def cpu_baseline(wl, P):
     return {"value": round(amort * 1e3, 1), "unit": "ms/step", "cores": int(cores),
             "kind": "oracle",
             "sample": (f"one Lion and one Muon fp64 oracle step on one tensor of each of the "
-                       f"{len(sample)} distinct shapes of {wl.name}, scaled by tensor count; "
+                       f"{len(sample)} distinct shapes of {wl.name}, scaled by tensor count, "
+                       f"repeated {rounds}x ({spent:.1f} s of CPU work) and averaged; "
                        f"Lion {t_lion * 1e3:.0f} ms/step, Muon {t_muon * 1e3:.0f} ms/step, "
                        f"amortised over P={P}")}
 
