@@ -44,8 +44,11 @@
  *    an error and modifies nothing. A HIP failure after enqueueing started
  *    returns LM_ERR_HIP; tensors may then be partly updated.
  *  - lionmuon_last_error() gives a thread-local message for the last failure.
- *  - Calls that use the library-owned workspace are serialised by a mutex;
- *    calls with caller workspaces may run concurrently on distinct streams.
+ *  - Calls that use the library-owned workspace are serialised: on the host
+ *    by a mutex, and on the device by an event, so a call on another stream
+ *    than the previous user of that workspace first waits (on the device,
+ *    without blocking the host) for that user's work. Calls with caller
+ *    workspaces may run concurrently on distinct streams.
  */
 #ifndef LIONMUON_H
 #define LIONMUON_H

@@ -69,10 +69,16 @@ constexpr size_t kMaxPlans = 16;
 std::mutex g_mu;                                      // plans, workspace, profiling
 std::list<std::shared_ptr<DevicePlan>> g_plans;       // most recent first
 
+// The library-owned workspace of a device. Calls that use it are serialised
+// on the host by g_mu, but their kernels run on the callers' streams: a call
+// on another stream than the previous user's first waits (on the device) for
+// the event recorded after that user's work.
 struct OwnedWorkspace {
   int device = -1;
   void* ptr = nullptr;
   size_t bytes = 0;
+  hipEvent_t done = nullptr;       // recorded after the last call that used it
+  hipStream_t last = nullptr;      // that call's stream
 };
 std::vector<OwnedWorkspace> g_ws;
 
@@ -196,32 +202,45 @@ lm_status get_plan(const TensorIn* x, int32_t n, lm::StepKind kind, lm::NsPrecis
   return LM_OK;
 }
 
-lm_status owned_workspace(size_t bytes, void** ptr) {
+lm_status owned_workspace(size_t bytes, hipStream_t stream, OwnedWorkspace** out) {
   int device = 0;
   hipError_t e = hipGetDevice(&device);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-  for (auto& w : g_ws) {
-    if (w.device != device) continue;
-    if (w.bytes >= bytes) {
-      *ptr = w.ptr;
-      return LM_OK;
-    }
-    (void)hipFree(w.ptr);          // waits for outstanding work on the device
-    w.ptr = nullptr;
-    w.bytes = 0;
-    e = hipMalloc(&w.ptr, bytes);
-    if (e != hipSuccess) return fail(LM_ERR_OUT_OF_MEMORY, "workspace: hipMalloc failed");
-    w.bytes = bytes;
-    *ptr = w.ptr;
-    return LM_OK;
+  OwnedWorkspace* w = nullptr;
+  for (auto& x : g_ws)
+    if (x.device == device) w = &x;
+  if (!w) {
+    g_ws.emplace_back();
+    w = &g_ws.back();
+    w->device = device;
   }
-  OwnedWorkspace w;
-  w.device = device;
-  e = hipMalloc(&w.ptr, bytes);
-  if (e != hipSuccess) return fail(LM_ERR_OUT_OF_MEMORY, "workspace: hipMalloc failed");
-  w.bytes = bytes;
-  g_ws.push_back(w);
-  *ptr = w.ptr;
+  if (w->bytes < bytes) {
+    if (w->ptr) (void)hipFree(w->ptr);   // waits for outstanding work on the device
+    w->ptr = nullptr;
+    w->bytes = 0;
+    e = hipMalloc(&w->ptr, bytes);
+    if (e != hipSuccess) return fail(LM_ERR_OUT_OF_MEMORY, "workspace: hipMalloc failed");
+    w->bytes = bytes;
+  }
+  if (w->done && w->last != stream) {
+    e = hipStreamWaitEvent(stream, w->done, 0);
+    if (e != hipSuccess) return hip_fail(e, "workspace: hipStreamWaitEvent");
+  }
+  *out = w;
+  return LM_OK;
+}
+
+// Record the end of this call's use of the owned workspace (device scope: the
+// event only orders later work on the same device).
+lm_status release_workspace(OwnedWorkspace* w, hipStream_t stream) {
+  hipError_t e = hipSuccess;
+  if (!w->done) {
+    e = hipEventCreateWithFlags(&w->done, hipEventDisableTiming | hipEventDisableSystemFence);
+    if (e != hipSuccess) return hip_fail(e, "workspace: hipEventCreate");
+  }
+  e = hipEventRecord(w->done, stream);
+  if (e != hipSuccess) return hip_fail(e, "workspace: hipEventRecord");
+  w->last = stream;
   return LM_OK;
 }
 
@@ -511,17 +530,24 @@ lm_status step_impl(float* const* params, const float* const* grads, float* cons
   lm_status s = get_plan(x.data(), n, kind, precision_of(*cfg), rms02, stream, &dp);
   if (s != LM_OK) return s;
   void* ws = workspace;
+  OwnedWorkspace* ow = nullptr;
   if (dp->plan.ws_bytes > 0) {
     if (workspace) {
       if (workspace_bytes < dp->plan.ws_bytes)
         return fail(LM_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than lionmuon_workspace_bytes");
     } else {
-      s = owned_workspace(dp->plan.ws_bytes, &ws);
+      s = owned_workspace(dp->plan.ws_bytes, stream, &ow);
       if (s != LM_OK) return s;
+      ws = ow->ptr;
     }
   }
-  return enqueue(*dp, step_consts(beta1, beta2, wd, cfg->lr_muon, cfg->lr_lion, cfg->ns_eps, cfg, t),
-                 *cfg, ws, false, aout, stream);
+  s = enqueue(*dp, step_consts(beta1, beta2, wd, cfg->lr_muon, cfg->lr_lion, cfg->ns_eps, cfg, t),
+              *cfg, ws, false, aout, stream);
+  if (ow) {                              // also after a partial enqueue
+    const lm_status r = release_workspace(ow, stream);
+    if (s == LM_OK) s = r;
+  }
+  return s;
 }
 
 }  // namespace
@@ -711,15 +737,22 @@ lm_status lionmuon_ns(const float* X, float* O, int64_t rows, int64_t cols, int3
                          &dp);
   if (s != LM_OK) return s;
   void* ws = workspace;
+  OwnedWorkspace* ow = nullptr;
   if (workspace) {
     if (workspace_bytes < dp->plan.ws_bytes)
       return fail(LM_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than lionmuon_workspace_bytes");
   } else {
-    s = owned_workspace(dp->plan.ws_bytes, &ws);
+    s = owned_workspace(dp->plan.ws_bytes, stream, &ow);
     if (s != LM_OK) return s;
+    ws = ow->ptr;
   }
-  return enqueue(*dp, step_consts(0.0, 0.0, 0.0, 0.0, 0.0, cfg->ns_eps, nullptr, 0), *cfg, ws, true,
-                 AdaptiveOut(), stream);
+  s = enqueue(*dp, step_consts(0.0, 0.0, 0.0, 0.0, 0.0, cfg->ns_eps, nullptr, 0), *cfg, ws, true,
+              AdaptiveOut(), stream);
+  if (ow) {
+    const lm_status r = release_workspace(ow, stream);
+    if (s == LM_OK) s = r;
+  }
+  return s;
 }
 
 lm_status lionmuon_profiling_enable(int32_t enable) {
@@ -762,8 +795,10 @@ lm_status lionmuon_profiling_reset(void) {
 void lionmuon_release(void) {
   std::lock_guard<std::mutex> lock(g_mu);
   g_plans.clear();
-  for (auto& w : g_ws)
+  for (auto& w : g_ws) {
     if (w.ptr) (void)hipFree(w.ptr);
+    if (w.done) (void)hipEventDestroy(w.done);
+  }
   g_ws.clear();
   for (const PendingEvent& pe : g_pending) {
     (void)hipEventSynchronize(pe.stop);

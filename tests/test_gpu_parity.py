@@ -364,6 +364,34 @@ def test_side_stream():
     check_muon(W0[0], G[0], M0[0], host(W), host(M), 0.9, 0.99, 0.01, 0.1, "bf16")
 
 
+def test_library_workspace_shared_across_streams():
+    """Two calls that both use the library-owned workspace, enqueued back to
+    back on two streams with no host synchronisation between them: the
+    second call's kernels must wait (on the device) for the first call's, or
+    its preparation would overwrite the first call's Newton-Schulz operands.
+    The first list needs the larger workspace, so the second call does not
+    reallocate it (which would synchronise the device)."""
+    lm.lionmuon_release()
+    shapes1, shapes2 = [(768, 2304)] * 6, [(1024, 1024)] * 4
+    assert (lm.lionmuon_workspace_bytes([(*sh, False) for sh in shapes1])
+            > lm.lionmuon_workspace_bytes([(*sh, False) for sh in shapes2]))
+    W1, M1, G1 = _state(shapes1, 61)
+    W2, M2, G2 = _state(shapes2, 62)
+    d1 = [[dev(x) for x in t] for t in (W1, M1, G1)]
+    d2 = [[dev(x) for x in t] for t in (W2, M2, G2)]
+    lr_m, wd = 0.02, 0.1
+    cfg = lm.config(ns_precision="bf16", lr_muon=lr_m, lr_lion=1e-3)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    sync()
+    print("library workspace on two streams", flush=True)
+    lm.lionmuon_step_ex(d1[0], d1[2], d1[1], 0, 1, 0.9, 0.99, wd, cfg, stream=s1)
+    lm.lionmuon_step_ex(d2[0], d2[2], d2[1], 0, 1, 0.9, 0.99, wd, cfg, stream=s2)
+    sync()
+    for W0, M0, G, Wd, Md in ((W1, M1, G1, d1[0], d1[1]), (W2, M2, G2, d2[0], d2[1])):
+        for i in range(len(W0)):
+            check_muon(W0[i], G[i], M0[i], host(Wd[i]), host(Md[i]), 0.9, 0.99, lr_m, wd, "bf16")
+
+
 def test_binding_rejects_cpu_and_non_contiguous_tensors():
     W = torch.zeros(8, 8, device=DEV)
     with pytest.raises(lm.LionMuonError):
