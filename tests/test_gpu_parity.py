@@ -146,6 +146,48 @@ def test_ns_hook_largest_long_side():
     assert err <= NS_TOL["bf16"], err
 
 
+def _sylvester_hadamard(n):
+    """n x n matrix of +-1 with orthogonal rows (Sylvester's construction)."""
+    H = torch.ones((1, 1), device=DEV)
+    while H.shape[0] < n:
+        H = torch.cat([torch.cat([H, H], 1), torch.cat([H, -H], 1)], 0)
+    return H
+
+
+def _scalar_quintic(x, steps=5, abc=(3.4445, -4.7750, 2.0315)):
+    a, b, c = abc
+    for _ in range(steps):
+        x = a * x + b * x ** 3 + c * x ** 5
+    return x
+
+
+@pytest.mark.parametrize("tall", [False, True])
+def test_ns_hook_maximum_size_orthogonal_rows(tall):
+    """The largest matrix the library takes (short side 16384, 2^30 elements):
+    X = [H H H H] with H a 16384 x 16384 Hadamard matrix, whose rows are
+    orthogonal with equal norms, so NS_5 has the closed form
+    p^5(sigma / ||X||_F) X / sigma (sigma = 256, ||X||_F = 32768) that holds at
+    any size; the tall case iterates X^T. Checked on the GPU against that form."""
+    s, l = 16384, 65536
+    H = _sylvester_hadamard(s)
+    X = torch.cat([H] * (l // s), 1)
+    del H
+    if tall:
+        X = X.t().contiguous()
+    print(f"NS hook at the maximum size, tall={tall}", flush=True)
+    out = lm.lionmuon_ns(X, lm.config(ns_precision="bf16"))
+    sync()
+    sigma, fro = 256.0, 32768.0
+    k = _scalar_quintic(sigma / (fro + 1e-7)) / sigma
+    err = (torch.linalg.vector_norm((out - k * X).double()) /
+           torch.linalg.vector_norm((k * X).double())).item()
+    print(f"  closed-form direction error {err:.2e}", flush=True)
+    del X, out
+    lm.lionmuon_release()
+    torch.cuda.empty_cache()
+    assert err <= NS_TOL["bf16"], err
+
+
 # --------------------------------------------------------------------------
 # Whole steps
 # --------------------------------------------------------------------------
