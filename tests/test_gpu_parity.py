@@ -236,6 +236,48 @@ def test_apply_small_tile_round_on_ragged_matrices(last):
         check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_m, wd, "bf16")
 
 
+def test_many_small_tensors_in_one_call():
+    """2000 tensors of random small shapes (1-D, tall, wide, square, some
+    empty) in one call: the multi-tensor Lion grid, the per-matrix
+    preparation, norm and Newton-Schulz task lists all span thousands of
+    segments. A Muon step (t = 0) and a Lion step (t = 1) are checked on
+    every tensor."""
+    rng = np.random.default_rng(55)
+    shapes = []
+    for i in range(2000):
+        kind = i % 5
+        if kind == 0:
+            shapes.append((1, int(rng.integers(1, 300))))
+        elif kind == 4 and i % 25 == 4:
+            shapes.append((0, int(rng.integers(1, 40))))
+        else:
+            shapes.append((int(rng.integers(2, 90)), int(rng.integers(2, 90))))
+    W0, M0, G = _state(shapes, 56)
+    W, M, Gd = [dev(x) for x in W0], [dev(x) for x in M0], [dev(x) for x in G]
+    lr_m, lr_l, wd = 0.02, 1e-3, 0.1
+    cfg = lm.config(lr_muon=lr_m, lr_lion=lr_l)
+    print("2000 small tensors, Muon step", flush=True)
+    lm.lionmuon_step_ex(W, Gd, M, 0, 2, 0.9, 0.99, wd, cfg)
+    sync()
+    W1 = [host(x) for x in W]
+    M1 = [host(x) for x in M]
+    for i, s in enumerate(shapes):
+        if min(s) == 0:
+            continue
+        if min(s) == 1:
+            check_lion(W0[i], G[i], M0[i], W1[i], M1[i], 0.9, 0.99, lr_l, wd)
+        else:
+            check_muon(W0[i], G[i], M0[i], W1[i], M1[i], 0.9, 0.99, lr_m, wd,
+                       "bf16" if min(s) >= 64 else "fp32")
+    print("2000 small tensors, Lion step", flush=True)
+    lm.lionmuon_step_ex(W, Gd, M, 1, 2, 0.9, 0.99, wd, cfg)
+    sync()
+    for i, s in enumerate(shapes):
+        if min(s) == 0:
+            continue
+        check_lion(W1[i], G[i], M1[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_l, wd)
+
+
 @pytest.mark.parametrize("t,P", [(0, 2), (1, 2), (5, 0)])
 def test_adamw_tensors_in_mixed_list(t, P):
     """1-D tensors (and a matrix) flagged AdamW take AdamW every step
