@@ -53,6 +53,31 @@ def test_lion_step_ragged_and_misaligned(numel, offset):
     assert torch.all(bufs[0][:offset] == 0) and torch.all(bufs[0][offset + numel:] == 0)
 
 
+@pytest.mark.parametrize("shape", [(300, 520), (520, 300), (256, 768), (768, 256)])
+@pytest.mark.parametrize("precision", ["fp32", "bf16"])
+def test_muon_step_misaligned_buffers(shape, precision):
+    """W, G and M of a matrix 4 bytes past a 16-byte boundary (and ragged
+    shapes): the preparation reads G and M, and the last apply updates W,
+    through their per-element paths. Guard elements around each buffer must
+    stay untouched."""
+    rng = np.random.default_rng([shape[0], shape[1], len(precision)])
+    n = shape[0] * shape[1]
+    W0 = (rng.standard_normal(shape) * 0.02).astype(np.float32)
+    M0 = (rng.standard_normal(shape) * 1e-2).astype(np.float32)
+    G = (rng.standard_normal(shape) * 1e-2).astype(np.float32)
+    bufs = [torch.zeros(n + 8, device=DEV) for _ in range(3)]
+    W, M, Gd = (b[1:1 + n].view(shape) for b in bufs)
+    W.copy_(dev(W0)); M.copy_(dev(M0)); Gd.copy_(dev(G))
+    lr_m, wd = 0.02, 0.1
+    cfg = lm.config(ns_precision=precision, lr_muon=lr_m, lr_lion=1e-3)
+    print(f"misaligned Muon step {shape} {precision}", flush=True)
+    lm.lionmuon_step_ex([W], [Gd], [M], 0, 2, 0.9, 0.99, wd, cfg)
+    sync()
+    check_muon(W0, G, M0, host(W), host(M), 0.9, 0.99, lr_m, wd, precision)
+    for b in bufs:
+        assert torch.all(b[:1] == 0) and torch.all(b[1 + n:] == 0)
+
+
 def test_lion_step_multi_tensor_list():
     shapes = [(1, 768), (768, 2304), (3, 5), (1, 1), (50, 77), (4096, 3)]
     rng = np.random.default_rng(7)
