@@ -1489,13 +1489,16 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
     }
   } else {
     // X' = alpha B' X with B' = a I + b A + c A A from the polynomial step
-    const float alpha = g.first ? kconst(g.rscale)[task.mat] : 1.0f;
+    // (alpha, the Frobenius scaling, only on the first step)
+    if (g.first) {
+      const float alpha = kconst(g.rscale)[task.mat];
 #pragma unroll
-    for (int mi = 0; mi < kMI; ++mi)
+      for (int mi = 0; mi < kMI; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < kNI; ++ni)
+        for (int ni = 0; ni < kNI; ++ni)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[mi][ni][r] *= alpha;
+          for (int r = 0; r < 16; ++r) acc[mi][ni][r] *= alpha;
+    }
     if constexpr (!LAST) {
       if (nslot < count) {
         dma(make_ops(tasks[nslot]), 0, 0);
