@@ -54,16 +54,17 @@ def check_lion(W0, G, M0, W_gpu, M_gpu, beta1, beta2, lr, wd, lion_only=True):
     return int(band.sum())
 
 
-def muon_direction_error(W0, G, M0, W_gpu, beta1, lr, wd, kappa=1.0):
+def muon_direction_error(W0, G, M0, W_gpu, beta1, lr, wd, kappa=1.0, steps=oracle.NS_STEPS):
     W0d = np.asarray(W0, np.float64)
     ghat = beta1 * np.asarray(M0, np.float64) + (1.0 - beta1) * np.asarray(G, np.float64)
-    o_ref = kappa * oracle.newton_schulz(ghat)
+    o_ref = kappa * oracle.newton_schulz(ghat, steps)
     o_gpu = (W0d - np.asarray(W_gpu, np.float64)) / lr - wd * W0d
     return rel_fro(o_gpu, o_ref)
 
 
-def check_muon(W0, G, M0, W_gpu, M_gpu, beta1, beta2, lr, wd, precision, kappa=1.0):
-    err = muon_direction_error(W0, G, M0, W_gpu, beta1, lr, wd, kappa)
+def check_muon(W0, G, M0, W_gpu, M_gpu, beta1, beta2, lr, wd, precision, kappa=1.0,
+               steps=oracle.NS_STEPS):
+    err = muon_direction_error(W0, G, M0, W_gpu, beta1, lr, wd, kappa, steps)
     assert err <= NS_TOL[precision], f"Muon direction error {err:.3e} > {NS_TOL[precision]}"
     check_momentum(M0, G, M_gpu, beta2)
     return err

@@ -161,6 +161,31 @@ def test_ns_hook_per_step_schedule(precision):
     assert err <= NS_TOL[precision], err
 
 
+@pytest.mark.parametrize("steps", [1, 2])
+@pytest.mark.parametrize("shape", [(300, 520), (520, 300)])
+@pytest.mark.parametrize("precision", ["fp32", "bf16"])
+def test_short_newton_schulz_runs(steps, shape, precision):
+    """One or two Newton-Schulz steps, through the hook and a whole Muon step.
+    With one, the first step (the only one that applies the Frobenius
+    scaling) is also the last (the one that writes O or updates W)."""
+    X = workloads.random_matrix([26, steps, *shape], *shape, std=1e-2)
+    print(f"NS hook, {steps} step(s), {shape} {precision}", flush=True)
+    out = lm.lionmuon_ns(dev(X), lm.config(ns_precision=precision, ns_steps=steps))
+    sync()
+    err = rel_fro(host(out), oracle.newton_schulz(X, steps))
+    assert err <= NS_TOL[precision], err
+    rng = np.random.default_rng([27, steps, *shape])
+    W0 = (rng.standard_normal(shape) * 0.02).astype(np.float32)
+    M0 = (rng.standard_normal(shape) * 1e-2).astype(np.float32)
+    G = (rng.standard_normal(shape) * 1e-2).astype(np.float32)
+    W, M, Gd = dev(W0), dev(M0), dev(G)
+    cfg = lm.config(ns_precision=precision, ns_steps=steps, lr_muon=0.02, lr_lion=1e-3)
+    print(f"Muon step, {steps} NS step(s), {shape} {precision}", flush=True)
+    lm.lionmuon_step_ex([W], [Gd], [M], 0, 2, 0.9, 0.99, 0.1, cfg)
+    sync()
+    check_muon(W0, G, M0, host(W), host(M), 0.9, 0.99, 0.02, 0.1, precision, steps=steps)
+
+
 def test_ns_hook_largest_long_side():
     """The embedding shape (50257 x 1280), the largest matrix of the benchmark
     sets, through the Muon kernels (long side padded to 50304)."""
