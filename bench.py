@@ -149,31 +149,78 @@ def pmc_summary(wl_name, fetch_csv, write_csv, calib_fetch_csv, calib_write_csv,
     return path
 
 
-def sq_summary(wl_name, sq_csv, command):
-    """MFMA and LDS occupancy of each library kernel from one rocprofv3 SQ
-    counter pass (sums over all dispatches of the kernel)."""
+SIMDS = 1024                      # 256 CUs x 4 SIMDs
+XCDS = 8
+
+
+def sq_summary(wl_name, sq_csvs, command):
+    assert len(sq_csvs) == 1, "one counter pass"
+    """MFMA issue and utilisation of each Newton-Schulz phase from rocprofv3
+    counter passes (one CSV per pass; per-dispatch durations from the CSV's
+    timestamps), against the phase's algorithmic flops: issued flops = 512
+    SQ_INSTS_VALU_MFMA_MOPS_BF16 (F32 for fp32 products)."""
     import collections
     import csv
-    tot = collections.defaultdict(lambda: collections.defaultdict(float))
-    for r in csv.DictReader(open(sq_csv)):
-        if phase_of(r["Kernel_Name"]) is None:
+    wl = workloads.get(wl_name.replace("-adaptive", ""))
+    algo = ns_flops_per_launch(wl)
+    # per phase: counter sums, per-dispatch durations and dispatch counts
+    cnt = collections.defaultdict(lambda: collections.defaultdict(float))
+    dur = collections.defaultdict(dict)          # phase -> {(pass, dispatch): ns}
+    n256 = collections.defaultdict(set)
+    nall = collections.defaultdict(set)
+    for k, path in enumerate(sq_csvs):
+        for r in csv.DictReader(open(path)):
+            ph = phase_of(r["Kernel_Name"])
+            if ph is None:
+                continue
+            key = (k, int(r["Dispatch_Id"]))
+            cnt[ph][r["Counter_Name"]] += float(r["Counter_Value"])
+            dur[ph][key] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+            nall[ph].add(key)
+            if "Li256" in r["Kernel_Name"]:
+                n256[ph].add(key)
+    lines = [f"# MFMA issue and utilisation: {wl_name}", "", f"Command: `{command}`", "",
+             "Per Newton-Schulz phase launch (the apply's launch includes its small-tile tail "
+             "and last-step kernels), from one counter pass (dispatches serialised; durations "
+             "from the pass's own timestamps).", "",
+             "- `algorithmic frac`: the phase's symmetric flop count (Gram s(s+1)l, polynomial "
+             "s^2(s+1), apply 2 s^2 l per matrix) over the launch duration, against the dense "
+             "bf16 peak 2516.6 TFLOP/s (256 CUs x 2.4 GHz x 4096 flop/clk).",
+             "- `issued frac`: 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16 (+_F32) flops over the same "
+             "duration and peak: the MFMA work the kernels actually execute.",
+             "- `issued / algorithmic`: MFMA work spent per useful flop. Above 1 where a "
+             "symmetric product computes its diagonal tiles in full and where padding to the "
+             "tile edge adds rows.",
+             "- `MFMA util`: SQ_VALU_MFMA_BUSY_CYCLES / (cycles x 1024 SIMDs), with cycles = "
+             "GRBM_GUI_ACTIVE / 8 (the counter is summed over the 8 XCDs and also covers the "
+             "collection window around the dispatch). The busy cycles are the issued MOPS / 2 "
+             "exactly (one 32x32x16 bf16 MFMA: 64 MOPS, 32 busy cycles), so this is the issued "
+             "work in cycles, not a separate measurement; it differs from `issued frac` only "
+             "by the clock.",
+             "- `clock GHz`: GRBM_GUI_ACTIVE / 8 / duration, an upper bound (collection window).",
+             "- `wait`: SQ_WAIT_ANY / SQ_WAVE_CYCLES; `LDS conflict`: SQ_LDS_BANK_CONFLICT / "
+             "SQ_LDS_IDX_ACTIVE.", "",
+             "| phase | launches | avg us | algorithmic frac | issued frac | issued / algorithmic "
+             "| MFMA util | clock GHz | wait | LDS conflict |",
+             "|---|---|---|---|---|---|---|---|---|---|"]
+    for ph in ("gram", "poly", "apply"):
+        if ph not in cnt:
             continue
-        tot[r["Kernel_Name"]][r["Counter_Name"]] += float(r["Counter_Value"])
-    lines = [f"# SQ counters: {wl_name}", "", f"Command: `{command}`", "",
-             "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x SQ_BUSY_CU_CYCLES): the fraction of "
-             "SIMD cycles, while the CU is busy, in which the matrix core is executing (a "
-             "32x32x16 bf16 MFMA occupies its SIMD for 32 cycles; 1024 flop per SIMD-cycle is "
-             "the nominal peak). Wait = SQ_WAIT_ANY / SQ_WAVE_CYCLES. LDS conflict = "
-             "SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE.", "",
-             "| kernel | phase | MFMA busy | wait | LDS conflict |", "|---|---|---|---|---|"]
-    for name, c in sorted(tot.items(), key=lambda kv: phase_of(kv[0])):
-        busy = c.get("SQ_BUSY_CU_CYCLES", 0.0)
-        mf = c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (4.0 * busy) if busy else 0.0
-        wt = c.get("SQ_WAIT_ANY", 0.0) / c["SQ_WAVE_CYCLES"] if c.get("SQ_WAVE_CYCLES") else 0.0
-        lc = (c.get("SQ_LDS_BANK_CONFLICT", 0.0) / c["SQ_LDS_IDX_ACTIVE"]
-              if c.get("SQ_LDS_IDX_ACTIVE") else 0.0)
-        short = name if len(name) < 70 else name[:67] + "..."
-        lines.append(f"| `{short}` | {phase_of(name)} | {mf:.3f} | {wt:.3f} | {lc:.3f} |")
+        c = cnt[ph]
+        launches = len(n256[ph]) or len(nall[ph])
+        t_ns = sum(dur[ph].values()) / launches
+        issued = 512.0 * (c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) +
+                          c.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0.0)) / launches
+        peak = BF16_PEAK_TFLOPS * 1e12 * t_ns * 1e-9
+        cycles = c.get("GRBM_GUI_ACTIVE", 0.0) / XCDS / launches
+        util = c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / launches / (cycles * SIMDS) if cycles else 0.0
+        clock = cycles / t_ns if t_ns else 0.0
+        wt = c["SQ_WAIT_ANY"] / c["SQ_WAVE_CYCLES"] if c.get("SQ_WAVE_CYCLES") else float("nan")
+        lc = (c["SQ_LDS_BANK_CONFLICT"] / c["SQ_LDS_IDX_ACTIVE"]
+              if c.get("SQ_LDS_IDX_ACTIVE") else float("nan"))
+        lines.append(
+            f"| {ph} | {launches} | {t_ns / 1e3:.1f} | {algo[ph] / peak:.3f} | {issued / peak:.3f} | "
+            f"{issued / algo[ph]:.3f} | {util:.3f} | {clock:.2f} | {wt:.3f} | {lc:.3f} |")
     path = os.path.join(TRAFFIC_DIR, f"sq_{wl_name}.md")
     with open(path, "w") as f:
         f.write("\n".join(lines) + "\n")
@@ -230,11 +277,12 @@ def ns_flops_per_launch(wl):
     return {"gram": gram, "poly": poly, "apply": apply}
 
 
-def cpu_baseline(wl, P, budget_s=10.0):
+def cpu_oracle_times(wl, budget_s=10.0):
     """fp64 oracle on a bounded sample: one Lion step and one Muon step on one
     tensor of every distinct shape, scaled to the whole set by tensor count,
     repeated until about `budget_s` seconds of CPU work (at least once) and
-    averaged over the repetitions, amortised over P."""
+    averaged over the repetitions. Returns (T_lion, T_muon) in seconds per
+    step and a description of the sample."""
     import numpy as np
     import oracle
     try:
@@ -264,7 +312,7 @@ def cpu_baseline(wl, P, budget_s=10.0):
         for t, W, M, G in inputs:
             reps = count[(t.rows, t.cols, t.lion_only)]
             t0 = time.perf_counter()
-            oracle.lionmuon_update(W, G, M, 1, P, wl.beta1, wl.beta2, wl.lr_muon, wl.lr_lion,
+            oracle.lionmuon_update(W, G, M, 1, 2, wl.beta1, wl.beta2, wl.lr_muon, wl.lr_lion,
                                    wl.wd, lion_only=True)
             t1 = time.perf_counter()
             oracle.lionmuon_update(W, G, M, 0, 1, wl.beta1, wl.beta2, wl.lr_muon, wl.lr_lion,
@@ -274,19 +322,190 @@ def cpu_baseline(wl, P, budget_s=10.0):
             t_muon += (t2 - t1) * reps
         rounds += 1
     spent = time.perf_counter() - start
-    t_lion /= rounds
-    t_muon /= rounds
-    if P == 0:
-        amort = t_lion
-    else:
-        amort = ((P - 1) * t_lion + t_muon) / P
-    return {"value": round(amort * 1e3, 1), "unit": "ms/step", "cores": int(cores),
-            "kind": "oracle",
-            "sample": (f"one Lion and one Muon fp64 oracle step on one tensor of each of the "
-                       f"{len(sample)} distinct shapes of {wl.name}, scaled by tensor count, "
-                       f"repeated {rounds}x ({spent:.1f} s of CPU work) and averaged; "
-                       f"Lion {t_lion * 1e3:.0f} ms/step, Muon {t_muon * 1e3:.0f} ms/step, "
+    desc = (f"one Lion and one Muon fp64 oracle step on one tensor of each of the "
+            f"{len(sample)} distinct shapes of {wl.name}, scaled by tensor count, "
+            f"repeated {rounds}x ({spent:.1f} s of CPU work) and averaged")
+    return t_lion / rounds, t_muon / rounds, int(cores), desc
+
+
+def cpu_baseline_for(times, P):
+    """The oracle's amortised ms/step at period P (0 = pure Lion) from the
+    sampled step times of cpu_oracle_times."""
+    t_lion, t_muon, cores, desc = times
+    amort = t_lion if P == 0 else ((P - 1) * t_lion + t_muon) / P
+    return {"value": round(amort * 1e3, 1), "unit": "ms/step", "cores": cores, "kind": "oracle",
+            "sample": (f"{desc}; Lion {t_lion * 1e3:.0f} ms/step, Muon {t_muon * 1e3:.0f} ms/step, "
                        f"amortised over P={P}")}
+
+
+KERNEL_NAMES = {"lion": "lion_kernel", "prep": "prep_kernel", "norm": "norm_kernel",
+                "gram": "ns_gram_kernel<bf16>", "poly": "ns_poly_kernel<bf16>",
+                "apply": "ns_apply_kernel<bf16> (+ ns_apply_last_kernel)",
+                "srank": "srank_pass+reduce+decide"}
+
+
+class Bench:
+    """Device state of one workload and timed runs of the step over it."""
+
+    def __init__(self, torch, lm, wl, n_grad=2):
+        self.torch, self.lm, self.wl = torch, lm, wl
+        self.dev = torch.device("cuda:0")
+        self.params, self.moms, self.grad_sets = workloads.device_state(
+            torch, wl, self.dev, seed=7, warm=True, n_grad=n_grad)
+        lion_only = [t.lion_only for t in wl.tensors]
+        self.lists = [lm.TensorList(self.params, g, self.moms, lion_only) for g in self.grad_sets]
+        self.specs = [(t.rows, t.cols, t.lion_only) for t in wl.tensors]
+        self.stream = torch.cuda.current_stream()
+
+    def close(self):
+        del self.lists, self.params, self.moms, self.grad_sets
+        self.lm.lionmuon_release()
+        self.torch.cuda.synchronize()
+        self.torch.cuda.empty_cache()
+
+    def run(self, t0, n, P, beta1, beta2, cfg, n_lists=None):
+        k_lists = n_lists or len(self.lists)
+        for k in range(n):
+            t = t0 + k
+            self.lm.lionmuon_step_ex(None, None, None, t, P, beta1, beta2, self.wl.wd, cfg,
+                                     stream=self.stream, tensors=self.lists[t % k_lists])
+
+    def measure(self, P, steps, warmup, beta1=None, beta2=None, adaptive=0.0, power_steps=5,
+                profile=True, n_lists=None):
+        """Amortised ms/step over `steps` timed steps (whole periods, the first
+        a Muon step) after `warmup` untimed ones, with the library's
+        per-launch events off; then, with `profile`, the same number of steps
+        again with the events on for the per-phase times, the split and the
+        roofline of the dominant kernel."""
+        torch, lm, wl = self.torch, self.lm, self.wl
+        beta1 = wl.beta1 if beta1 is None else beta1
+        beta2 = wl.beta2 if beta2 is None else beta2
+        adaptive_on = adaptive > 0.0
+        if P > 1 and steps % P and not adaptive_on:
+            steps += P - steps % P                 # whole periods only
+        cfg = lm.config(ns_precision=wl.ns_precision, lr_muon=wl.lr_muon, lr_lion=wl.lr_lion,
+                        adaptive_alpha=adaptive, adaptive_power_steps=power_steps)
+        cfg_period = lm.config(ns_precision=wl.ns_precision, lr_muon=wl.lr_muon,
+                               lr_lion=wl.lr_lion)
+        info_muon = lm.lionmuon_plan_info(self.specs, 0, 1, cfg_period)
+        info_lion = lm.lionmuon_plan_info(self.specs, 1, 2, cfg_period)
+        info_adaptive = lm.lionmuon_plan_info(self.specs, 0, 0, cfg) if adaptive_on else None
+        stream = self.stream
+        self.run(1, warmup, P, beta1, beta2, cfg, n_lists)
+        torch.cuda.synchronize()
+        t_start = 1 + warmup
+        t_start += (-t_start) % max(P, 1)         # timed region starts on a Muon step
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        self.run(t_start, steps, P, beta1, beta2, cfg, n_lists)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_step = e0.elapsed_time(e1) / steps
+        out = {"ms_per_step": round(ms_step, 4), "steps": steps, "P": None if adaptive_on else P,
+               "beta1": beta1, "beta2": beta2}
+        if not profile:
+            return out
+        lm.lionmuon_profiling_reset()
+        lm.lionmuon_profiling_enable(True)
+        self.run(t_start + steps, steps, P, beta1, beta2, cfg, n_lists)
+        torch.cuda.synchronize()
+        phases = lm.lionmuon_profiling_read()
+        lm.lionmuon_profiling_enable(False)
+        if adaptive_on:
+            dec = torch.zeros(len(wl.tensors), dtype=torch.int32, device=self.dev)
+            lm.lionmuon_step_adaptive(None, None, None, t_start + 2 * steps, beta1, beta2, wl.wd,
+                                      cfg, stream=stream, tensors=self.lists[0], decisions=dec)
+            torch.cuda.synchronize()
+            out["muon_fraction_after_timing"] = round(float(dec.sum().item()) /
+                                                      info_adaptive["n_muon"], 4)
+            n_muon_steps = 0
+        else:
+            n_muon_steps = sum(1 for k in range(steps) if P >= 1 and (t_start + k) % P == 0)
+        n_lion_steps = steps - n_muon_steps
+        flops = ns_flops_per_launch(wl)
+        peak_mfma = BF16_PEAK_TFLOPS if wl.ns_precision == "bf16" else FP32_MFMA_PEAK_TFLOPS
+        ph = {}
+        for name, v in phases.items():
+            if v["launches"] == 0:
+                continue
+            avg = v["ms"] / v["launches"]
+            entry = {"launches": v["launches"], "avg_ms": round(avg, 5)}
+            if name in flops and not adaptive_on:   # adaptive: NS work depends on the decisions
+                entry["tflops"] = round(flops[name] / (avg * 1e-3) / 1e12, 1)
+                entry["frac_mfma_peak"] = round(entry["tflops"] / peak_mfma, 4)
+            if name == "srank":
+                entry["gbps"] = round(info_adaptive["srank_bytes"] / (avg * 1e-3) / 1e9, 1)
+                entry["frac_hbm_peak"] = round(entry["gbps"] / HBM_PEAK_GBPS, 4)
+            if name == "lion" and not adaptive_on:
+                # Lion steps update every tensor; Muon steps only the Lion-only ones
+                lion_elems = n_lion_steps * info_lion["lion_elements"]
+                if n_muon_steps and info_muon["lion_elements"]:
+                    lion_elems += n_muon_steps * info_muon["lion_elements"]
+                bytes_launch = 20.0 * lion_elems / v["launches"]
+                entry["gbps"] = round(bytes_launch / (avg * 1e-3) / 1e9, 1)
+                entry["frac_hbm_peak"] = round(entry["gbps"] / HBM_PEAK_GBPS, 4)
+            if name == "prep" and not adaptive_on:
+                entry["gbps"] = round(14.0 * info_muon["muon_elements"] / (avg * 1e-3) / 1e9, 1)
+                entry["frac_hbm_peak"] = round(entry["gbps"] / HBM_PEAK_GBPS, 4)
+            ph[name] = entry
+        out["phases"] = ph
+        ns_ms = sum(phases[p]["ms"] for p in ("gram", "poly", "apply"))
+        if n_muon_steps:
+            out["ns_tflops"] = round(info_muon["ns_flops"] * n_muon_steps / (ns_ms * 1e-3) / 1e12, 1)
+            out["ns_frac_mfma_peak"] = round(out["ns_tflops"] / peak_mfma, 4)
+            out["ns_tflops_dense_convention"] = round(
+                info_muon["ns_flops_dense"] * n_muon_steps / (ns_ms * 1e-3) / 1e12, 1)
+            out["ns_ms_per_muon_step"] = round(ns_ms / n_muon_steps, 4)
+        if not adaptive_on:
+            # time split of the two step kinds and the amortisation cross-check
+            # ((P-1) T_lion + T_muon) / P against the measured ms/step
+            lion_ms = phases["lion"]["ms"]
+            muon_ms = sum(phases[p]["ms"] for p in ("prep", "norm", "gram", "poly", "apply"))
+            split = {}
+            if n_lion_steps:
+                lion_only_ms = 0.0
+                if n_muon_steps and info_muon["lion_elements"] and phases["lion"]["launches"]:
+                    # Lion-only tensors on Muon steps: pro rata by element count
+                    per_elem = lion_ms / (n_lion_steps * info_lion["lion_elements"]
+                                          + n_muon_steps * info_muon["lion_elements"])
+                    lion_only_ms = per_elem * n_muon_steps * info_muon["lion_elements"]
+                split["t_lion_ms"] = round((lion_ms - lion_only_ms) / n_lion_steps, 4)
+                muon_ms += lion_only_ms
+            if n_muon_steps:
+                split["t_muon_ms"] = round(muon_ms / n_muon_steps, 4)
+            if len(split) == 2 or P in (0, 1):
+                tl, tm = split.get("t_lion_ms", 0.0), split.get("t_muon_ms", 0.0)
+                split["amortised_from_split_ms"] = round(
+                    tl if P == 0 else ((P - 1) * tl + tm) / P, 4)
+            out["split"] = split
+        if "lion" in ph and "gbps" in ph["lion"]:
+            out["lion_gbps"] = ph["lion"]["gbps"]
+            out["lion_frac_hbm_peak"] = ph["lion"]["frac_hbm_peak"]
+        # dominant kernel: most total time in the timed region
+        dom = max((p for p in phases if phases[p]["launches"]), key=lambda p: phases[p]["ms"])
+        d = ph[dom]
+        if "tflops" in d:
+            roof = {"kernel": KERNEL_NAMES[dom], "bound": "mfma", "achieved": d["tflops"],
+                    "peak": peak_mfma, "unit": "TFLOP/s", "frac": d["frac_mfma_peak"]}
+        elif "gbps" in d:
+            roof = {"kernel": KERNEL_NAMES[dom], "bound": "hbm", "achieved": d["gbps"],
+                    "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": d["frac_hbm_peak"]}
+        else:
+            roof = {"kernel": KERNEL_NAMES[dom], "bound": "hbm", "achieved": None,
+                    "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": None}
+        roof["avg_launch_ms"] = d["avg_ms"]
+        roof["traffic"] = load_traffic(wl.name + ("-adaptive" if adaptive_on else ""), dom)
+        out["roofline"] = roof
+        return out
+
+
+def workload_config(wl, info):
+    return {"workload": wl.name, "n_tensors": len(wl.tensors), "elements": wl.numel,
+            "muon_elements": info["muon_elements"], "ns_precision": wl.ns_precision,
+            "ns_steps": 5, "gradients": wl.grad_dist,
+            "state": "fp32 W, M, G; " + ("bf16 MFMA Newton-Schulz with fp32 accumulation"
+                                         if wl.ns_precision == "bf16"
+                                         else "fp32 MFMA Newton-Schulz")}
 
 
 def main():
@@ -300,6 +519,10 @@ def main():
     ap.add_argument("--adaptive", type=float, default=0.0, metavar="ALPHA",
                     help="stable-rank rule of Appendix G with this alpha instead of the period")
     ap.add_argument("--power-steps", type=int, default=5, help="power-iteration steps (adaptive)")
+    ap.add_argument("--single", action="store_true",
+                    help="only the selected workload and period (no other configurations)")
+    ap.add_argument("--grad-sets", type=int, default=2,
+                    help="gradient sets the steps rotate through (1 = fixed addresses)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without per-launch events (no roofline object)")
@@ -310,8 +533,8 @@ def main():
                     help="write profiles/traffic_<workload>.json from rocprofv3 counter CSVs")
     ap.add_argument("--trace-summary", metavar="KERNEL_STATS_CSV",
                     help="write profiles/kernel_trace_<workload>.md from a rocprofv3 stats CSV")
-    ap.add_argument("--sq-summary", metavar="SQ_CSV",
-                    help="write profiles/sq_<workload>.md from a rocprofv3 SQ counter CSV")
+    ap.add_argument("--sq-summary", nargs=1, metavar="SQ_CSV",
+                    help="write profiles/sq_<workload>.md from one rocprofv3 SQ counter pass")
     ap.add_argument("--command", default="", help="profiling command recorded in summaries")
     args = ap.parse_args()
     # profiles of the adaptive variant are kept apart from the periodic step's
@@ -345,171 +568,116 @@ def main():
     import torch
     from paper_2605_19811_amd import lionmuon as lm
 
+    def log(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    profile = not args.no_profile
     wl = workloads.get(args.workload)
     P = 1 if args.pure_muon else args.P
-    beta1, beta2 = (0.9, 0.9) if args.pure_muon else (wl.beta1, wl.beta2)
+    beta = (0.9, 0.9) if args.pure_muon else (None, None)
     adaptive = args.adaptive > 0.0
-    steps = args.steps
-    if P > 1 and steps % P and not adaptive:
-        steps += P - steps % P                 # whole periods only
-    dev = torch.device("cuda:0")
-    params, moms, grad_sets = workloads.device_state(torch, wl, dev, seed=7, warm=True, n_grad=2)
-    lion_only = [t.lion_only for t in wl.tensors]
-    lists = [lm.TensorList(params, g, moms, lion_only) for g in grad_sets]
-    cfg = lm.config(ns_precision=wl.ns_precision, lr_muon=wl.lr_muon, lr_lion=wl.lr_lion,
-                    adaptive_alpha=args.adaptive, adaptive_power_steps=args.power_steps)
-    cfg_period = lm.config(ns_precision=wl.ns_precision, lr_muon=wl.lr_muon, lr_lion=wl.lr_lion)
-    specs = [(t.rows, t.cols, t.lion_only) for t in wl.tensors]
-    info_muon = lm.lionmuon_plan_info(specs, 0, 1, cfg_period)
-    info_lion = lm.lionmuon_plan_info(specs, 1, 2, cfg_period)
-    info_adaptive = lm.lionmuon_plan_info(specs, 0, 0, cfg) if adaptive else None
-    stream = torch.cuda.current_stream()
-
-    def run(t0, n):
-        for k in range(n):
-            t = t0 + k
-            lm.lionmuon_step_ex(None, None, None, t, P, beta1, beta2, wl.wd, cfg,
-                                stream=stream, tensors=lists[t % 2])
-
-    run(1, args.warmup)
-    torch.cuda.synchronize()
-    t_start = 1 + args.warmup
-    t_start += (-t_start) % max(P, 1)         # timed region starts on a Muon step
-    profile = not args.no_profile
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    run(t_start, steps)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    total_ms = e0.elapsed_time(e1)
-    ms_step = total_ms / steps
-    phases = None
-    if profile:
-        # per-launch times: a second timed region of the same steps (whole
-        # periods, starting on a Muon step) with the library's events on
-        lm.lionmuon_profiling_reset()
-        lm.lionmuon_profiling_enable(True)
-        run(t_start + steps, steps)
-        torch.cuda.synchronize()
-        phases = lm.lionmuon_profiling_read()
-        lm.lionmuon_profiling_enable(False)
-
-    muon_fraction = None
-    if adaptive:
-        # decisions of one further step (after the timed region)
-        dec = torch.zeros(len(wl.tensors), dtype=torch.int32, device=dev)
-        t_next = t_start + (2 if profile else 1) * steps
-        lm.lionmuon_step_adaptive(None, None, None, t_next, beta1, beta2, wl.wd, cfg,
-                                  stream=stream, tensors=lists[0], decisions=dec)
-        torch.cuda.synchronize()
-        muon_fraction = round(float(dec.sum().item()) / info_adaptive["n_muon"], 4)
-        n_muon_steps = 0
-    else:
-        n_muon_steps = sum(1 for k in range(steps) if P >= 1 and (t_start + k) % P == 0)
-    n_lion_steps = steps - n_muon_steps
+    log(f"{wl.name} P={P}{' adaptive' if adaptive else ''}")
+    b = Bench(torch, lm, wl, n_grad=max(1, args.grad_sets))
+    res = b.measure(P, args.steps, args.warmup, beta[0], beta[1], args.adaptive,
+                    args.power_steps, profile)
+    info = lm.lionmuon_plan_info(b.specs, 0, 1, lm.config(ns_precision=wl.ns_precision))
+    b.close()
     out = {
         "metric": "amortised optimizer-step ms per period P (LionMuon step, 1 GPU)",
-        "value": round(ms_step, 4),
+        "value": res["ms_per_step"],
         "unit": "ms/step",
         "n_gpus": 1,
-        "steps": steps,
+        "steps": res["steps"],
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4),
+        "ms_per_step": res["ms_per_step"],
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16" if wl.ns_precision == "bf16" else "f32",
         "data": "synthetic (seeded gradients of the workload's shapes; random-init weights)",
-        "config": {"workload": wl.name, "P": None if adaptive else P, "beta1": beta1,
-                   "beta2": beta2,
-                   "n_tensors": len(wl.tensors), "elements": wl.numel,
-                   "muon_elements": info_muon["muon_elements"],
-                   "ns_precision": wl.ns_precision, "ns_steps": 5,
-                   "state": "fp32 W, M, G; bf16 MFMA Newton-Schulz with fp32 accumulation"},
+        "config": dict(workload_config(wl, info), P=res["P"], beta1=res["beta1"],
+                       beta2=res["beta2"], grad_sets=args.grad_sets),
     }
     if adaptive:
         out["metric"] = "optimizer-step ms (adaptive LionMuon step, Appendix G rule, 1 GPU)"
         out["config"].update({"rule": "adaptive stable rank", "alpha": args.adaptive,
                               "power_steps": args.power_steps,
-                              "muon_fraction_after_timing": muon_fraction})
-    if phases is not None:
-        flops = ns_flops_per_launch(wl)
-        ph = {}
-        for name, v in phases.items():
-            if v["launches"] == 0:
-                continue
-            avg = v["ms"] / v["launches"]
-            entry = {"launches": v["launches"], "avg_ms": round(avg, 5)}
-            if name in flops and not adaptive:   # adaptive: NS work depends on the decisions
-                entry["tflops"] = round(flops[name] / (avg * 1e-3) / 1e12, 1)
-                entry["frac_bf16_peak"] = round(entry["tflops"] / BF16_PEAK_TFLOPS, 4)
-            if name == "srank":
-                entry["gbps"] = round(info_adaptive["srank_bytes"] / (avg * 1e-3) / 1e9, 1)
-                entry["frac_hbm_peak"] = round(entry["gbps"] / HBM_PEAK_GBPS, 4)
-            if name == "lion" and not adaptive:
-                # Lion steps update every tensor; Muon steps only the Lion-only ones
-                lion_elems = n_lion_steps * info_lion["lion_elements"]
-                if n_muon_steps and info_muon["lion_elements"]:
-                    lion_elems += n_muon_steps * info_muon["lion_elements"]
-                bytes_launch = 20.0 * lion_elems / v["launches"]
-                entry["gbps"] = round(bytes_launch / (avg * 1e-3) / 1e9, 1)
-                entry["frac_hbm_peak"] = round(entry["gbps"] / HBM_PEAK_GBPS, 4)
-            ph[name] = entry
-        out["phases"] = ph
-        ns_ms = sum(phases[p]["ms"] for p in ("gram", "poly", "apply"))
-        if n_muon_steps:
-            out["ns_tflops"] = round(info_muon["ns_flops"] * n_muon_steps / (ns_ms * 1e-3) / 1e12, 1)
-            out["ns_frac_bf16_peak"] = round(out["ns_tflops"] / BF16_PEAK_TFLOPS, 4)
-            out["ns_tflops_dense_convention"] = round(
-                info_muon["ns_flops_dense"] * n_muon_steps / (ns_ms * 1e-3) / 1e12, 1)
-            out["ns_ms_per_muon_step"] = round(ns_ms / n_muon_steps, 4)
-        if not adaptive:
-            # time split of the two step kinds and the amortisation cross-check
-            # ((P-1) T_lion + T_muon) / P against the measured ms/step
-            lion_ms = phases["lion"]["ms"]
-            muon_ms = sum(phases[p]["ms"] for p in ("prep", "norm", "gram", "poly", "apply"))
-            split = {}
-            if n_lion_steps:
-                lion_only_ms = 0.0
-                if n_muon_steps and info_muon["lion_elements"] and phases["lion"]["launches"]:
-                    # Lion-only tensors on Muon steps: pro rata by element count
-                    per_elem = lion_ms / (n_lion_steps * info_lion["lion_elements"]
-                                          + n_muon_steps * info_muon["lion_elements"])
-                    lion_only_ms = per_elem * n_muon_steps * info_muon["lion_elements"]
-                split["t_lion_ms"] = round((lion_ms - lion_only_ms) / n_lion_steps, 4)
-                muon_ms += lion_only_ms
-            if n_muon_steps:
-                split["t_muon_ms"] = round(muon_ms / n_muon_steps, 4)
-            if len(split) == 2 or P in (0, 1):
-                tl, tm = split.get("t_lion_ms", 0.0), split.get("t_muon_ms", 0.0)
-                split["amortised_from_split_ms"] = round(
-                    tl if P == 0 else ((P - 1) * tl + tm) / P, 4)
-            out["split"] = split
-        if "lion" in ph and "gbps" in ph["lion"]:
-            out["lion_gbps"] = ph["lion"]["gbps"]
-            out["lion_frac_hbm_peak"] = ph["lion"]["frac_hbm_peak"]
-        # dominant kernel: most total time in the timed region
-        dom = max((p for p in phases if phases[p]["launches"]), key=lambda p: phases[p]["ms"])
-        d = ph[dom]
-        kernel_names = {"lion": "lion_kernel", "prep": "prep_kernel", "norm": "norm_kernel",
-                        "gram": "ns_gram_kernel<bf16>", "poly": "ns_poly_kernel<bf16>",
-                        "apply": "ns_apply_kernel<bf16> (+ ns_apply_last_kernel)", "srank": "srank_pass+reduce+decide"}
-        if "tflops" in d:
-            roof = {"kernel": kernel_names[dom], "bound": "mfma", "achieved": d["tflops"],
-                    "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": d["frac_bf16_peak"]}
-        elif "gbps" in d:
-            roof = {"kernel": kernel_names[dom], "bound": "hbm", "achieved": d["gbps"],
-                    "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": d["frac_hbm_peak"]}
-        else:
-            roof = {"kernel": kernel_names[dom], "bound": "hbm", "achieved": None,
-                    "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": None}
-        roof["avg_launch_ms"] = d["avg_ms"]
-        roof["traffic"] = load_traffic(prof_name, dom)
-        out["roofline"] = roof
-    if not args.no_cpu_baseline and not adaptive:
-        out["cpu_baseline"] = cpu_baseline(wl, P)
+                              "muon_fraction_after_timing": res.get("muon_fraction_after_timing")})
+    for k in ("phases", "ns_tflops", "ns_frac_mfma_peak", "ns_tflops_dense_convention",
+              "ns_ms_per_muon_step", "split", "lion_gbps", "lion_frac_hbm_peak", "roofline"):
+        if k in res:
+            out[k] = res[k]
+    cpu = not args.no_cpu_baseline and not adaptive
+    if cpu:
+        log("cpu baseline")
+        out["cpu_baseline"] = cpu_baseline_for(cpu_oracle_times(wl, 10.0), P)
+    if not args.single and not adaptive:
+        out["configs"] = other_configs(torch, lm, args, wl.name, P, profile, cpu, log)
     print(json.dumps(out), flush=True)
+
+
+def other_configs(torch, lm, args, main_name, main_P, profile, cpu, log):
+    """Every other configuration the metric names, measured with the same
+    step counts: the 355M and 720M sets at P = 2, the 768 x 768 fp32 case,
+    the 355M period sweep (P = 1, 2, 4, 8, infinity and pure Muon), and the
+    headline set with fixed gradient addresses against four rotating sets."""
+    keep = ("ms_per_step", "steps", "P", "beta1", "beta2", "ns_tflops", "ns_frac_mfma_peak",
+            "ns_tflops_dense_convention", "ns_ms_per_muon_step", "lion_gbps",
+            "lion_frac_hbm_peak", "split", "roofline", "phases")
+    out = {}
+
+    def pick(res):
+        return {k: res[k] for k in keep if k in res}
+
+    for name in ("gpt2-355m", "gpt2-720m", "single768"):
+        if name == main_name:
+            continue
+        wl = workloads.get(name)
+        sweep = name == "gpt2-355m"
+        log(f"{name}{' + period sweep' if sweep else ''}")
+        b = Bench(torch, lm, wl, n_grad=2)
+        info = lm.lionmuon_plan_info(b.specs, 0, 1, lm.config(ns_precision=wl.ns_precision))
+        entry = dict(config=workload_config(wl, info), **pick(b.measure(wl.P, args.steps,
+                                                                        args.warmup,
+                                                                        profile=profile)))
+        runs = {}
+        if sweep:
+            for label, Pp, beta in (("P=1", 1, None), ("P=4", 4, None), ("P=8", 8, None),
+                                    ("P=inf (pure Lion)", 0, None),
+                                    ("pure Muon (P=1, beta1=beta2=0.9)", 1, 0.9)):
+                log(f"{name} {label}")
+                runs[label] = pick(b.measure(Pp, args.steps, args.warmup, beta, beta,
+                                             profile=profile))
+        b.close()
+        if cpu:
+            log(f"{name} cpu baseline")
+            times = cpu_oracle_times(wl, 6.0)
+            entry["cpu_baseline"] = cpu_baseline_for(times, wl.P)
+            for label, r in runs.items():
+                r["cpu_baseline"] = cpu_baseline_for(times, r["P"] or 0)
+        if sweep:
+            runs["P=2"] = {k: entry[k] for k in entry if k != "config"}
+            out["period_sweep_gpt2-355m"] = {
+                "config": entry["config"],
+                "note": "amortised ms/step per period; split = T_lion, T_muon per step kind",
+                "runs": {k: runs[k] for k in ("P=1", "P=2", "P=4", "P=8", "P=inf (pure Lion)",
+                                              "pure Muon (P=1, beta1=beta2=0.9)")}}
+        out[name] = entry
+    # gradient addresses: fixed (one set) against four rotating sets, which
+    # give the library new addresses on every step
+    wl = workloads.get(main_name)
+    log(f"{main_name} fixed vs rotating gradient addresses")
+    b = Bench(torch, lm, wl, n_grad=4)
+    fixed = b.measure(main_P, args.steps, args.warmup, profile=False, n_lists=1)
+    rot = b.measure(main_P, args.steps, args.warmup, profile=False, n_lists=4)
+    b.close()
+    out[f"gradient_addresses_{main_name}"] = {
+        "fixed_ms_per_step": fixed["ms_per_step"], "rotating4_ms_per_step": rot["ms_per_step"],
+        "ratio": round(rot["ms_per_step"] / fixed["ms_per_step"], 4), "steps": fixed["steps"],
+        "note": "same steps with one gradient set (addresses never change) and with four sets "
+                "used in turn (new addresses every step: the library rewrites its per-call "
+                "address table on the stream)"}
+    return out
 
 
 if __name__ == "__main__":

@@ -49,6 +49,16 @@
  *    than the previous user of that workspace first waits (on the device,
  *    without blocking the host) for that user's work. Calls with caller
  *    workspaces may run concurrently on distinct streams.
+ *  - The library caches one device plan (tile lists, descriptors) per list
+ *    signature: step kind, NS precision and scaling, and each tensor's shape,
+ *    flags and 16-byte alignment -- never its address. The tensor addresses
+ *    of a call go to the device as a small per-plan table that is rewritten
+ *    (one asynchronous copy on the call's stream, staged through a pinned
+ *    ring) only when they differ from the previous call's, so callers whose
+ *    gradient buffers move between steps pay no plan rebuild or allocation.
+ *    Up to 16 signatures stay cached; a 17th evicts the least recently used
+ *    (its device memory is freed, which waits for the device).
+ *  - Grids are sized from the device's compute-unit and XCD counts.
  */
 #ifndef LIONMUON_H
 #define LIONMUON_H
@@ -62,7 +72,7 @@
 extern "C" {
 #endif
 
-#define LIONMUON_ABI_VERSION 2
+#define LIONMUON_ABI_VERSION 3
 
 typedef enum lm_status {
   LM_OK = 0,
@@ -127,8 +137,8 @@ typedef struct lm_config {
   int32_t reserved2;        /* must be 0                                          */
   double ns_schedule[16][3];
   /* AdamW for LM_TENSOR_ADAMW tensors: W <- W - adam_lr (mhat/(sqrt(vhat) +
-   * adam_eps) + adam_wd W), bias corrections with AdamW step t + 1.
-   * Defaults (1e-3, 0.8, 0.999, 1e-8, 0). */
+   * adam_eps) + adam_wd W), bias corrections 1/(1 - beta^k) with the AdamW
+   * step count k = adam_step (below). Defaults (1e-3, 0.8, 0.999, 1e-8, 0). */
   double adam_lr, adam_beta1, adam_beta2, adam_eps, adam_wd;
   /* Adaptive Muon / Lion choice (Appendix G): 0 (default) = off, the period
    * P decides; in (0, 1] = threshold alpha of the stable-rank rule, P is then
@@ -136,6 +146,10 @@ typedef struct lm_config {
   double adaptive_alpha;
   int32_t adaptive_power_steps;  /* power-iteration steps k in [0, 64], default 5 */
   int32_t reserved3;             /* must be 0                                      */
+  /* AdamW step count k >= 1 of this call's bias corrections (the first AdamW
+   * step is k = 1). 0 (default): k = t + 1, for callers whose t counts from 0
+   * as in Algorithm 1; a caller counting steps from 1 passes adam_step = t. */
+  int64_t adam_step;
 } lm_config;
 
 #define LM_MAX_NS_SCHEDULE 16
@@ -201,7 +215,9 @@ lm_status lionmuon_step_adaptive(float* const* params, const float* const* grads
 
 /* Device workspace (bytes) a Muon step -- or, with cfg->adaptive_alpha > 0,
  * an adaptive step -- over these tensors needs with cfg (NULL = defaults).
- * A Lion step needs none. Host-only; no HIP call. */
+ * A Lion step needs none. The size depends on shapes, flags and cfg only (not
+ * on the tensors' alignment), so it holds for any buffers of these shapes.
+ * Host-only: no device work. */
 lm_status lionmuon_workspace_bytes(const lm_shape* shapes, int32_t n_tensors,
                                    const lm_config* cfg, size_t* out_bytes);
 
@@ -217,7 +233,9 @@ lm_status lionmuon_ns(const float* X, float* O, int64_t rows, int64_t cols,
                       int32_t batch, const lm_config* cfg, void* workspace,
                       size_t workspace_bytes, hipStream_t stream);
 
-/* Host-side description of the work one step would enqueue (no HIP call).
+/* Host-side description of the work one step would enqueue (no device work;
+ * the tile lists are those of the current device's CU and XCD counts, or of
+ * a full MI355X -- 256 CUs in 8 XCDs -- when no device is present).
  * With cfg->adaptive_alpha > 0, n_muon / muon_elements count the Muon
  * candidates (each takes Muon or Lion on the device), n_lion / lion_elements
  * the tensors that always take the Lion branch. */

@@ -121,9 +121,6 @@ def newton_schulz(G: np.ndarray, steps: int = NS_STEPS, coeffs=QUINTIC,
     return X
 
 
-ADAMW_DEFAULTS = dict(lr=1e-3, beta1=0.8, beta2=0.999, eps=1e-8, wd=0.0)
-
-
 def adamw_update(W, G, m, v, step, lr, beta1, beta2, eps, wd):
     """AdamW with decoupled weight decay (Loshchilov & Hutter), the fallback
     Section 3 names for 1-D parameters (Table 3: betas (0.8, 0.999), lr 1e-3):

@@ -5,6 +5,7 @@
 
 #include <cmath>
 #include <cstring>
+#include <deque>
 #include <list>
 #include <memory>
 #include <mutex>
@@ -35,19 +36,85 @@ lm_status hip_fail(hipError_t e, const char* what) {
 }
 
 // ---------------------------------------------------------------------------
+// Device shape
+// ---------------------------------------------------------------------------
+// Compute units and XCDs of a device, read once per device. Without a
+// device (host-only queries on a machine with no GPU) a full MI355X is
+// assumed: 256 CUs in 8 XCDs.
+std::mutex g_chip_mu;
+std::vector<std::pair<int, lm::ChipShape>> g_chips;
+
+lm::ChipShape chip_of(int device) {
+  std::lock_guard<std::mutex> lock(g_chip_mu);
+  for (const auto& c : g_chips)
+    if (c.first == device) return c.second;
+  lm::ChipShape chip;
+  int cus = 0, xccs = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) == hipSuccess &&
+      cus > 0) {
+    chip.cus = cus;
+    if (hipDeviceGetAttribute(&xccs, hipDeviceAttributeNumberOfXccs, device) != hipSuccess ||
+        xccs < 1)
+      xccs = 1;
+    chip.xcds = std::min(xccs, lm::kMaxXcds);
+    if (chip.cus < chip.xcds) chip.xcds = chip.cus;
+  } else {
+    (void)hipGetLastError();
+  }
+  g_chips.push_back({device, chip});
+  return chip;
+}
+
+// Shape of the current device, or the MI355X default when there is none.
+lm::ChipShape current_chip() {
+  int device = 0;
+  if (hipGetDevice(&device) != hipSuccess) {
+    (void)hipGetLastError();
+    return lm::ChipShape();
+  }
+  return chip_of(device);
+}
+
+// ---------------------------------------------------------------------------
+// Pinned staging ring
+// ---------------------------------------------------------------------------
+// Host-to-device copies of per-call binding tables are staged through one
+// pinned ring. A region is handed out again only after the event recorded
+// behind its copy has completed, which a host that runs no further ahead of
+// the device than the ring's capacity never waits for.
+struct StagingRing {
+  uint8_t* host = nullptr;
+  size_t cap = 0;
+  uint64_t head = 0;                 // bytes handed out so far (monotonic)
+  struct Region {
+    uint64_t start, end;
+    hipEvent_t done;
+  };
+  std::deque<Region> inflight;       // oldest first
+  std::vector<hipEvent_t> pool;
+};
+StagingRing g_ring;
+
+// ---------------------------------------------------------------------------
 // Uploaded plans
 // ---------------------------------------------------------------------------
-// One plan per (device, tensor list, step kind, NS element size, scaling).
-// Its descriptor tables live in one device allocation, filled once from a
-// pinned host copy on the stream of the call that created the plan.
+// One plan per (device, step kind, NS element size, scaling, and the
+// tensors' shapes, flags and 16-byte alignment). Its descriptor tables live in
+// one device allocation, filled once from a pinned host copy on the stream of
+// the call that created the plan. The same allocation holds the plan's
+// binding table (one TensorPtrs per input tensor), rewritten on the call's
+// stream whenever a call brings other tensor addresses than the previous
+// call of the plan.
 struct DevicePlan {
   Plan plan;
   int device = -1;
   std::vector<uint8_t> key;
   void* dev = nullptr;
-  void* host = nullptr;             // pinned staging copy (kept for the plan's life)
-  hipEvent_t uploaded = nullptr;
-  hipStream_t upload_stream = nullptr;
+  void* host = nullptr;             // pinned staging copy of the tables
+  hipEvent_t last_use = nullptr;    // recorded after the last call that used the plan
+  hipStream_t last_stream = nullptr;
+  std::vector<lm::TensorPtrs> bound;   // addresses the device binding holds
+  lm::TensorPtrs* d_bind = nullptr;
   lm::LionTensor* d_lion = nullptr;
   int32_t* d_lion_start = nullptr;
   lm::MuonMat* d_mats = nullptr;
@@ -59,14 +126,14 @@ struct DevicePlan {
   lm::XcdSplit* d_splits = nullptr;   // [precision * 4 + list]
 
   ~DevicePlan() {
-    if (uploaded) (void)hipEventDestroy(uploaded);
+    if (last_use) (void)hipEventDestroy(last_use);
     if (dev) (void)hipFree(dev);
     if (host) (void)hipHostFree(host);
   }
 };
 
 constexpr size_t kMaxPlans = 16;
-std::mutex g_mu;                                      // plans, workspace, profiling
+std::mutex g_mu;                                      // plans, workspace, profiling, ring
 std::list<std::shared_ptr<DevicePlan>> g_plans;       // most recent first
 
 // The library-owned workspace of a device. Calls that use it are serialised
@@ -117,25 +184,175 @@ void place(std::vector<T>& v, size_t* off, std::vector<std::pair<size_t, std::pa
   *off = align256(*off + v.size() * sizeof(T));
 }
 
+// The call's tensor addresses, one entry per input tensor.
+std::vector<lm::TensorPtrs> binding_of(const TensorIn* x, int32_t n) {
+  std::vector<lm::TensorPtrs> b(size_t(n > 0 ? n : 0));
+  for (int32_t i = 0; i < n; ++i) {
+    b[size_t(i)].w = x[i].w;
+    b[size_t(i)].g = x[i].g;
+    b[size_t(i)].m = x[i].m;
+    b[size_t(i)].v = (x[i].flags & lm::kFlagAdamW) ? x[i].v : nullptr;
+  }
+  return b;
+}
+
+bool same_binding(const std::vector<lm::TensorPtrs>& a, const std::vector<lm::TensorPtrs>& b) {
+  return a.size() == b.size() &&
+         (a.empty() || std::memcmp(a.data(), b.data(), a.size() * sizeof(lm::TensorPtrs)) == 0);
+}
+
+// Copy `bytes` from host memory to device memory `dst` on `stream` through
+// the pinned ring (the source may be reused as soon as this returns).
+lm_status stage_upload(void* dst, const void* src, size_t bytes, hipStream_t stream) {
+  StagingRing& r = g_ring;
+  hipError_t e = hipSuccess;
+  const size_t need = (bytes + 63) & ~size_t(63);
+  if (need > r.cap) {
+    // grow: wait for every staged copy, then replace the ring
+    for (auto& reg : r.inflight) {
+      (void)hipEventSynchronize(reg.done);
+      r.pool.push_back(reg.done);
+    }
+    r.inflight.clear();
+    if (r.host) (void)hipHostFree(r.host);
+    r.host = nullptr;
+    r.cap = 0;
+    size_t cap = size_t(1) << 20;
+    while (cap < 4 * need) cap <<= 1;
+    void* h = nullptr;
+    e = hipHostMalloc(&h, cap, hipHostMallocPortable);
+    if (e != hipSuccess) return fail(LM_ERR_OUT_OF_MEMORY, "staging ring: hipHostMalloc failed");
+    r.host = static_cast<uint8_t*>(h);
+    r.cap = cap;
+  }
+  uint64_t s = r.head;
+  if (s % r.cap + need > r.cap) s += r.cap - s % r.cap;   // no region straddles the end
+  while (!r.inflight.empty() && r.inflight.front().start + r.cap < s + need) {
+    e = hipEventSynchronize(r.inflight.front().done);
+    if (e != hipSuccess) return hip_fail(e, "staging ring: hipEventSynchronize");
+    r.pool.push_back(r.inflight.front().done);
+    r.inflight.pop_front();
+  }
+  uint8_t* h = r.host + s % r.cap;
+  std::memcpy(h, src, bytes);
+  e = hipMemcpyAsync(dst, h, bytes, hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "binding upload: hipMemcpyAsync");
+  hipEvent_t ev = nullptr;
+  if (!r.pool.empty()) {
+    ev = r.pool.back();
+    r.pool.pop_back();
+  } else {
+    e = hipEventCreateWithFlags(&ev, hipEventDisableTiming | hipEventDisableSystemFence);
+    if (e != hipSuccess) return hip_fail(e, "staging ring: hipEventCreate");
+  }
+  e = hipEventRecord(ev, stream);
+  if (e != hipSuccess) {
+    r.pool.push_back(ev);
+    return hip_fail(e, "staging ring: hipEventRecord");
+  }
+  r.inflight.push_back({s, s + need, ev});
+  r.head = s + need;
+  return LM_OK;
+}
+
+// Cache key of a list signature: device, step kind, NS precision and
+// scaling, then each tensor's shape, flags and alignment class.
+std::vector<uint8_t> plan_key(int device, const TensorIn* x, int32_t n, lm::StepKind kind,
+                              lm::NsPrecision prec, bool rms02) {
+  std::vector<uint8_t> key;
+  key.reserve(size_t(n) * 24 + 32);
+  const int32_t hdr[5] = {device, static_cast<int32_t>(kind), prec.all_fp32 ? 1 : 0,
+                          prec.bf16_min_side, rms02 ? 1 : 0};
+  append_key(&key, hdr, sizeof(hdr));
+  for (int32_t i = 0; i < n; ++i) {
+    const int64_t dims[2] = {x[i].rows, x[i].cols};
+    const uint32_t fa[2] = {x[i].flags, lm::align_class(x[i])};
+    append_key(&key, dims, sizeof(dims));
+    append_key(&key, fa, sizeof(fa));
+  }
+  return key;
+}
+
+// Device image of a plan's tables and binding: one byte block, each table
+// 256-byte aligned at its offset.
+struct TableImage {
+  std::vector<uint8_t> bytes;
+  size_t o_bind = 0, o_lion = 0, o_lion_start = 0, o_mats = 0, o_prep = 0, o_sr = 0, o_rd = 0,
+         o_tm = 0, o_splits = 0;
+  size_t o_tasks[2][4] = {};
+};
+
+void pack_tables(Plan& p, std::vector<lm::TensorPtrs>& bind, TableImage* img) {
+  std::vector<std::pair<size_t, std::pair<const void*, size_t>>> parts;
+  size_t off = 0;
+  img->o_bind = off;       place(bind, &off, &parts);
+  img->o_lion = off;       place(p.lion, &off, &parts);
+  img->o_lion_start = off; place(p.lion_block_start, &off, &parts);
+  img->o_mats = off;       place(p.mats, &off, &parts);
+  img->o_prep = off;       place(p.prep_start, &off, &parts);
+  img->o_sr = off;         place(p.sr_tab, &off, &parts);
+  img->o_rd = off;         place(p.rd_start, &off, &parts);
+  img->o_tm = off;         place(p.tensor_mat, &off, &parts);
+  std::vector<lm::XcdSplit> splits;
+  for (int pr = 0; pr < 2; ++pr) {
+    img->o_tasks[pr][0] = off; place(p.gram[pr], &off, &parts);
+    img->o_tasks[pr][1] = off; place(p.poly[pr], &off, &parts);
+    img->o_tasks[pr][2] = off; place(p.apply[pr], &off, &parts);
+    img->o_tasks[pr][3] = off; place(p.apply_tail[pr], &off, &parts);
+    splits.push_back(p.gram_split[pr]);
+    splits.push_back(p.poly_split[pr]);
+    splits.push_back(p.apply_split[pr]);
+    splits.push_back(p.apply_tail_split[pr]);
+  }
+  img->o_splits = off;     place(splits, &off, &parts);
+  img->bytes.assign(std::max<size_t>(off, 256), 0);
+  for (const auto& part : parts)
+    if (part.second.second)
+      std::memcpy(img->bytes.data() + part.first, part.second.first, part.second.second);
+}
+
+// Point a plan's device table pointers into the image placed at `base`.
+void point_tables(DevicePlan* dp, uint8_t* base, const TableImage& img) {
+  dp->d_bind = reinterpret_cast<lm::TensorPtrs*>(base + img.o_bind);
+  dp->d_lion = reinterpret_cast<lm::LionTensor*>(base + img.o_lion);
+  dp->d_lion_start = reinterpret_cast<int32_t*>(base + img.o_lion_start);
+  dp->d_mats = reinterpret_cast<lm::MuonMat*>(base + img.o_mats);
+  dp->d_prep_start = reinterpret_cast<int32_t*>(base + img.o_prep);
+  dp->d_sr_tab = reinterpret_cast<lm::SrBlock*>(base + img.o_sr);
+  dp->d_rd_start = reinterpret_cast<int32_t*>(base + img.o_rd);
+  dp->d_tensor_mat = reinterpret_cast<int32_t*>(base + img.o_tm);
+  for (int pr = 0; pr < 2; ++pr)
+    for (int st4 = 0; st4 < 4; ++st4)
+      dp->d_tasks[pr][st4] = reinterpret_cast<lm::GemmTask*>(base + img.o_tasks[pr][st4]);
+  dp->d_splits = reinterpret_cast<lm::XcdSplit*>(base + img.o_splits);
+}
+
+// Find or build the plan of this list signature and make its tables and
+// binding ready on `stream`: the stream first waits (on the device) for the
+// plan's last user when that ran on another stream, and the binding is
+// rewritten when the call's addresses differ from those it holds.
 lm_status get_plan(const TensorIn* x, int32_t n, lm::StepKind kind, lm::NsPrecision prec,
                    bool rms02, hipStream_t stream, std::shared_ptr<DevicePlan>* out) {
   int device = 0;
   hipError_t e = hipGetDevice(&device);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-  std::vector<uint8_t> key;
-  key.reserve(size_t(n) * sizeof(TensorIn) + 16);
-  const int32_t hdr[5] = {device, static_cast<int32_t>(kind), prec.all_fp32 ? 1 : 0,
-                          prec.bf16_min_side, rms02 ? 1 : 0};
-  append_key(&key, hdr, sizeof(hdr));
-  append_key(&key, x, size_t(n) * sizeof(TensorIn));
+  std::vector<uint8_t> key = plan_key(device, x, n, kind, prec, rms02);
+  std::vector<lm::TensorPtrs> bind = binding_of(x, n);
   for (auto it = g_plans.begin(); it != g_plans.end(); ++it) {
     if ((*it)->key == key) {
       g_plans.splice(g_plans.begin(), g_plans, it);
-      *out = g_plans.front();
-      if ((*out)->upload_stream != stream) {
-        e = hipStreamWaitEvent(stream, (*out)->uploaded, 0);
+      DevicePlan& dp = *g_plans.front();
+      if (dp.last_use && dp.last_stream != stream) {
+        e = hipStreamWaitEvent(stream, dp.last_use, 0);
         if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
       }
+      if (!same_binding(dp.bound, bind)) {
+        lm_status s = stage_upload(dp.d_bind, bind.data(), bind.size() * sizeof(lm::TensorPtrs),
+                                   stream);
+        if (s != LM_OK) return s;
+        dp.bound.swap(bind);
+      }
+      *out = g_plans.front();
       return LM_OK;
     }
   }
@@ -143,62 +360,39 @@ lm_status get_plan(const TensorIn* x, int32_t n, lm::StepKind kind, lm::NsPrecis
   dp->device = device;
   dp->key = std::move(key);
   std::string err;
-  Status st = lm::build_plan(x, n, kind, prec, rms02, &dp->plan, &err);
+  Status st = lm::build_plan(x, n, kind, prec, rms02, chip_of(device), &dp->plan, &err);
   if (st != Status::kOk) return fail(to_c(st), err);
-  Plan& p = dp->plan;
-  std::vector<std::pair<size_t, std::pair<const void*, size_t>>> parts;
-  size_t off = 0;
-  const size_t o_lion = off;       place(p.lion, &off, &parts);
-  const size_t o_lion_start = off; place(p.lion_block_start, &off, &parts);
-  const size_t o_mats = off;       place(p.mats, &off, &parts);
-  const size_t o_prep = off;       place(p.prep_start, &off, &parts);
-  const size_t o_sr = off;         place(p.sr_tab, &off, &parts);
-  const size_t o_rd = off;         place(p.rd_start, &off, &parts);
-  const size_t o_tm = off;         place(p.tensor_mat, &off, &parts);
-  size_t o_tasks[2][4];
-  std::vector<lm::XcdSplit> splits;
-  for (int pr = 0; pr < 2; ++pr) {
-    o_tasks[pr][0] = off; place(p.gram[pr], &off, &parts);
-    o_tasks[pr][1] = off; place(p.poly[pr], &off, &parts);
-    o_tasks[pr][2] = off; place(p.apply[pr], &off, &parts);
-    o_tasks[pr][3] = off; place(p.apply_tail[pr], &off, &parts);
-    splits.push_back(p.gram_split[pr]);
-    splits.push_back(p.poly_split[pr]);
-    splits.push_back(p.apply_split[pr]);
-    splits.push_back(p.apply_tail_split[pr]);
-  }
-  const size_t o_splits = off;     place(splits, &off, &parts);
-  const size_t total = std::max<size_t>(off, 256);
+  TableImage img;
+  pack_tables(dp->plan, bind, &img);
+  const size_t total = img.bytes.size();
   e = hipMalloc(&dp->dev, total);
   if (e != hipSuccess) return fail(LM_ERR_OUT_OF_MEMORY, "plan tables: hipMalloc failed");
   e = hipHostMalloc(&dp->host, total, hipHostMallocDefault);
   if (e != hipSuccess) return fail(LM_ERR_OUT_OF_MEMORY, "plan tables: hipHostMalloc failed");
-  std::memset(dp->host, 0, total);
-  for (const auto& part : parts)
-    if (part.second.second) std::memcpy(static_cast<uint8_t*>(dp->host) + part.first,
-                                        part.second.first, part.second.second);
+  std::memcpy(dp->host, img.bytes.data(), total);
   e = hipMemcpyAsync(dp->dev, dp->host, total, hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return hip_fail(e, "plan tables: hipMemcpyAsync");
-  e = hipEventCreateWithFlags(&dp->uploaded, hipEventDisableTiming);
-  if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
-  e = hipEventRecord(dp->uploaded, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
-  dp->upload_stream = stream;
-  uint8_t* base = static_cast<uint8_t*>(dp->dev);
-  dp->d_lion = reinterpret_cast<lm::LionTensor*>(base + o_lion);
-  dp->d_lion_start = reinterpret_cast<int32_t*>(base + o_lion_start);
-  dp->d_mats = reinterpret_cast<lm::MuonMat*>(base + o_mats);
-  dp->d_prep_start = reinterpret_cast<int32_t*>(base + o_prep);
-  dp->d_sr_tab = reinterpret_cast<lm::SrBlock*>(base + o_sr);
-  dp->d_rd_start = reinterpret_cast<int32_t*>(base + o_rd);
-  dp->d_tensor_mat = reinterpret_cast<int32_t*>(base + o_tm);
-  for (int pr = 0; pr < 2; ++pr)
-    for (int st4 = 0; st4 < 4; ++st4)
-      dp->d_tasks[pr][st4] = reinterpret_cast<lm::GemmTask*>(base + o_tasks[pr][st4]);
-  dp->d_splits = reinterpret_cast<lm::XcdSplit*>(base + o_splits);
+  dp->bound.swap(bind);
+  point_tables(dp.get(), static_cast<uint8_t*>(dp->dev), img);
   g_plans.push_front(dp);
-  while (g_plans.size() > kMaxPlans) g_plans.pop_back();   // hipFree waits for the device
+  // Plans are keyed by shapes, so eviction happens only when more than
+  // kMaxPlans list signatures alternate; hipFree waits for the device.
+  while (g_plans.size() > kMaxPlans) g_plans.pop_back();
   *out = dp;
+  return LM_OK;
+}
+
+// Record the end of this call's use of a plan (device scope: the event only
+// orders later work on the same device).
+lm_status release_plan(DevicePlan* dp, hipStream_t stream) {
+  hipError_t e = hipSuccess;
+  if (!dp->last_use) {
+    e = hipEventCreateWithFlags(&dp->last_use, hipEventDisableTiming | hipEventDisableSystemFence);
+    if (e != hipSuccess) return hip_fail(e, "plan: hipEventCreate");
+  }
+  e = hipEventRecord(dp->last_use, stream);
+  if (e != hipSuccess) return hip_fail(e, "plan: hipEventRecord");
+  dp->last_stream = stream;
   return LM_OK;
 }
 
@@ -268,8 +462,8 @@ struct Timer {
 lm::StepConsts step_consts(double beta1, double beta2, double wd, double lr_muon,
                            double lr_lion, double eps, const lm_config* cfg, int64_t t) {
   lm::StepConsts k{};
-  if (cfg) {                       // AdamW; the AdamW step count is t + 1
-    const double step = double(t) + 1.0;
+  if (cfg) {   // AdamW: step count adam_step, or t + 1 (t counts from 0) when it is 0
+    const double step = cfg->adam_step > 0 ? double(cfg->adam_step) : double(t) + 1.0;
     k.adam_lr = float(cfg->adam_lr);
     k.adam_b1 = float(cfg->adam_beta1);
     k.adam_omb1 = float(1.0 - cfg->adam_beta1);
@@ -309,6 +503,7 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
     decide = reinterpret_cast<int32_t*>(wsb + p.ws_decide_off);
     lm::SrankLaunch sl;
     sl.mats = dp.d_mats;
+    sl.bind = dp.d_bind;
     sl.tab = dp.d_sr_tab;
     sl.rd_start = dp.d_rd_start;
     sl.tensor_mat = dp.d_tensor_mat;
@@ -352,6 +547,7 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
   if (!p.lion.empty()) {
     lm::LionLaunch l;
     l.tensors = dp.d_lion;
+    l.bind = dp.d_bind;
     l.block_start = dp.d_lion_start;
     l.n_tensors = int32_t(p.lion.size());
     l.n_blocks = p.lion_block_start.back();
@@ -367,6 +563,7 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
   float* rscale = reinterpret_cast<float*>(wsb + p.ws_rscale_off);
   lm::PrepLaunch pl;
   pl.mats = dp.d_mats;
+  pl.bind = dp.d_bind;
   pl.prep_start = dp.d_prep_start;
   pl.n_mats = int32_t(p.mats.size());
   pl.n_tiles = p.prep_start.back();
@@ -389,6 +586,8 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
   }
   lm::GemmLaunch gl;
   gl.mats = dp.d_mats;
+  gl.bind = dp.d_bind;
+  gl.chip = p.chip;
   gl.ws = ws;
   gl.rscale = rscale;
   gl.store_o = store_o ? 1 : 0;
@@ -457,6 +656,7 @@ lm_status check_config(const lm_config* cfg) {
   if (cfg->adaptive_power_steps < 0 || cfg->adaptive_power_steps > 64)
     return fail(LM_ERR_INVALID_ARGUMENT, "adaptive_power_steps must lie in [0, 64]");
   if (cfg->reserved3 != 0) return fail(LM_ERR_INVALID_ARGUMENT, "lm_config reserved fields must be 0");
+  if (cfg->adam_step < 0) return fail(LM_ERR_INVALID_ARGUMENT, "adam_step must be >= 0 (0: t + 1)");
   if (cfg->ns_schedule_steps != 0) {
     if (cfg->ns_schedule_steps != cfg->ns_steps || cfg->ns_steps > LM_MAX_NS_SCHEDULE)
       return fail(LM_ERR_INVALID_ARGUMENT,
@@ -543,7 +743,11 @@ lm_status step_impl(float* const* params, const float* const* grads, float* cons
   }
   s = enqueue(*dp, step_consts(beta1, beta2, wd, cfg->lr_muon, cfg->lr_lion, cfg->ns_eps, cfg, t),
               *cfg, ws, false, aout, stream);
-  if (ow) {                              // also after a partial enqueue
+  {                                      // also after a partial enqueue
+    const lm_status r = release_plan(dp.get(), stream);
+    if (s == LM_OK) s = r;
+  }
+  if (ow) {
     const lm_status r = release_workspace(ow, stream);
     if (s == LM_OK) s = r;
   }
@@ -579,6 +783,7 @@ void lionmuon_config_default(lm_config* cfg) {
   cfg->adaptive_alpha = 0.0;
   cfg->adaptive_power_steps = 5;
   cfg->reserved3 = 0;
+  cfg->adam_step = 0;
 }
 
 lm_status lionmuon_step(float* const* params, const float* const* grads, float* const* momentum,
@@ -666,7 +871,7 @@ lm_status lionmuon_plan_info(const lm_shape* shapes, int32_t n, int64_t t, int32
   if (st != Status::kOk) return fail(to_c(st), err);
   Plan p;
   st = lm::build_plan(x.data(), n, step_kind(*cfg, t, P), precision_of(*cfg),
-                      cfg->ns_scale_mode == LM_NS_SCALE_RMS02, &p, &err);
+                      cfg->ns_scale_mode == LM_NS_SCALE_RMS02, current_chip(), &p, &err);
   if (st != Status::kOk) return fail(to_c(st), err);
   std::memset(out, 0, sizeof(*out));
   out->n_tensors = p.n_tensors;
@@ -748,6 +953,10 @@ lm_status lionmuon_ns(const float* X, float* O, int64_t rows, int64_t cols, int3
   }
   s = enqueue(*dp, step_consts(0.0, 0.0, 0.0, 0.0, 0.0, cfg->ns_eps, nullptr, 0), *cfg, ws, true,
               AdaptiveOut(), stream);
+  {
+    const lm_status r = release_plan(dp.get(), stream);
+    if (s == LM_OK) s = r;
+  }
   if (ow) {
     const lm_status r = release_workspace(ow, stream);
     if (s == LM_OK) s = r;
@@ -795,6 +1004,16 @@ lm_status lionmuon_profiling_reset(void) {
 void lionmuon_release(void) {
   std::lock_guard<std::mutex> lock(g_mu);
   g_plans.clear();
+  for (auto& reg : g_ring.inflight) {
+    (void)hipEventSynchronize(reg.done);
+    g_ring.pool.push_back(reg.done);
+  }
+  g_ring.inflight.clear();
+  for (hipEvent_t e : g_ring.pool) (void)hipEventDestroy(e);
+  g_ring.pool.clear();
+  if (g_ring.host) (void)hipHostFree(g_ring.host);
+  g_ring.host = nullptr;
+  g_ring.cap = 0;
   for (auto& w : g_ws) {
     if (w.ptr) (void)hipFree(w.ptr);
     if (w.done) (void)hipEventDestroy(w.done);

@@ -19,6 +19,7 @@ struct StepConsts {
 
 struct LionLaunch {
   const LionTensor* tensors;     // device
+  const TensorPtrs* bind;        // device: the call's tensor addresses
   const int32_t* block_start;    // device, n_tensors + 1
   int32_t n_tensors;
   int32_t n_blocks;
@@ -30,6 +31,7 @@ hipError_t launch_lion(const LionLaunch& a, hipStream_t stream);
 
 struct PrepLaunch {
   const MuonMat* mats;           // device
+  const TensorPtrs* bind;        // device: the call's tensor addresses
   const int32_t* prep_start;     // device, n_mats + 1
   int32_t n_mats;
   int32_t n_tiles;
@@ -48,9 +50,11 @@ enum GemmMode { kGram = 0, kPoly = 1, kApply = 2 };
 
 struct GemmLaunch {
   const MuonMat* mats;           // device
+  const TensorPtrs* bind;        // device: the call's tensor addresses (last apply: W)
+  ChipShape chip;                // CUs and XCDs: grid of the persistent apply
   const GemmTask* tasks;         // device, grouped by XCD segment
   const XcdSplit* split;         // device: one segment of `tasks` per XCD
-  int32_t max_count;             // largest segment (host copy): grid = 8 x max_count
+  int32_t max_count;             // largest segment (host copy): grid = xcds x max_count
   void* ws;
   const float* rscale;
   int32_t src;                   // ping-pong index of the current X, X^T
@@ -69,6 +73,7 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& a, hipStream_t stream);
 // momentum by power iteration on the Gram matrix of its short side, in fp64.
 struct SrankLaunch {
   const MuonMat* mats;           // device
+  const TensorPtrs* bind;        // device: the call's tensor addresses (M)
   const SrBlock* tab;            // device: pass workgroups, grouped by class
   const int32_t* rd_start;       // device, n_mats + 1: reduction chunks
   const int32_t* tensor_mat;     // device, n_inputs: candidate index or -1

@@ -59,6 +59,7 @@ __device__ __forceinline__ float wave_sum(float v) {
 // ---------------------------------------------------------------------------
 struct LionArgs {
   const LionTensor* tensors;
+  const TensorPtrs* bind;
   const int32_t* block_start;
   const int32_t* decide;
   int32_t n_tensors;
@@ -88,13 +89,14 @@ __global__ __launch_bounds__(256) void lion_kernel(LionArgs a) {
   const int ti = find_segment(a.block_start, a.n_tensors, b);
   const LionTensor t = a.tensors[ti];
   if (t.gate >= 0 && a.decide[t.gate] != 0) return;   // the candidate took Muon
+  const TensorPtrs tp = a.bind[t.tensor];
   const int64_t base = int64_t(b - a.block_start[ti]) * kLionBlockElems;
   const int tid = threadIdx.x;
   const bool full = t.vec_ok && base + kLionBlockElems <= t.numel;
   if (full && !t.adamw) {
-    f32x4* w4 = reinterpret_cast<f32x4*>(t.w + base);
-    const f32x4* g4 = reinterpret_cast<const f32x4*>(t.g + base);
-    f32x4* m4 = reinterpret_cast<f32x4*>(t.m + base);
+    f32x4* w4 = reinterpret_cast<f32x4*>(tp.w + base);
+    const f32x4* g4 = reinterpret_cast<const f32x4*>(tp.g + base);
+    f32x4* m4 = reinterpret_cast<f32x4*>(tp.m + base);
     f32x4 w[kLionUnroll], g[kLionUnroll], m[kLionUnroll];
     // every stream is touched once per step: non-temporal loads and stores
     // (measured: pure-Lion steps 7-8% faster than with cached W, M loads)
@@ -122,10 +124,10 @@ __global__ __launch_bounds__(256) void lion_kernel(LionArgs a) {
       __builtin_nontemporal_store(m[u], &m4[i]);
     }
   } else if (full) {
-    f32x4* w4 = reinterpret_cast<f32x4*>(t.w + base);
-    const f32x4* g4 = reinterpret_cast<const f32x4*>(t.g + base);
-    f32x4* m4 = reinterpret_cast<f32x4*>(t.m + base);
-    f32x4* v4 = reinterpret_cast<f32x4*>(t.v + base);
+    f32x4* w4 = reinterpret_cast<f32x4*>(tp.w + base);
+    const f32x4* g4 = reinterpret_cast<const f32x4*>(tp.g + base);
+    f32x4* m4 = reinterpret_cast<f32x4*>(tp.m + base);
+    f32x4* v4 = reinterpret_cast<f32x4*>(tp.v + base);
 #pragma unroll
     for (int u = 0; u < kLionUnroll; ++u) {
       const int i = tid + 256 * u;
@@ -145,16 +147,16 @@ __global__ __launch_bounds__(256) void lion_kernel(LionArgs a) {
   } else {
     const int64_t end = min(base + int64_t(kLionBlockElems), t.numel);
     for (int64_t i = base + tid; i < end; i += 256) {
-      float w = t.w[i], m = t.m[i];
+      float w = tp.w[i], m = tp.m[i];
       if (t.adamw) {
-        float v = t.v[i];
-        adamw_elem(w, t.g[i], m, v, a);
-        t.v[i] = v;
+        float v = tp.v[i];
+        adamw_elem(w, tp.g[i], m, v, a);
+        tp.v[i] = v;
       } else {
-        lion_elem(w, t.g[i], m, a);
+        lion_elem(w, tp.g[i], m, a);
       }
-      t.w[i] = w;
-      t.m[i] = m;
+      tp.w[i] = w;
+      tp.m[i] = m;
     }
   }
 }
@@ -164,6 +166,7 @@ __global__ __launch_bounds__(256) void lion_kernel(LionArgs a) {
 // ---------------------------------------------------------------------------
 struct PrepArgs {
   const MuonMat* mats;
+  const TensorPtrs* bind;
   const int32_t* prep_start;
   int32_t n_mats;
   void* ws;
@@ -209,6 +212,8 @@ __device__ __forceinline__ void prep_wide(const PrepArgs& a, const MuonMat& mm, 
   constexpr int kPasses = kRows / kRowsPass;
   static_assert(kPasses * kRowsPass == kRows, "whole passes per strip");
   __shared__ float red[4];
+  const float* G = a.bind[mm.tensor].g;
+  float* Mp = a.bind[mm.tensor].m;           // null for the NS hook
   const int local = b - mm.prep_first;
   const int ti = local / mm.prep_tiles_n, tj = local - ti * mm.prep_tiles_n;
   T* X = reinterpret_cast<T*>(static_cast<char*>(a.ws) + mm.off_x[0]);
@@ -224,18 +229,18 @@ __device__ __forceinline__ void prep_wide(const PrepArgs& a, const MuonMat& mm, 
     const bool vec = row_in && mm.vec_ok && q + 3 < mm.cols;
     const int64_t idx = p * mm.cols + q;
     if (vec) {
-      const f32x4 g = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(mm.g + idx));
+      const f32x4 g = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(G + idx));
       gv[0] = g[0]; gv[1] = g[1]; gv[2] = g[2]; gv[3] = g[3];
-      if (mm.m) {
-        const f32x4 m = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(mm.m + idx));
+      if (Mp) {
+        const f32x4 m = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(Mp + idx));
         mv[0] = m[0]; mv[1] = m[1]; mv[2] = m[2]; mv[3] = m[3];
       }
     } else if (row_in) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         if (q + e < mm.cols) {
-          gv[e] = mm.g[idx + e];
-          if (mm.m) mv[e] = mm.m[idx + e];
+          gv[e] = G[idx + e];
+          if (Mp) mv[e] = Mp[idx + e];
         }
       }
     }
@@ -246,14 +251,14 @@ __device__ __forceinline__ void prep_wide(const PrepArgs& a, const MuonMat& mm, 
       mn[e] = fmaf(a.b2, mv[e], a.omb2 * gv[e]);
       ss = fmaf(c[e], c[e], ss);
     }
-    if (mm.m) {
+    if (Mp) {
       if (vec) {
         const f32x4 mv4 = {mn[0], mn[1], mn[2], mn[3]};
-        __builtin_nontemporal_store(mv4, reinterpret_cast<f32x4*>(mm.m + idx));
+        __builtin_nontemporal_store(mv4, reinterpret_cast<f32x4*>(Mp + idx));
       } else if (row_in) {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          if (q + e < mm.cols) mm.m[idx + e] = mn[e];
+          if (q + e < mm.cols) Mp[idx + e] = mn[e];
       }
     }
     store4(X + p * cols_pad + q, c);
@@ -277,6 +282,8 @@ __device__ __forceinline__ void prep_tall(const PrepArgs& a, const MuonMat& mm, 
   static_assert(kTR * (kTC + kPad) * sizeof(T) <= kPrepLdsBytes, "tile fits the LDS block");
   T (*tile)[kTC + kPad] = reinterpret_cast<T (*)[kTC + kPad]>(lds);
   __shared__ float red[4];
+  const float* G = a.bind[mm.tensor].g;
+  float* Mp = a.bind[mm.tensor].m;           // null for the NS hook
   const int local = b - mm.prep_first;
   const int ti = local / mm.prep_tiles_n, tj = local - ti * mm.prep_tiles_n;
   const int64_t rows_pad = mm.l_pad;           // of the original (tall) matrix
@@ -293,18 +300,18 @@ __device__ __forceinline__ void prep_tall(const PrepArgs& a, const MuonMat& mm, 
     const bool vec = row_in && mm.vec_ok && q + 3 < mm.cols;
     const int64_t idx = p * mm.cols + q;
     if (vec) {
-      const f32x4 g = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(mm.g + idx));
+      const f32x4 g = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(G + idx));
       gv[0] = g[0]; gv[1] = g[1]; gv[2] = g[2]; gv[3] = g[3];
-      if (mm.m) {
-        const f32x4 m = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(mm.m + idx));
+      if (Mp) {
+        const f32x4 m = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(Mp + idx));
         mv[0] = m[0]; mv[1] = m[1]; mv[2] = m[2]; mv[3] = m[3];
       }
     } else if (row_in) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         if (q + e < mm.cols) {
-          gv[e] = mm.g[idx + e];
-          if (mm.m) mv[e] = mm.m[idx + e];
+          gv[e] = G[idx + e];
+          if (Mp) mv[e] = Mp[idx + e];
         }
       }
     }
@@ -315,14 +322,14 @@ __device__ __forceinline__ void prep_tall(const PrepArgs& a, const MuonMat& mm, 
       mn[e] = fmaf(a.b2, mv[e], a.omb2 * gv[e]);
       ss = fmaf(c[e], c[e], ss);
     }
-    if (mm.m) {
+    if (Mp) {
       if (vec) {
         const f32x4 mv4 = {mn[0], mn[1], mn[2], mn[3]};
-        __builtin_nontemporal_store(mv4, reinterpret_cast<f32x4*>(mm.m + idx));
+        __builtin_nontemporal_store(mv4, reinterpret_cast<f32x4*>(Mp + idx));
       } else if (row_in) {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          if (q + e < mm.cols) mm.m[idx + e] = mn[e];
+          if (q + e < mm.cols) Mp[idx + e] = mn[e];
       }
     }
 #pragma unroll
@@ -401,6 +408,7 @@ __global__ __launch_bounds__(256) void norm_kernel(PrepArgs a) {
 // All sums are fp64 in a fixed order.
 struct SrankArgs {
   const MuonMat* mats;
+  const TensorPtrs* bind;
   const SrBlock* tab;
   const int32_t* rd_start;
   const int32_t* tensor_mat;
@@ -499,7 +507,7 @@ __global__ __launch_bounds__(256) void srank_tall_kernel(SrankArgs a, int32_t fi
   const int64_t r0 = int64_t(sb.blk) * kSrTallRows;
   const int nr = int(min(int64_t(kSrTallRows), mm.l - r0));
   // per-lane base; row and chunk offsets below are wave-uniform
-  const float* Ml = mm.m + (r0 + wave * kRg) * s + lane * 4;
+  const float* Ml = a.bind[mm.tensor].m + (r0 + wave * kRg) * s + lane * 4;
   const int cmax = s - lane * 4;                  // chunk q is in range iff q * 256 < cmax
   double w[NCH][4];
 #pragma unroll
@@ -604,7 +612,7 @@ __global__ __launch_bounds__(1024) void srank_wide_kernel(SrankArgs a, int32_t f
     const int64_t c = int64_t(sb.blk) * kSrWideCols + ss * SW + sub * 4;
     const bool cok = c < l;                       // l is a multiple of 4
     // per-lane base; pass offsets p * kRpp rows are wave-uniform
-    const float* Ml = mm.m + int64_t(r_lane) * l + c;
+    const float* Ml = a.bind[mm.tensor].m + int64_t(r_lane) * l + c;
     f32x4 x[NP];
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
@@ -677,15 +685,15 @@ __device__ __forceinline__ void load_vw(const float* p, bool ok, double x[VW]) {
 // Generic path, tall M (rows = l >= cols = s): block = kSrBlock rows; wave w
 // owns rows w, w + 4, ... of the block; lanes run along the row, VW floats each.
 template <int VW, bool FIRST, bool LAST>
-__device__ void srank_generic_tall(double (*red)[256], const MuonMat& mm, const SrBufs& B, int blk,
-                                   double inv) {
+__device__ void srank_generic_tall(double (*red)[256], const MuonMat& mm, const float* Mbase,
+                                   const SrBufs& B, int blk, double inv) {
   constexpr int kRows = kSrBlock / 4;
   constexpr int kChunk = 64 * VW;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int s = mm.s;
   const int64_t r0 = int64_t(blk) * kSrBlock;
   const int nr = int(min(int64_t(kSrBlock), mm.l - r0));
-  const float* M = mm.m + r0 * s;
+  const float* M = Mbase + r0 * s;
   double acc[kRows], fs[kRows];
 #pragma unroll
   for (int j = 0; j < kRows; ++j) acc[j] = fs[j] = 0.0;
@@ -745,8 +753,8 @@ __device__ void srank_generic_tall(double (*red)[256], const MuonMat& mm, const 
 // Generic path, wide M (rows = s < cols = l): block = kSrBlock columns; LPR
 // lanes cover one row's kSrBlock columns, VW floats each.
 template <int VW, bool FIRST, bool LAST>
-__device__ void srank_generic_wide(double (*red)[256], const MuonMat& mm, const SrBufs& B, int blk,
-                                   double inv) {
+__device__ void srank_generic_wide(double (*red)[256], const MuonMat& mm, const float* Mbase,
+                                   const SrBufs& B, int blk, double inv) {
   constexpr int kLpr = kSrBlock / VW;
   constexpr int kRpw = 64 / kLpr;
   constexpr int kRpp = 4 * kRpw;
@@ -757,7 +765,7 @@ __device__ void srank_generic_wide(double (*red)[256], const MuonMat& mm, const 
   const int64_t c = int64_t(blk) * kSrBlock + sub * VW;
   const bool cok = c < l;                        // VW = 4: l is a multiple of 4
   const int passes = (s + kRpp - 1) / kRpp;
-  const float* Mc = mm.m + c;
+  const float* Mc = Mbase + c;
   double acc[VW], fs[VW];
 #pragma unroll
   for (int e = 0; e < VW; ++e) acc[e] = fs[e] = 0.0;
@@ -825,11 +833,11 @@ __global__ __launch_bounds__(256) void srank_generic_kernel(SrankArgs a, int32_t
   const SrBufs B = sr_bufs(a.ws, mm);
   const double inv = sr_inv_norm(mm, B, FIRST);
   if (mm.tall) {
-    if (mm.vec_ok) srank_generic_tall<4, FIRST, LAST>(red, mm, B, sb.blk, inv);
-    else srank_generic_tall<1, FIRST, LAST>(red, mm, B, sb.blk, inv);
+    if (mm.vec_ok) srank_generic_tall<4, FIRST, LAST>(red, mm, a.bind[mm.tensor].m, B, sb.blk, inv);
+    else srank_generic_tall<1, FIRST, LAST>(red, mm, a.bind[mm.tensor].m, B, sb.blk, inv);
   } else {
-    if (mm.vec_ok) srank_generic_wide<4, FIRST, LAST>(red, mm, B, sb.blk, inv);
-    else srank_generic_wide<1, FIRST, LAST>(red, mm, B, sb.blk, inv);
+    if (mm.vec_ok) srank_generic_wide<4, FIRST, LAST>(red, mm, a.bind[mm.tensor].m, B, sb.blk, inv);
+    else srank_generic_wide<1, FIRST, LAST>(red, mm, a.bind[mm.tensor].m, B, sb.blk, inv);
   }
 }
 
@@ -1023,12 +1031,14 @@ template <int BT> struct TileGeom {
 
 struct GemmArgs {
   const MuonMat* mats;
+  const TensorPtrs* bind;
   const GemmTask* tasks;
   const XcdSplit* split;
   void* ws;
   const float* rscale;
   const int32_t* decide;
   int32_t src, first, last, store_o;
+  int32_t xcds;                  // workgroup i runs on XCD i mod xcds
   float a, b, c, lr, wd;
 };
 
@@ -1072,10 +1082,11 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // stage their results through the whole LDS and run one tile per
   // workgroup, so a finished workgroup's successor starts at once.
   constexpr bool kPersistent = MODE == kApply && !LAST;
-  const int xcd = blockIdx.x % kXcds;
+  const int xcds = g.xcds;
+  const int xcd = int(blockIdx.x) % xcds;
   const int count = kconst(g.split)->count[xcd];
   const auto* tasks = kconst(g.tasks) + kconst(g.split)->start[xcd];
-  const int step = int(gridDim.x) / kXcds;
+  const int step = int(gridDim.x) / xcds;
   auto live = [&](int s) {
     while (s < count && g.decide && kconst(g.decide)[tasks[s].mat] == 0) s += step;
     return s;
@@ -1087,7 +1098,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // they drain. kDirect is the number of those stores per lane.
   constexpr int kDirect = Geo::kMI * Geo::kNI * 4;
   bool prefetched = false;
-  for (int slot = live(blockIdx.x / kXcds); slot < count;) {
+  for (int slot = live(int(blockIdx.x) / xcds); slot < count;) {
   // Lane-derived values are recomputed for every tile (the empty asm keeps
   // the compiler from hoisting them out of the tile loop, where they would
   // stay live, in registers, through the epilogue).
@@ -1533,6 +1544,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
       static_assert(kIter * kNT == kHalf * (BT / 4), "W pieces split evenly over the threads");
       float (*fst)[kFs] = reinterpret_cast<float (*)[kFs]>(smem);
       const bool tall = mm.transposed != 0;
+      float* Wp = kconst(g.bind)[mm.tensor].w;
       const int64_t wrow0 = tall ? col0 : row0, wcol0 = tall ? row0 : col0;
       const int64_t wrows = mm.rows, wcols = mm.cols;
       const float kappa = mm.kappa;
@@ -1547,7 +1559,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
             const int64_t gr = wrow0 + h * kHalf + i, gc = wcol0 + j;
             wv[it] = f32x4{0.f, 0.f, 0.f, 0.f};
             if (mm.vec_ok && gr < wrows && gc + 3 < wcols)
-              wv[it] = *reinterpret_cast<const f32x4*>(mm.w + gr * wcols + gc);
+              wv[it] = *reinterpret_cast<const f32x4*>(Wp + gr * wcols + gc);
           }
         }
 #pragma unroll
@@ -1576,7 +1588,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
           const int i = idx / (BT / 4), j = (idx % (BT / 4)) * 4;
           const int64_t gr = wrow0 + h * kHalf + i, gc = wcol0 + j;
           if (gr >= wrows || gc >= wcols) continue;
-          float* wp = mm.w + gr * wcols + gc;
+          float* wp = Wp + gr * wcols + gc;
           float o[4];
           load4(&fst[i][j], o);
           if (mm.vec_ok && gc + 3 < wcols) {
@@ -1634,6 +1646,7 @@ hipError_t launch_lion(const LionLaunch& l, hipStream_t stream) {
   if (l.n_blocks == 0) return hipSuccess;
   LionArgs a;
   a.tensors = l.tensors;
+  a.bind = l.bind;
   a.block_start = l.block_start;
   a.n_tensors = l.n_tensors;
   a.b1 = l.k.beta1;
@@ -1659,6 +1672,7 @@ hipError_t launch_lion(const LionLaunch& l, hipStream_t stream) {
 static PrepArgs prep_args(const PrepLaunch& l) {
   PrepArgs a;
   a.mats = l.mats;
+  a.bind = l.bind;
   a.prep_start = l.prep_start;
   a.n_mats = l.n_mats;
   a.ws = l.ws;
@@ -1689,6 +1703,8 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
   if (l.max_count == 0) return hipSuccess;
   GemmArgs a;
   a.mats = l.mats;
+  a.bind = l.bind;
+  a.xcds = l.chip.xcds;
   a.tasks = l.tasks;
   a.split = l.split;
   a.ws = l.ws;
@@ -1709,8 +1725,8 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
   // (only the non-final apply is persistent; the others keep one workgroup
   // per tile)
   const int per_cu = l.tile == 256 ? 1 : (l.tile == 128 ? (l.fp32 ? 2 : 1) : (l.fp32 ? 4 : 2));
-  const int per_xcd = (mode != kApply || l.last) ? l.max_count : (kComputeUnits / kXcds) * per_cu;
-  const dim3 grid(unsigned(l.max_count < per_xcd ? l.max_count : per_xcd) * kXcds);
+  const int per_xcd = (mode != kApply || l.last) ? l.max_count : (l.chip.cus / l.chip.xcds) * per_cu;
+  const dim3 grid(unsigned(l.max_count < per_xcd ? l.max_count : per_xcd) * unsigned(l.chip.xcds));
 #define LM_LAUNCH(KERNEL, T, BT) \
   hipLaunchKernelGGL((KERNEL<T, BT>), grid, dim3(TileGeom<BT>::kThreads), 0, stream, a)
 #define LM_LAUNCH_MODE(T, BT)                                   \
@@ -1742,6 +1758,7 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
 static SrankArgs srank_args(const SrankLaunch& l) {
   SrankArgs a;
   a.mats = l.mats;
+  a.bind = l.bind;
   a.tab = l.tab;
   a.rd_start = l.rd_start;
   a.tensor_mat = l.tensor_mat;

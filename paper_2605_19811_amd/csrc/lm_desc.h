@@ -1,7 +1,9 @@
 // Plain-old-data descriptors shared by the host planner and the gfx950
-// kernels of the LionMuon step. Only integer and pointer fields: the planner
-// fills them on the host, uploads them once per tensor-list signature, and the
-// kernels read them from device memory.
+// kernels of the LionMuon step. The planner fills them on the host from the
+// shapes, flags and alignment of a tensor list (no tensor addresses), uploads
+// them once per such signature, and the kernels read them from device memory.
+// The caller's tensor addresses reach the kernels separately, as one
+// TensorPtrs entry per input tensor (the per-call binding table).
 #pragma once
 
 #include <stdint.h>
@@ -17,8 +19,9 @@ constexpr int kPrepTile = 64;    // rows of a tall matrix's preparation / transp
 constexpr int kPrepTallCols = 128;  // its columns with bf16 X (64 with fp32 X)
 constexpr int kPrepElems = 4096; // elements of every preparation tile (wide: 16 x 256 or 32 x 128)
 constexpr int kLionBlockElems = 4096;  // elements per Lion workgroup (256 x float4 x 4)
-constexpr int kXcds = 8;         // accelerator complex dies of one MI355X
-constexpr int kComputeUnits = 256;  // CUs of one MI355X: workgroups of one full round
+constexpr int kMaxXcds = 8;      // most accelerator complex dies of one device
+                                 // (MI355X: 8 XCDs of 32 CUs; the counts in use
+                                 // are read from the device, see ChipShape)
 // Stable-rank passes (adaptive step). Matrices with 16-byte rows and a short
 // side up to kSrMaxRegSide hold their block in registers (tall: blocks of
 // kSrTallRows rows; wide: strips of kSrWideCols columns, taken 32 columns at a
@@ -31,6 +34,22 @@ constexpr int kSrMaxRegSide = 2048;
 constexpr int kSrChunk = 64;     // short-side entries per stable-rank reduction workgroup
 enum SrKind : int32_t { kSrGeneric = 0, kSrTall = 1, kSrWide = 2, kSrWideNarrow = 3 };
 
+// Compute units and XCDs of the device a plan is built for. Workgroup i of a
+// launch runs on XCD i mod xcds; a full round of one-per-CU workgroups is cus.
+struct ChipShape {
+  int32_t cus = 256;
+  int32_t xcds = 8;
+};
+
+// Device addresses of one input tensor, uploaded per call (the plan holds
+// only tensor indices into this table).
+struct TensorPtrs {
+  float* w;          // W (the output O for the NS hook)
+  const float* g;    // G
+  float* m;          // M (null for the NS hook)
+  float* v;          // AdamW second moment, or null
+};
+
 // One workgroup of a stable-rank pass: matrix index and block index.
 struct SrBlock {
   int32_t mat;
@@ -39,26 +58,20 @@ struct SrBlock {
 
 // One tensor of the elementwise pass: the Lion branch, or AdamW.
 struct LionTensor {
-  float* w;
-  const float* g;
-  float* m;         // Lion momentum / AdamW first moment
-  float* v;         // AdamW second moment (null for Lion)
   int64_t numel;
+  int32_t tensor;   // index into the binding table (w, g, m and, for AdamW, v)
   int32_t vec_ok;   // every buffer of the tensor is 16-byte aligned
   int32_t adamw;    // 1: AdamW, 0: Lion
   int32_t gate;     // adaptive step: Muon-candidate index whose decision gates
                     // this tensor (skipped when the candidate took Muon); -1: always
-  int32_t pad_;
 };
 
 // One matrix on the Muon branch. Workspace offsets are in BYTES from the
 // workspace base; the Newton-Schulz buffers of the matrix hold bf16 or fp32
 // elements (`fp32`).
 struct MuonMat {
-  float* w;          // W (m x n, row-major); the output O for the NS hook
-  const float* g;    // G
-  float* m;          // M, or null (NS hook: no momentum)
-  int64_t rows, cols;      // m, n of the original tensor
+  int64_t rows, cols;      // m, n of the original tensor (W, G, M row-major;
+                           // their addresses are entry `tensor` of the binding)
   int32_t s, l;            // short and long side
   int32_t s_pad, l_pad;    // padded to 128 (fp32) or 256 (bf16)
   int32_t transposed;      // rows > cols: iterate on G^T
@@ -89,10 +102,11 @@ struct GemmTask {
   int16_t tm, tn;          // tile row / column (units of the launch's tile edge)
 };
 
-// Per-launch partition of a task list into one contiguous segment per XCD.
+// Per-launch partition of a task list into one contiguous segment per XCD
+// (the first ChipShape::xcds entries are used).
 struct XcdSplit {
-  int32_t start[kXcds];
-  int32_t count[kXcds];
+  int32_t start[kMaxXcds];
+  int32_t count[kMaxXcds];
   int32_t max_count;
 };
 

@@ -39,14 +39,14 @@ void sym_tiles(const MuonMat& mm, int32_t mi, int tile, int64_t inner,
 // 256-tile rate, measured on the benchmark sets); set-up and epilogue cost
 // 7 and 5 units.
 int64_t sym_launch_estimate(const std::vector<GemmTask>& tasks, const std::vector<int64_t>& inner,
-                            const XcdSplit& split, int tile) {
+                            const XcdSplit& split, int tile, ChipShape chip) {
   const bool big = tile == kTileBig;
-  const int slots = kComputeUnits / kXcds * (big ? 1 : 2);
+  const int slots = std::max(1, chip.cus / chip.xcds) * (big ? 1 : 2);
   const int64_t per_stage = big ? 4 : 3, fixed = big ? 7 : 5;
   const int64_t kbk = 64;
   int64_t worst = 0;
   std::vector<int64_t> free_at(size_t(slots), 0);
-  for (int x = 0; x < kXcds; ++x) {
+  for (int x = 0; x < chip.xcds; ++x) {
     std::fill(free_at.begin(), free_at.end(), 0);
     for (int32_t i = split.start[x]; i < split.start[x] + split.count[x]; ++i) {
       auto it = std::min_element(free_at.begin(), free_at.end());
@@ -60,7 +60,7 @@ int64_t sym_launch_estimate(const std::vector<GemmTask>& tasks, const std::vecto
 // Tile edge for a bf16 symmetric product (Gram if `gram`, else the
 // polynomial): 256 unless 128-tiles are estimated to finish sooner (too few
 // 256-tiles to fill the chip, or too uneven a last round).
-int32_t pick_sym_tile(const std::vector<MuonMat>& mats, bool gram) {
+int32_t pick_sym_tile(const std::vector<MuonMat>& mats, bool gram, ChipShape chip) {
   int64_t est[2] = {0, 0};
   const int32_t sizes[2] = {kTileBig, kTileSmall};
   for (int k = 0; k < 2; ++k) {
@@ -73,13 +73,13 @@ int32_t pick_sym_tile(const std::vector<MuonMat>& mats, bool gram) {
     }
     if (tasks.empty()) return kTileBig;
     XcdSplit split;
-    split_by_xcd(&tasks, cost, &split);
+    split_by_xcd(&tasks, cost, chip.xcds, &split);
     std::vector<int64_t> inner(tasks.size());
     for (size_t i = 0; i < tasks.size(); ++i) {
       const MuonMat& mm = mats[size_t(tasks[i].mat)];
       inner[i] = gram ? mm.l_pad : mm.s_pad;
     }
-    est[k] = sym_launch_estimate(tasks, inner, split, sizes[k]);
+    est[k] = sym_launch_estimate(tasks, inner, split, sizes[k], chip);
   }
   return est[0] <= est[1] ? kTileBig : kTileSmall;
 }
@@ -106,6 +106,12 @@ int sr_wide_bucket(int64_t s) {
 }
 
 bool is_muon_step(int64_t t, int32_t P) { return P >= 1 && t % P == 0; }
+
+uint32_t align_class(const TensorIn& x) {
+  const uintptr_t vbits = (x.flags & kFlagAdamW) ? reinterpret_cast<uintptr_t>(x.v) : 0;
+  return ((reinterpret_cast<uintptr_t>(x.w) | reinterpret_cast<uintptr_t>(x.g) |
+           reinterpret_cast<uintptr_t>(x.m) | vbits) & 15u) == 0 ? 1u : 0u;
+}
 
 bool is_matrix(const TensorIn& x) {
   return x.rows > 1 && x.cols > 1 && !(x.flags & (kFlagLionOnly | kFlagAdamW));
@@ -188,27 +194,28 @@ Status validate_tensors(const TensorIn* x, int32_t n, std::string* err) {
   return Status::kOk;
 }
 
-void split_by_xcd(std::vector<GemmTask>* tasks, const std::vector<int64_t>& cost,
+void split_by_xcd(std::vector<GemmTask>* tasks, const std::vector<int64_t>& cost, int xcds,
                   XcdSplit* split) {
   const size_t n = tasks->size();
   const int64_t total = std::accumulate(cost.begin(), cost.end(), int64_t(0));
-  // cut points: segment x ends once the running cost reaches (x+1)/8 of total
-  std::vector<size_t> cut(kXcds + 1, 0);
+  *split = XcdSplit{};
+  // cut points: segment x ends once the running cost reaches (x+1)/xcds of total
+  std::vector<size_t> cut(size_t(xcds) + 1, 0);
   size_t pos = 0;
   int64_t run = 0;
-  for (int x = 0; x < kXcds; ++x) {
+  for (int x = 0; x < xcds; ++x) {
     cut[x] = pos;
-    const int64_t goal = (total * (x + 1) + kXcds - 1) / kXcds;
-    while (pos < n && (run < goal || x == kXcds - 1)) {
+    const int64_t goal = (total * (x + 1) + xcds - 1) / xcds;
+    while (pos < n && (run < goal || x == xcds - 1)) {
       run += cost[pos];
       ++pos;
     }
   }
-  cut[kXcds] = n;
+  cut[xcds] = n;
   std::vector<GemmTask> out;
   out.reserve(n);
   split->max_count = 0;
-  for (int x = 0; x < kXcds; ++x) {
+  for (int x = 0; x < xcds; ++x) {
     std::vector<size_t> idx(cut[x + 1] - cut[x]);
     std::iota(idx.begin(), idx.end(), cut[x]);
     std::stable_sort(idx.begin(), idx.end(),
@@ -222,8 +229,13 @@ void split_by_xcd(std::vector<GemmTask>* tasks, const std::vector<int64_t>& cost
 }
 
 Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
-                  bool kappa_rms02, Plan* p, std::string* err) {
+                  bool kappa_rms02, ChipShape chip, Plan* p, std::string* err) {
   *p = Plan();
+  if (chip.xcds < 1 || chip.xcds > kMaxXcds || chip.cus < chip.xcds) {
+    *err = "unsupported device shape (compute units / XCDs)";
+    return Status::kUnsupported;
+  }
+  p->chip = chip;
   const bool muon_step = kind != StepKind::kLion;
   p->muon_step = muon_step;
   p->adaptive = kind == StepKind::kAdaptive;
@@ -238,16 +250,11 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
     if (t.rows == 0 || t.cols == 0) continue;
     ++p->n_tensors;
     const bool adamw = (t.flags & kFlagAdamW) != 0;
-    const uintptr_t vbits = adamw ? reinterpret_cast<uintptr_t>(t.v) : 0;
-    const bool vec_ok = ((reinterpret_cast<uintptr_t>(t.w) | reinterpret_cast<uintptr_t>(t.g) |
-                          reinterpret_cast<uintptr_t>(t.m) | vbits) & 15u) == 0;
+    const bool vec_ok = align_class(t) != 0;
     const bool candidate = muon_step && is_matrix(t);
     if (!candidate || p->adaptive) {
       LionTensor lt{};
-      lt.w = t.w;
-      lt.g = t.g;
-      lt.m = t.m;
-      lt.v = adamw ? t.v : nullptr;
+      lt.tensor = i;
       lt.numel = t.rows * t.cols;
       lt.vec_ok = vec_ok ? 1 : 0;
       lt.adamw = adamw ? 1 : 0;
@@ -268,9 +275,6 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
       if (!candidate) continue;
     }
     MuonMat mm{};
-    mm.w = t.w;
-    mm.g = t.g;
-    mm.m = t.m;
     mm.rows = t.rows;
     mm.cols = t.cols;
     mm.transposed = t.rows > t.cols ? 1 : 0;
@@ -348,8 +352,8 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
   // below favours. fp32: 128-tiles, or 64-tiles for a product whose
   // 128-tiles would not give every CU one.
   if (p->mats.size() > 0) {
-    p->tile[0][0] = pick_sym_tile(p->mats, true);
-    p->tile[0][1] = pick_sym_tile(p->mats, false);
+    p->tile[0][0] = pick_sym_tile(p->mats, true, chip);
+    p->tile[0][1] = pick_sym_tile(p->mats, false, chip);
   }
   p->tile[0][2] = kTileBig;
   {
@@ -360,8 +364,8 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
       sym += ts * (ts + 1) / 2;
       app += ts * (mm.l_pad / kTileSmall);
     }
-    p->tile[1][0] = p->tile[1][1] = sym < kComputeUnits ? kTileTiny : kTileSmall;
-    p->tile[1][2] = app < kComputeUnits ? kTileTiny : kTileSmall;
+    p->tile[1][0] = p->tile[1][1] = sym < chip.cus ? kTileTiny : kTileSmall;
+    p->tile[1][2] = app < chip.cus ? kTileTiny : kTileSmall;
   }
   for (int pr = 0; pr < 2; ++pr) {
     std::vector<int64_t> cg, cp, ca;
@@ -384,11 +388,12 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
     // their indices fit the task fields), else 128-tiles (4 per 256-tile).
     std::vector<int64_t> ct;
     if (t_app == kTileBig) {
-      const size_t n = p->apply[pr].size(), rem = n % kComputeUnits;
-      if (n > rem && rem > 0 && 2 * rem <= size_t(kComputeUnits)) {
+      const size_t cus = size_t(chip.cus);
+      const size_t n = p->apply[pr].size(), rem = n % cus;
+      if (n > rem && rem > 0 && 2 * rem <= cus) {
         int64_t max_tl = 0;
         for (size_t i = n - rem; i < n; ++i) max_tl = std::max<int64_t>(max_tl, p->apply[pr][i].tn);
-        const int split = (16 * rem <= size_t(kComputeUnits) && 4 * (max_tl + 1) <= INT16_MAX) ? 4 : 2;
+        const int split = (16 * rem <= cus && 4 * (max_tl + 1) <= INT16_MAX) ? 4 : 2;
         p->tail_tile[pr] = kTileBig / split;
         for (size_t i = n - rem; i < n; ++i) {
           const GemmTask t = p->apply[pr][i];
@@ -402,10 +407,10 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
         ca.resize(n - rem);
       }
     }
-    split_by_xcd(&p->gram[pr], cg, &p->gram_split[pr]);
-    split_by_xcd(&p->poly[pr], cp, &p->poly_split[pr]);
-    split_by_xcd(&p->apply[pr], ca, &p->apply_split[pr]);
-    split_by_xcd(&p->apply_tail[pr], ct, &p->apply_tail_split[pr]);
+    split_by_xcd(&p->gram[pr], cg, chip.xcds, &p->gram_split[pr]);
+    split_by_xcd(&p->poly[pr], cp, chip.xcds, &p->poly_split[pr]);
+    split_by_xcd(&p->apply[pr], ca, chip.xcds, &p->apply_split[pr]);
+    split_by_xcd(&p->apply_tail[pr], ct, chip.xcds, &p->apply_tail_split[pr]);
   }
 
   size_t off = align256(size_t(ns_off));
@@ -429,7 +434,11 @@ Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
     p->ws_decide_off = off;
     off = align256(off + p->mats.size() * sizeof(int32_t));
     for (MuonMat& mm : p->mats) {
-      const int64_t nb = mm.sr_blocks, s = mm.s;
+      // sized for the generic path's block count (the largest of the three
+      // paths), so the workspace a list needs does not depend on which path
+      // its alignment selects
+      const int64_t nb = std::max<int64_t>(mm.sr_blocks, (mm.l + kSrBlock - 1) / kSrBlock);
+      const int64_t s = mm.s;
       mm.off_sr = int64_t(off);
       off = align256(off + size_t(s + nb * s + 2 * nb + (s + kSrChunk - 1) / kSrChunk) *
                                sizeof(double));

@@ -57,6 +57,7 @@ enum class StepKind : int { kLion = 0, kMuon = 1, kAdaptive = 2 };
 struct Plan {
   bool muon_step = false;
   bool adaptive = false;
+  ChipShape chip;
 
   // Lion branch
   std::vector<LionTensor> lion;
@@ -72,7 +73,7 @@ struct Plan {
   // grouped per XCD segment
   std::vector<GemmTask> gram[2], poly[2], apply[2];
   XcdSplit gram_split[2]{}, poly_split[2]{}, apply_split[2]{};
-  // bf16 apply tiles past the last full round of kComputeUnits 256-tiles,
+  // bf16 apply tiles past the last full round of 256-tiles (one per CU),
   // when they fill at most half a round, each split into four 128-tiles
   // (a second launch after `apply`)
   std::vector<GemmTask> apply_tail[2];
@@ -111,10 +112,18 @@ Status validate_scalars(int64_t t, int32_t P, double beta1, double beta2, double
 // Validate the tensor list: pointers, shapes, flags and buffer overlaps.
 Status validate_tensors(const TensorIn* x, int32_t n, std::string* err);
 
-// Build the plan of one step kind; kappa_rms02 selects Table 3 output
-// scaling.
+// Build the plan of one step kind for a device of the given shape;
+// kappa_rms02 selects Table 3 output scaling. The plan depends on the
+// tensors' shapes, flags and 16-byte alignment only, never on their
+// addresses (those go into the per-call binding table). Its workspace size
+// does not depend on alignment either.
 Status build_plan(const TensorIn* x, int32_t n, StepKind kind, NsPrecision prec,
-                  bool kappa_rms02, Plan* out, std::string* err);
+                  bool kappa_rms02, ChipShape chip, Plan* out, std::string* err);
+
+// 16-byte alignment class of one tensor's buffers (the only property of its
+// addresses a plan depends on): bit 0 = W, G, M (and V for AdamW) all 16-byte
+// aligned.
+uint32_t align_class(const TensorIn& x);
 
 // Register buckets of the stable-rank passes: the smallest listed bucket
 // holding ceil(s / 256) column chunks (tall, s <= 2048), ceil(s / 128) row
@@ -127,9 +136,9 @@ int sr_tall_bucket(int64_t s);
 int sr_wide_bucket(int64_t s);
 
 // Split an ordered task list (cost = inner dimension of each tile) into one
-// contiguous segment per XCD with near-equal total cost, then order each
-// segment by decreasing cost (stable). Exposed for tests.
-void split_by_xcd(std::vector<GemmTask>* tasks, const std::vector<int64_t>& cost,
+// contiguous segment per XCD (xcds of them) with near-equal total cost, then
+// order each segment by decreasing cost (stable). Exposed for tests.
+void split_by_xcd(std::vector<GemmTask>* tasks, const std::vector<int64_t>& cost, int xcds,
                   XcdSplit* split);
 
 // Algorithmic Newton-Schulz flops of one Muon step over the plan's matrices.

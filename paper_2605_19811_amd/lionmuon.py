@@ -54,7 +54,7 @@ class lm_config(ctypes.Structure):
                 ("adam_beta2", ctypes.c_double), ("adam_eps", ctypes.c_double),
                 ("adam_wd", ctypes.c_double),
                 ("adaptive_alpha", ctypes.c_double), ("adaptive_power_steps", ctypes.c_int32),
-                ("reserved3", ctypes.c_int32)]
+                ("reserved3", ctypes.c_int32), ("adam_step", ctypes.c_int64)]
 
 
 class lm_plan_info(ctypes.Structure):
@@ -137,10 +137,13 @@ def _check(status, what):
 def config(ns_steps=5, ns_coeffs=(3.4445, -4.7750, 2.0315), ns_eps=1e-7,
            ns_precision="bf16", ns_scale="none", lr_muon=0.0, lr_lion=0.0,
            ns_bf16_min_side=64, ns_schedule=None, adam_lr=1e-3, adam_betas=(0.8, 0.999),
-           adam_eps=1e-8, adam_wd=0.0, adaptive_alpha=0.0, adaptive_power_steps=5) -> lm_config:
+           adam_eps=1e-8, adam_wd=0.0, adaptive_alpha=0.0, adaptive_power_steps=5,
+           adam_step=0) -> lm_config:
     """lm_config with defaults; ``ns_schedule`` is an optional list of
     per-step (a, b, c) triples (its length sets ns_steps); ``adaptive_alpha``
-    > 0 selects the stable-rank rule of Appendix G instead of the period."""
+    > 0 selects the stable-rank rule of Appendix G instead of the period;
+    ``adam_step`` is the AdamW step count k >= 1 of the call's bias
+    corrections (0: k = t + 1)."""
     cfg = lm_config()
     library().lionmuon_config_default(ctypes.byref(cfg))
     cfg.ns_steps = ns_steps
@@ -157,6 +160,7 @@ def config(ns_steps=5, ns_coeffs=(3.4445, -4.7750, 2.0315), ns_eps=1e-7,
     cfg.adam_wd = adam_wd
     cfg.adaptive_alpha = adaptive_alpha
     cfg.adaptive_power_steps = adaptive_power_steps
+    cfg.adam_step = int(adam_step)
     if ns_schedule is not None:
         sched = [tuple(float(v) for v in t) for t in ns_schedule]
         if not 1 <= len(sched) <= 16 or any(len(t) != 3 for t in sched):
@@ -232,6 +236,10 @@ class TensorList:
             raise ValueError("params, grads and momentum must have one length")
         lion_only = list(lion_only) if lion_only is not None else [False] * n
         second_moment = list(second_moment) if second_moment is not None else [None] * n
+        if len(lion_only) != n:
+            raise ValueError(f"lion_only has {len(lion_only)} entries for {n} tensors")
+        if len(second_moment) != n:
+            raise ValueError(f"second_moment has {len(second_moment)} entries for {n} tensors")
         for i, v in enumerate(second_moment):
             if v is not None:
                 _check_tensor(v, f"second_moment[{i}]")
@@ -253,6 +261,8 @@ class TensorList:
         self._keep = (list(params), list(grads), list(momentum), second_moment)
 
     def set_grads(self, grads):
+        if len(grads) != self.n:
+            raise ValueError(f"{len(grads)} gradients for {self.n} tensors")
         for i, t in enumerate(grads):
             _check_tensor(t, f"grads[{i}]")
             if t.shape != self._keep[0][i].shape:
@@ -335,6 +345,9 @@ def lionmuon_ns(X, cfg: lm_config | None = None, out=None, stream=None):
     if out is None:
         out = torch.empty_like(X)
     _check_tensor(out, "out")
+    if out.shape != X.shape or out.device != X.device:
+        raise LionMuonError(LM_ERR_INVALID_ARGUMENT,
+                            f"out must have X's shape {tuple(X.shape)} and device {X.device}")
     st = library().lionmuon_ns(X.data_ptr(), out.data_ptr(), rows, cols, batch,
                                ctypes.byref(cfg) if cfg is not None else None, None, 0,
                                _stream_handle(stream))

@@ -9,7 +9,7 @@
 #include <string>
 using namespace lm;
 static int run(const std::vector<std::pair<long, long>>& shapes, StepKind kind, bool fp32,
-               int flags = 0) {
+               int flags = 0, ChipShape chip = ChipShape()) {
   std::vector<TensorIn> x(shapes.size());
   for (size_t i = 0; i < shapes.size(); ++i) {
     x[i] = TensorIn{};
@@ -24,7 +24,7 @@ static int run(const std::vector<std::pair<long, long>>& shapes, StepKind kind, 
   std::string err;
   NsPrecision prec;
   prec.all_fp32 = fp32;
-  Status st = build_plan(x.data(), int(x.size()), kind, prec, false, &p, &err);
+  Status st = build_plan(x.data(), int(x.size()), kind, prec, false, chip, &p, &err);
   size_t ntask = 0;
   for (int pr = 0; pr < 2; ++pr)
     ntask += p.gram[pr].size() + p.poly[pr].size() + p.apply[pr].size() + p.apply_tail[pr].size();
@@ -59,6 +59,16 @@ int main() {
   bad += run({{8192, 8192}}, StepKind::kMuon, false);
   bad += run({{100000, 64}}, StepKind::kAdaptive, false);
   bad += run({}, StepKind::kMuon, false);
+  // partitioned devices: one XCD of 32 CUs, two XCDs of 64
+  ChipShape one_xcd;
+  one_xcd.cus = 32;
+  one_xcd.xcds = 1;
+  ChipShape two_xcd;
+  two_xcd.cus = 64;
+  two_xcd.xcds = 2;
+  bad += run(s124, StepKind::kMuon, false, 0, one_xcd);
+  bad += run(s720, StepKind::kAdaptive, false, 0, two_xcd);
+  bad += run(edge, StepKind::kMuon, true, 0, one_xcd);
   printf("failures %d\n", bad);
   return bad;
 }

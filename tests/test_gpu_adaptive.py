@@ -314,3 +314,40 @@ def test_adaptive_gated_tiles_every_tensor_checked():
             check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 0.02, 0.1, "bf16")
         else:
             check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 1e-3, 0.1)
+
+
+def test_adaptive_caller_workspace_on_misaligned_tensors():
+    """A caller workspace sized by lionmuon_workspace_bytes (which never sees
+    addresses) must hold an adaptive step whose tensors sit 4 bytes off a
+    16-byte boundary, where the stable-rank passes take the generic path and
+    its smaller blocks need the most partial products."""
+    shapes = [(768, 2304), (2304, 768), (300, 1000)]
+    rng = np.random.default_rng(91)
+    W0 = [(rng.standard_normal(s) * 0.02).astype(np.float32) for s in shapes]
+    G = [(rng.standard_normal(s) * 1e-2).astype(np.float32) for s in shapes]
+    M0 = [low_rank_momentum([91, i], s, 2, 1e-3) if i != 1 else
+          (rng.standard_normal(s) * 1e-2).astype(np.float32) for i, s in enumerate(shapes)]
+    alpha, k = 0.05, 3
+    cfg = lm.config(ns_precision="fp32", lr_muon=0.02, lr_lion=1e-3, adaptive_alpha=alpha,
+                    adaptive_power_steps=k)
+    nbytes = lm.lionmuon_workspace_bytes([(*s, False) for s in shapes], cfg)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+    n = [int(np.prod(s)) for s in shapes]
+    bufs = [[torch.zeros(k_ + 8, device=DEV) for k_ in n] for _ in range(3)]
+    W, M, Gd = ([b[1:1 + k_].view(s) for b, k_, s in zip(bl, n, shapes)] for bl in bufs)
+    for i in range(len(shapes)):
+        W[i].copy_(dev(W0[i])); M[i].copy_(dev(M0[i])); Gd[i].copy_(dev(G[i]))
+    dec = torch.zeros(len(shapes), dtype=torch.int32, device=DEV)
+    sr = torch.zeros(len(shapes), dtype=torch.float64, device=DEV)
+    print("adaptive step, caller workspace, misaligned tensors", flush=True)
+    lm.lionmuon_step_adaptive(W, Gd, M, 3, 0.9, 0.99, 0.1, cfg, workspace=ws, decisions=dec,
+                              stable_rank=sr)
+    torch.cuda.synchronize()
+    dec, sr = dec.cpu().numpy(), sr.cpu().numpy()
+    check_decisions(M0, {0, 1, 2}, dec, sr, alpha, k)
+    assert dec[0] == 1 and dec[1] == 0
+    for i in range(len(shapes)):
+        if dec[i]:
+            check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 0.02, 0.1, "fp32")
+        else:
+            check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 1e-3, 0.1)

@@ -621,12 +621,13 @@ def test_full_set_sampled(name):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("name", ["gpt2-124m", "gpt2-355m"])
+@pytest.mark.parametrize("name", ["gpt2-124m", "gpt2-355m", "gpt2-720m"])
 def test_full_set_every_matrix(name):
     """The set's Muon step in the benchmark's launch configuration, with every
     matrix compared with the oracle (at 124M the persistent apply walks five
     tiles per workgroup and the last round goes to the 64-tile launch; at
-    355M eighteen)."""
+    355M eighteen; at 720M the Lion-only 50257 x 1280 embedding and the 290
+    1-D vectors take the Lion branch in the same step, every row checked)."""
     wl = workloads.get(name)
     params, moms, grads = workloads.device_state(torch, wl, DEV, seed=8, warm=True, n_grad=1)
     grads = grads[0]
@@ -637,12 +638,18 @@ def test_full_set_every_matrix(name):
     print(f"{name}: Muon step, every matrix checked", flush=True)
     lm.lionmuon_step_ex(None, None, None, 2, wl.P, wl.beta1, wl.beta2, wl.wd, cfg, tensors=tl)
     sync()
-    errs = []
+    errs, bands = [], 0
     for i, (W0, M0, G) in enumerate(before):
-        errs.append(check_muon(W0, G, M0, params[i].cpu().numpy(), moms[i].cpu().numpy(),
-                               wl.beta1, wl.beta2, wl.lr_muon, wl.wd, "bf16"))
-    print(f"{name}: max Muon direction error {max(errs):.2e} over {len(errs)} matrices",
-          flush=True)
+        spec = wl.tensors[i]
+        W1, M1 = params[i].cpu().numpy(), moms[i].cpu().numpy()
+        if spec.lion_only or spec.rows == 1:
+            bands += check_lion(W0, G, M0, W1, M1, wl.beta1, wl.beta2, wl.lr_lion, wl.wd)
+            continue
+        errs.append(check_muon(W0, G, M0, W1, M1, wl.beta1, wl.beta2, wl.lr_muon, wl.wd, "bf16"))
+        if len(errs) % 24 == 0:
+            print(f"{name}: {len(errs)} matrices checked, max error {max(errs):.2e}", flush=True)
+    print(f"{name}: max Muon direction error {max(errs):.2e} over {len(errs)} matrices; "
+          f"{bands} rounding-band positions on the Lion-only tensors", flush=True)
     del params, moms, grads, tl
     lm.lionmuon_release()
     torch.cuda.empty_cache()
