@@ -195,6 +195,34 @@ lm_status lionmuon_step_ex(float* const* params, const float* const* grads,
                            hipStream_t stream);
 
 /*
+ * lionmuon_step_ex for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments and results as lionmuon_step_ex without a workspace; the
+ * call allocates nothing (no hipMalloc / hipHostMalloc / hipFree, no events;
+ * phase timing is not recorded). Its plan tables, the call's tensor
+ * addresses and the Newton-Schulz workspace live in one static device array
+ * of LIONMUON_NOALLOC_SCRATCH_BYTES bytes per device, which each device holds
+ * from the library's first use of it until the process ends. Tables reach
+ * the array through kernel arguments, on `stream`, only when the list
+ * signature (shapes, flags, alignment, step kind, cfg precision and scaling)
+ * or the tensor addresses differ from the previous call's.
+ * A list whose tables and workspace exceed the array fails with
+ * LM_ERR_UNSUPPORTED before anything is enqueued (the message gives the
+ * bytes needed): a Muon step over one 768x3072 bf16 matrix needs about
+ * 12 MB, one 2048x4096 matrix about 50 MB.
+ * All calls on one device share the array, which keeps the last call's
+ * contents: calls on one device must not overlap (on different streams they
+ * race); consecutive calls on one stream are ordered. No kernel reads scratch
+ * it has not written in the same call, so nothing needs clearing.
+ */
+#define LIONMUON_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+lm_status lionmuon_step_noalloc(float* const* params, const float* const* grads,
+                                float* const* momentum, float* const* second_moment,
+                                const lm_shape* shapes, int32_t n_tensors, int64_t t, int32_t P,
+                                double beta1, double beta2, double wd, const lm_config* cfg,
+                                hipStream_t stream);
+
+/*
  * One step of the adaptive variant (Appendix G) with per-tensor diagnostics:
  * lionmuon_step_ex with cfg->adaptive_alpha in (0, 1] (required here), plus
  *   decisions:   optional device int32[n_tensors]: 1 where the tensor took the

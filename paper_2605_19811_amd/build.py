@@ -47,7 +47,7 @@ def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     inc = [f"-I{INCLUDE}", f"-I{CSRC}"]
     objs = []
-    for src in ("kernels.hip",):
+    for src in ("kernels.hip", "scratch.hip"):
         obj = os.path.join(BUILD, src + ".o")
         _run([HIPCC, *HIP_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o", obj], verbose)
         objs.append(obj)

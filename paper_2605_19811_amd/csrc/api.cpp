@@ -149,8 +149,10 @@ struct OwnedWorkspace {
 };
 std::vector<OwnedWorkspace> g_ws;
 
-// Phase timing
+// Phase timing (never in the no-allocation entry point, which creates no
+// events)
 bool g_prof = false;
+bool g_prof_suppressed = false;
 struct PendingEvent {
   int phase;
   hipEvent_t start, stop;
@@ -446,7 +448,7 @@ struct Timer {
   int phase;
   hipEvent_t start = nullptr, stop = nullptr;
   Timer(hipStream_t s, int ph) : stream(s), phase(ph) {
-    if (!g_prof) return;
+    if (!g_prof || g_prof_suppressed) return;
     if (get_event(&start) != hipSuccess || get_event(&stop) != hipSuccess ||
         hipEventRecord(start, stream) != hipSuccess) {
       start = stop = nullptr;
@@ -754,6 +756,101 @@ lm_status step_impl(float* const* params, const float* const* grads, float* cons
   return s;
 }
 
+// ---------------------------------------------------------------------------
+// No-allocation entry point
+// ---------------------------------------------------------------------------
+// Per device: the scratch array's device address and which list signature's
+// tables and which addresses it holds. Calls on one device share the array
+// and must not overlap.
+struct StaticScratch {
+  int device = -1;
+  uint8_t* ptr = nullptr;
+  std::vector<uint8_t> key;               // signature whose tables are resident
+  DevicePlan view;                        // the plan, its tables in scratch (not owned)
+  size_t ws_off = 0;                      // workspace offset in scratch
+};
+std::vector<std::unique_ptr<StaticScratch>> g_static;
+
+lm_status step_noalloc_impl(float* const* params, const float* const* grads,
+                            float* const* momentum, float* const* second_moment,
+                            const lm_shape* shapes, int32_t n, int64_t t, int32_t P, double beta1,
+                            double beta2, double wd, const lm_config* cfg, hipStream_t stream) {
+  if (cfg == nullptr) return fail(LM_ERR_INVALID_ARGUMENT, "null config");
+  lm_status cs = check_config(cfg);
+  if (cs != LM_OK) return cs;
+  std::string err;
+  Status st = lm::validate_scalars(t, P, beta1, beta2, wd, cfg->lr_muon, cfg->lr_lion, &err);
+  if (st != Status::kOk) return fail(to_c(st), err);
+  if (n < 0) return fail(LM_ERR_INVALID_ARGUMENT, "n_tensors must be >= 0");
+  if (n == 0) return LM_OK;
+  if (!params || !grads || !momentum || !shapes) return fail(LM_ERR_INVALID_ARGUMENT, "null tensor array");
+  std::vector<TensorIn> x = gather(params, grads, momentum, second_moment, shapes, n);
+  st = lm::validate_tensors(x.data(), n, &err);
+  if (st != Status::kOk) return fail(to_c(st), err);
+  bool any = false;
+  for (const TensorIn& ti : x) any = any || (ti.rows > 0 && ti.cols > 0);
+  if (!any) return LM_OK;
+  const lm::StepKind kind = step_kind(*cfg, t, P);
+  const bool rms02 = cfg->ns_scale_mode == LM_NS_SCALE_RMS02;
+  const lm::NsPrecision prec = precision_of(*cfg);
+
+  std::lock_guard<std::mutex> lock(g_mu);
+  int device = 0;
+  hipError_t e = hipGetDevice(&device);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  StaticScratch* sc = nullptr;
+  for (auto& d : g_static)
+    if (d->device == device) sc = d.get();
+  if (!sc) {
+    void* ptr = nullptr;
+    e = lm::scratch_address(device, &ptr);
+    if (e != hipSuccess) return hip_fail(e, "scratch: hipGetSymbolAddress");
+    g_static.push_back(std::make_unique<StaticScratch>());
+    sc = g_static.back().get();
+    sc->device = device;
+    sc->ptr = static_cast<uint8_t*>(ptr);
+  }
+  std::vector<uint8_t> key = plan_key(device, x.data(), n, kind, prec, rms02);
+  std::vector<lm::TensorPtrs> bind = binding_of(x.data(), n);
+  if (key != sc->key) {
+    // new signature: plan on the host, check the size limit, then upload
+    // the tables (and the binding) into the scratch array
+    Plan p;
+    st = lm::build_plan(x.data(), n, kind, prec, rms02, chip_of(device), &p, &err);
+    if (st != Status::kOk) return fail(to_c(st), err);
+    TableImage img;
+    pack_tables(p, bind, &img);
+    const size_t ws_off = align256(img.bytes.size());
+    const size_t need = ws_off + p.ws_bytes;
+    if (need > lm::kScratchBytes)
+      return fail(LM_ERR_UNSUPPORTED,
+                  "lionmuon_step_noalloc: this list needs " + std::to_string(need) +
+                      " bytes of device scratch (plan tables and workspace); its static scratch "
+                      "holds at most " + std::to_string(lm::kScratchBytes) +
+                      " bytes (use lionmuon_step_ex for larger lists)");
+    sc->key.clear();                       // invalid until the upload is enqueued
+    e = lm::launch_upload(sc->ptr, img.bytes.data(), img.bytes.size(), stream);
+    if (e != hipSuccess) return hip_fail(e, "scratch: table upload");
+    sc->view.plan = std::move(p);
+    sc->view.bound.swap(bind);
+    point_tables(&sc->view, sc->ptr, img);
+    sc->ws_off = ws_off;
+    sc->key.swap(key);
+  } else if (!same_binding(sc->view.bound, bind)) {
+    e = lm::launch_upload(sc->view.d_bind, bind.data(), bind.size() * sizeof(lm::TensorPtrs),
+                          stream);
+    if (e != hipSuccess) return hip_fail(e, "scratch: address table upload");
+    sc->view.bound.swap(bind);
+  }
+  void* ws = sc->view.plan.ws_bytes > 0 ? sc->ptr + sc->ws_off : nullptr;
+  g_prof_suppressed = true;
+  const lm_status s = enqueue(sc->view, step_consts(beta1, beta2, wd, cfg->lr_muon, cfg->lr_lion,
+                                                    cfg->ns_eps, cfg, t),
+                              *cfg, ws, false, AdaptiveOut(), stream);
+  g_prof_suppressed = false;
+  return s;
+}
+
 }  // namespace
 
 extern "C" {
@@ -804,6 +901,15 @@ lm_status lionmuon_step_ex(float* const* params, const float* const* grads, floa
                            hipStream_t stream) {
   return step_impl(params, grads, momentum, second_moment, shapes, n_tensors, t, P, beta1, beta2,
                    wd, cfg, workspace, workspace_bytes, AdaptiveOut(), stream);
+}
+
+lm_status lionmuon_step_noalloc(float* const* params, const float* const* grads,
+                                float* const* momentum, float* const* second_moment,
+                                const lm_shape* shapes, int32_t n_tensors, int64_t t, int32_t P,
+                                double beta1, double beta2, double wd, const lm_config* cfg,
+                                hipStream_t stream) {
+  return step_noalloc_impl(params, grads, momentum, second_moment, shapes, n_tensors, t, P, beta1,
+                           beta2, wd, cfg, stream);
 }
 
 lm_status lionmuon_step_adaptive(float* const* params, const float* const* grads,

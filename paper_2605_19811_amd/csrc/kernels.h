@@ -100,4 +100,16 @@ hipError_t launch_srank_reduce(const SrankLaunch& a, hipStream_t stream);
 // r_hat = ||M||_F^2 / sigma_hat^2 and the decision r_hat <= alpha * min(m, n).
 hipError_t launch_srank_decide(const SrankLaunch& a, hipStream_t stream);
 
+// No-allocation entry point: one file-scope device array per device (its
+// size is the most a call of that entry point may use: plan tables, address
+// table and workspace together).
+constexpr size_t kScratchBytes = size_t(64) << 20;
+// Device address of the scratch array on `device`, which must be current
+// (looked up on the first call per device, then cached).
+hipError_t scratch_address(int device, void** out);
+// Copy `bytes` (a multiple of 4; dst 4-byte aligned) from host memory to
+// device memory on `stream` through kernel arguments: no staging buffer. The
+// source may be reused as soon as this returns.
+hipError_t launch_upload(void* dst, const void* src, size_t bytes, hipStream_t stream);
+
 }  // namespace lm

@@ -27,8 +27,10 @@ LM_NS_SCALE_NONE = 0
 LM_NS_SCALE_RMS02 = 1
 
 PHASES = ("lion", "prep", "norm", "gram", "poly", "apply", "srank")
+NOALLOC_SCRATCH_BYTES = 64 << 20     # LIONMUON_NOALLOC_SCRATCH_BYTES
 
 EXPORTED = ("lionmuon_config_default", "lionmuon_step", "lionmuon_step_ex",
+            "lionmuon_step_noalloc",
             "lionmuon_step_adaptive",
             "lionmuon_workspace_bytes", "lionmuon_ns", "lionmuon_plan_info",
             "lionmuon_profiling_enable", "lionmuon_profiling_read",
@@ -100,6 +102,9 @@ def library():
     lib.lionmuon_step_ex.argtypes = [vp, vp, vp, vp, P(lm_shape), i32, i64, i32, f64, f64, f64,
                                      P(lm_config), vp, sz, vp]
     lib.lionmuon_step_ex.restype = ctypes.c_int
+    lib.lionmuon_step_noalloc.argtypes = [vp, vp, vp, vp, P(lm_shape), i32, i64, i32, f64, f64,
+                                          f64, P(lm_config), vp]
+    lib.lionmuon_step_noalloc.restype = ctypes.c_int
     lib.lionmuon_step_adaptive.argtypes = [vp, vp, vp, vp, P(lm_shape), i32, i64, f64, f64, f64,
                                            P(lm_config), vp, sz, vp, vp, vp]
     lib.lionmuon_step_adaptive.restype = ctypes.c_int
@@ -299,6 +304,22 @@ def lionmuon_step_ex(params, grads, momentum, t, P, beta1, beta2, wd, cfg: lm_co
                                     int(P), beta1, beta2, wd, ctypes.byref(cfg), ws_ptr, ws_bytes,
                                     _stream_handle(stream))
     _check(st, "lionmuon_step_ex")
+
+
+def lionmuon_step_noalloc(params, grads, momentum, t, P, beta1, beta2, wd, cfg: lm_config,
+                          stream=None, lion_only=None, tensors: TensorList | None = None,
+                          second_moment=None):
+    """lionmuon_step_ex without a workspace, for callers that cannot allocate:
+    the library allocates nothing and uses its static device scratch (at most
+    NOALLOC_SCRATCH_BYTES per device; larger lists raise)."""
+    tl = tensors or TensorList(params, grads, momentum, lion_only, second_moment)
+    st = library().lionmuon_step_noalloc(ctypes.cast(tl.p, ctypes.c_void_p),
+                                         ctypes.cast(tl.g, ctypes.c_void_p),
+                                         ctypes.cast(tl.m, ctypes.c_void_p),
+                                         ctypes.cast(tl.v, ctypes.c_void_p), tl.shapes, tl.n, int(t),
+                                         int(P), beta1, beta2, wd, ctypes.byref(cfg),
+                                         _stream_handle(stream))
+    _check(st, "lionmuon_step_noalloc")
 
 
 def lionmuon_step_adaptive(params, grads, momentum, t, beta1, beta2, wd, cfg: lm_config,
