@@ -163,6 +163,8 @@ def sq_summary(wl_name, sq_csvs, command):
     import csv
     wl = workloads.get(wl_name.replace("-adaptive", ""))
     algo = ns_flops_per_launch(wl)
+    fp32 = wl.ns_precision == "fp32"
+    peak_tflops = FP32_MFMA_PEAK_TFLOPS if fp32 else BF16_PEAK_TFLOPS
     # per phase: counter sums, per-dispatch durations and dispatch counts
     cnt = collections.defaultdict(lambda: collections.defaultdict(float))
     dur = collections.defaultdict(dict)          # phase -> {(pass, dispatch): ns}
@@ -185,7 +187,8 @@ def sq_summary(wl_name, sq_csvs, command):
              "from the pass's own timestamps).", "",
              "- `algorithmic frac`: the phase's symmetric flop count (Gram s(s+1)l, polynomial "
              "s^2(s+1), apply 2 s^2 l per matrix) over the launch duration, against the dense "
-             "bf16 peak 2516.6 TFLOP/s (256 CUs x 2.4 GHz x 4096 flop/clk).",
+             "MFMA peak of the path's type: bf16 2516.6 TFLOP/s (256 CUs x 2.4 GHz x 4096 "
+             "flop/clk), fp32 157.3 TFLOP/s" + (" (this workload: fp32)." if fp32 else "."),
              "- `issued frac`: 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16 (+_F32) flops over the same "
              "duration and peak: the MFMA work the kernels actually execute.",
              "- `issued / algorithmic`: MFMA work spent per useful flop. Above 1 where a "
@@ -211,7 +214,7 @@ def sq_summary(wl_name, sq_csvs, command):
         t_ns = sum(dur[ph].values()) / launches
         issued = 512.0 * (c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) +
                           c.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0.0)) / launches
-        peak = BF16_PEAK_TFLOPS * 1e12 * t_ns * 1e-9
+        peak = peak_tflops * 1e12 * t_ns * 1e-9
         cycles = c.get("GRBM_GUI_ACTIVE", 0.0) / XCDS / launches
         util = c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / launches / (cycles * SIMDS) if cycles else 0.0
         clock = cycles / t_ns if t_ns else 0.0
@@ -227,7 +230,21 @@ def sq_summary(wl_name, sq_csvs, command):
     return path
 
 
-def trace_summary(wl_name, stats_csv, command):
+def launch_gaps(trace_csv):
+    """Idle time between consecutive library kernels in a rocprofv3 kernel
+    trace: gaps shorter than 50 us (back-to-back launches of one step; longer
+    ones are host-side pauses between timed regions)."""
+    import csv
+    ev = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
+                for r in csv.DictReader(open(trace_csv)) if phase_of(r["Kernel_Name"]))
+    gaps = [b[0] - a[1] for a, b in zip(ev, ev[1:]) if 0 <= b[0] - a[1] < 50000]
+    busy = sum(e - s for s, e in ev)
+    return {"launches": len(ev), "gaps": len(gaps),
+            "mean_gap_us": sum(gaps) / len(gaps) / 1e3 if gaps else 0.0,
+            "gap_share": sum(gaps) / (sum(gaps) + busy) if ev else 0.0}
+
+
+def trace_summary(wl_name, stats_csv, command, trace_csv=None):
     """Text summary of a rocprofv3 --kernel-trace --stats run."""
     import csv
     rows = list(csv.DictReader(open(stats_csv)))
@@ -259,6 +276,11 @@ def trace_summary(wl_name, stats_csv, command):
     for ph, t in sorted(tot.items(), key=lambda kv: -kv[1]["ns"]):
         n = t["n_decide"] if ph == "srank" else (t["n_256"] or t["n_all"])
         lines.append(f"| {ph} | {n} | {t['ns'] / n / 1e3:.1f} |")
+    if trace_csv:
+        g = launch_gaps(trace_csv)
+        lines += ["", f"Between consecutive library kernels (per-dispatch timestamps, {g['launches']} "
+                  f"dispatches): mean idle gap {g['mean_gap_us']:.2f} us over {g['gaps']} "
+                  f"back-to-back pairs, {100 * g['gap_share']:.1f}% of the kernels' timeline."]
     path = os.path.join(TRAFFIC_DIR, f"kernel_trace_{wl_name}.md")
     with open(path, "w") as f:
         f.write("\n".join(lines) + "\n")
@@ -544,7 +566,9 @@ def main():
                           commands=args.command))
         return
     if args.trace_summary:
-        print(trace_summary(prof_name, args.trace_summary, args.command))
+        trace_csv = args.trace_summary.replace("kernel_stats.csv", "kernel_trace.csv")
+        print(trace_summary(prof_name, args.trace_summary, args.command,
+                            trace_csv if os.path.exists(trace_csv) else None))
         return
     if args.sq_summary:
         print(sq_summary(prof_name, args.sq_summary, args.command))
