@@ -1223,7 +1223,8 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   };
   constexpr int kSub = kBK / M::kKStep;
   // bf16 apply: the B fragments of a whole stage are read into registers
-  // (transpose reads) before the next stage's copies are issued.
+  // (transpose reads) at the start of the stage, right after the next
+  // stage's copies are issued.
   constexpr bool kTrB = kBRows && sizeof(T) == 2;
   typename M::Frag bq[kTrB ? kSub : 1][kNI];
   // The 16 (64-tiles: 8) transpose reads of a stage are one assembly block that ends by
@@ -1388,15 +1389,18 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   lds_barrier();
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & (kNBuf - 1);
+    // the next stage's copies go out first, into the buffer of stage kt - 1,
+    // which every wave finished before the barrier that ended the previous
+    // step: their issue (which stalls while the memory pipeline is full)
+    // then overlaps this stage's transpose reads (an assembly block: the
+    // compiler adds no wait for the copies before it)
+    const int nxt = kt + kNBuf - 1;
+    if (nxt < nk) dma(ops, nxt & (kNBuf - 1), nxt * kBK);
+    __builtin_amdgcn_sched_barrier(0);
     if constexpr (kTrB) {
       preload_b(buf);
       __builtin_amdgcn_sched_barrier(0);
     }
-    // the buffer of stage kt - 1, which every wave finished before the
-    // barrier that ended the previous step
-    const int nxt = kt + kNBuf - 1;
-    if (nxt < nk) dma(ops, nxt & (kNBuf - 1), nxt * kBK);
-    __builtin_amdgcn_sched_barrier(0);
     compute(buf);
     __builtin_amdgcn_sched_barrier(0);
     wait_stage(nk - 2 - kt, false);              // stage kt + 1
