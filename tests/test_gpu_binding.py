@@ -202,3 +202,48 @@ def test_inf_gradients_propagate_like_the_oracle():
             assert np.isfinite(w[3, 5]) and np.isnan(w[10, 20])
             fin = np.isfinite(w_ref)
             assert np.abs(w[fin] - w_ref[fin]).max() <= 1e-6 * np.abs(w_ref[fin]).max()
+
+
+def test_plan_eviction_and_return():
+    """Twenty lists of different signatures (more than the 16 cached plans),
+    a Lion step each, then the first signature again (its plan was evicted and
+    is rebuilt): every step matches the oracle."""
+    rng = np.random.default_rng(77)
+    shapes = [[(64 + 8 * i, 96), (1, 300 + i)] for i in range(20)] + [[(64, 96), (1, 300)]]
+    for k, shp in enumerate(shapes):
+        W0 = [(rng.standard_normal(s) * 0.02).astype(np.float32) for s in shp]
+        M0 = [(rng.standard_normal(s) * 1e-2).astype(np.float32) for s in shp]
+        G = [(rng.standard_normal(s) * 1e-2).astype(np.float32) for s in shp]
+        W, M = [dev(x) for x in W0], [dev(x) for x in M0]
+        lm.lionmuon_step([W[0], W[1].view(-1)], [dev(G[0]), dev(G[1]).view(-1)],
+                         [M[0], M[1].view(-1)], t=1, P=2, beta1=0.9, beta2=0.99, lr=0.01, wd=0.1)
+        torch.cuda.synchronize()
+        for i in range(2):
+            check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 0.01, 0.1)
+
+
+def test_staging_ring_wraps_and_single_address_changes():
+    """A list of 600 small tensors (19 KB of addresses per call) stepped 70
+    times with one gradient tensor replaced by a fresh one on every call, so
+    the address table is rewritten each time and the 1 MB staging ring wraps
+    around; every tensor is checked on the last calls."""
+    n = 600
+    rng = np.random.default_rng(78)
+    sizes = [int(rng.integers(1, 300)) for _ in range(n)]
+    W0 = [(rng.standard_normal(k) * 0.02).astype(np.float32) for k in sizes]
+    M0 = [(rng.standard_normal(k) * 1e-2).astype(np.float32) for k in sizes]
+    G = [(rng.standard_normal(k) * 1e-2).astype(np.float32) for k in sizes]
+    Gd = [dev(g) for g in G]
+    keep = []
+    for call in range(70):
+        W, M = [dev(x) for x in W0], [dev(x) for x in M0]
+        j = call % n
+        fresh = dev(G[j])                          # new address for tensor j only
+        keep.append(fresh)
+        grads = list(Gd)
+        grads[j] = fresh
+        lm.lionmuon_step(W, grads, M, t=1, P=2, beta1=0.9, beta2=0.99, lr=0.01, wd=0.1)
+        if call >= 67:
+            torch.cuda.synchronize()
+            for i in range(n):
+                check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 0.01, 0.1)
