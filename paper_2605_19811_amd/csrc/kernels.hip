@@ -189,6 +189,10 @@ __device__ __forceinline__ void store4(float* p, const float v[4]) {
   const f32x4 x = {v[0], v[1], v[2], v[3]};
   *reinterpret_cast<f32x4*>(p) = x;
 }
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const bf16 a = bf16(lo), b = bf16(hi);
+  return uint32_t(__builtin_bit_cast(uint16_t, a)) | (uint32_t(__builtin_bit_cast(uint16_t, b)) << 16);
+}
 __device__ __forceinline__ void load4(const bf16* p, float v[4]) {
   const bf16x4 x = *reinterpret_cast<const bf16x4*>(p);
   v[0] = float(x[0]); v[1] = float(x[1]); v[2] = float(x[2]); v[3] = float(x[3]);
@@ -1098,6 +1102,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // they drain. kDirect is the number of those stores per lane.
   constexpr int kDirect = Geo::kMI * Geo::kNI * 4;
   bool prefetched = false;
+  int base = 0;                                  // LDS buffer of the tile's first K stage
   for (int slot = live(int(blockIdx.x) / xcds); slot < count;) {
   // Lane-derived values are recomputed for every tile (the empty asm keeps
   // the compiler from hoisting them out of the tile loop, where they would
@@ -1117,12 +1122,11 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // Each wave instruction fills 8 rows (1 KB): lane L writes row L/8,
   // physical chunk L%8, and fetches the logical chunk that lands there.
   constexpr int kWaves = kNT / 64;
-  // Waves that issue the operand copies: in the 256-tile apply only the first
-  // four (one per SIMD), so that the other wave of each SIMD keeps the matrix
-  // core busy while the issuing wave stalls on a full memory pipeline
-  // (measured: apply 0.5-0.9% faster at 124M-720M; the same for the Gram and
-  // polynomial products made them up to 2% slower).
-  constexpr int kDmaWaves = (BT == 256 && MODE == kApply) ? kWaves / 2 : kWaves;
+  // Waves that issue the operand copies: on 256-tiles only the first four
+  // (one per SIMD), so that the other wave of each SIMD keeps the matrix core
+  // busy while the issuing wave stalls on a full memory pipeline (measured:
+  // apply 0.5-0.9%, Gram 1-4%, polynomial 0-2.5% faster at 124M-720M).
+  constexpr int kDmaWaves = (BT == 256) ? kWaves / 2 : kWaves;
   constexpr int kInst = BT / 8 / kDmaWaves;      // wave instructions per operand per stage
   // k-major B rows (apply): kChunksB 16-byte chunks per row, each wave
   // instruction fills kRpiB rows; chunks are XOR-swizzled by swb(k) so that
@@ -1178,23 +1182,33 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
         : uint32_t(((dw * 8 + (lane >> 3)) * o.ldb + ((lane & 7) ^ swz(dw * 8 + (lane >> 3))) * kEpc) * sizeof(T));
     return o;
   };
-  auto gsrc = [](const T* base, uint32_t off) {
-    return reinterpret_cast<const void*>(reinterpret_cast<const char*>(base) + off);
+  // One 16-byte-per-lane copy in the scalar-base form: wave-uniform base
+  // address and LDS destination (M0, one wait state after writing it) in
+  // scalar registers, one 32-bit offset per lane. Written as an assembly
+  // block: from the builtin, inside the K loop, the compiler formed 64-bit
+  // per-lane addresses and moved M0 from vector registers for every copy
+  // (apply 2-5%, polynomial 5% slower). The compiler neither counts these
+  // copies nor waits for them: every wait for them is explicit (wait_stage).
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  auto copy16 = [&](const T* src, uint32_t off, const T* dst) {
+    const uint32_t d = uint32_t(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const T*)(dst)));
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :: "v"(off), "s"(src), "s"(d) : "memory", "m0");
   };
   auto dma = [&](const Ops& o, int buf, int k0) {
-    if (wave >= kDmaWaves) return;
+    if (wave_u >= kDmaWaves) return;
 #pragma unroll
     for (int q = 0; q < kInst; ++q) {
-      const int blk = q * kDmaWaves + wave;      // 8-row block
-      __builtin_amdgcn_global_load_lds(gsrc(o.a + int64_t(q * kDmaWaves * 8) * o.lda + k0, o.a_off), &sA[buf][blk * 8][0], 16, 0, 0);
+      const int blk = q * kDmaWaves + wave_u;    // 8-row block
+      copy16(o.a + int64_t(q * kDmaWaves * 8) * o.lda + k0, o.a_off, &sA[buf][blk * 8][0]);
       if constexpr (!kBRows)
-        __builtin_amdgcn_global_load_lds(gsrc(o.b + int64_t(q * kDmaWaves * 8) * o.ldb + k0, o.b_off), &sB[buf][blk * 8][0], 16, 0, 0);
+        copy16(o.b + int64_t(q * kDmaWaves * 8) * o.ldb + k0, o.b_off, &sB[buf][blk * 8][0]);
     }
     if constexpr (kBRows) {
 #pragma unroll
       for (int q = 0; q < kInstB; ++q) {
-        const int rr = (q * kDmaWaves + wave) * kRpiB;  // first of the instruction's rows
-        __builtin_amdgcn_global_load_lds(gsrc(o.b + int64_t(k0 + q * kDmaWaves * kRpiB) * o.ldb, o.b_off), &sBr[buf][rr][0], 16, 0, 0);
+        const int rr = (q * kDmaWaves + wave_u) * kRpiB;  // first of the instruction's rows
+        copy16(o.b + int64_t(k0 + q * kDmaWaves * kRpiB) * o.ldb, o.b_off, &sBr[buf][rr][0]);
       }
     }
   };
@@ -1387,23 +1401,31 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
     }
   };
   // stages 0 .. kNBuf - 2 in flight before the first MFMA (stage 0 may have
-  // been requested already, before the previous tile's stores)
-  if (!prefetched) dma(ops, 0, 0);
+  // been requested already, during the previous tile's last K stage)
+  if (!prefetched) dma(ops, base, 0);
 #pragma unroll
   for (int st = 1; st < kNBuf - 1; ++st)
-    if (st < nk) dma(ops, st, st * kBK);
+    if (st < nk) dma(ops, (base + st) & (kNBuf - 1), st * kBK);
   wait_stage(nk - 1, prefetched);
   prefetched = false;
   lds_barrier();
+  // persistent apply: the next tile's first stage is requested at the start
+  // of this tile's last stage, into the buffer no stage of this tile uses
+  // then, so that it lands during that stage and the epilogue
+  const int nslot = live(slot + step);
   for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & (kNBuf - 1);
+    const int buf = (base + kt) & (kNBuf - 1);
     // the next stage's copies go out first, into the buffer of stage kt - 1,
     // which every wave finished before the barrier that ended the previous
     // step: their issue (which stalls while the memory pipeline is full)
     // then overlaps this stage's transpose reads (an assembly block: the
     // compiler adds no wait for the copies before it)
     const int nxt = kt + kNBuf - 1;
-    if (nxt < nk) dma(ops, nxt & (kNBuf - 1), nxt * kBK);
+    if (nxt < nk) dma(ops, (base + nxt) & (kNBuf - 1), nxt * kBK);
+    if (kPersistent && kt == nk - 1 && nslot < count) {
+      dma(make_ops(tasks[nslot]), (base + nk) & (kNBuf - 1), 0);
+      prefetched = true;
+    }
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (kTrB) {
       preload_b(buf);
@@ -1411,12 +1433,14 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
     }
     compute(buf);
     __builtin_amdgcn_sched_barrier(0);
-    wait_stage(nk - 2 - kt, false);              // stage kt + 1
+    // stage kt + 1 (after the last stage nothing: the next tile's first
+    // stage stays in flight)
+    if (kt < nk - 1) wait_stage(nk - 2 - kt, false);
     lds_barrier();
   }
   // (the barrier after the last stage means no wave reads the operand
   // buffers any more)
-  const int nslot = live(slot + step);
+  if (kPersistent) base = (base + nk) & (kNBuf - 1);
 
   // ---- epilogues ----------------------------------------------------------
   // The Gram and polynomial results leave through LDS: each lane writes its
@@ -1523,27 +1547,63 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
           for (int r = 0; r < 16; ++r) acc[mi][ni][r] *= alpha;
     }
     if constexpr (!LAST) {
-      if (nslot < count) {
-        dma(make_ops(tasks[nslot]), 0, 0);
-        prefetched = true;
-      }
-      // each quad of lanes transposes its 4 x 4 blocks (DPP) so that every
-      // lane stores 4 consecutive columns of one row
       T* out = at(off_x_nxt) + row0 * l_pad + col0;
       const int b = lane & 3;
+      if constexpr (sizeof(T) == 2 && kNI == 2) {
+        // Each quad of lanes transposes its 4 x 4 blocks (DPP), so that a
+        // lane holds 4 consecutive columns of one row in each of the two
+        // column blocks; then the two half-waves trade the second block of
+        // the first half's rows for the first block of the second half's
+        // (v_permlane32_swap). One store then writes 4 rows x 64 columns,
+        // four whole 128-byte lines, where 8 rows x 32 columns (eight half
+        // lines) took twice as long per byte. The stores are non-temporal:
+        // a round of tiles writes as many bytes of X' as the L2 caches of
+        // all XCDs hold, and would otherwise evict the operands the next
+        // tiles read (apply 3.7% faster at 124M, 1.5% slower at 355M).
 #pragma unroll
-      for (int mi = 0; mi < kMI; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < kNI; ++ni)
+        for (int mi = 0; mi < kMI; ++mi)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            float v[4];
+            uint32_t h0[2], h1[2];               // rows 8 q + 4 lk + b, column block 0 / 1
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = acc[mi][ni][4 * q + e];
-            quad_transpose(v, b);
-            const int r = wm + 32 * mi + 8 * q + 4 * lk + b, c = wn + 32 * ni + (lr & ~3);
-            store4(out + r * l_pad + c, v);
+            for (int ni = 0; ni < 2; ++ni) {
+              float v[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = acc[mi][ni][4 * q + e];
+              quad_transpose(v, b);
+              uint32_t* h = ni == 0 ? h0 : h1;
+              h[0] = pack_bf16x2(v[0], v[1]);
+              h[1] = pack_bf16x2(v[2], v[3]);
+            }
+            // lanes 32..63 of h0 <-> lanes 0..31 of h1: then h0 holds row
+            // 8 q + b and h1 row 8 q + 4 + b, column block lk
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+              const auto sw = __builtin_amdgcn_permlane32_swap(h0[k], h1[k], false, false);
+              h0[k] = sw[0];
+              h1[k] = sw[1];
+            }
+            const int r = wm + 32 * mi + 8 * q + b, c = wn + 32 * lk + (lr & ~3);
+            __builtin_nontemporal_store(u32x2{h0[0], h0[1]}, reinterpret_cast<u32x2*>(out + r * l_pad + c));
+            __builtin_nontemporal_store(u32x2{h1[0], h1[1]}, reinterpret_cast<u32x2*>(out + (r + 4) * l_pad + c));
           }
+      } else {
+        // each quad of lanes transposes its 4 x 4 blocks (DPP) so that every
+        // lane stores 4 consecutive columns of one row
+#pragma unroll
+        for (int mi = 0; mi < kMI; ++mi)
+#pragma unroll
+          for (int ni = 0; ni < kNI; ++ni)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              float v[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = acc[mi][ni][4 * q + e];
+              quad_transpose(v, b);
+              const int r = wm + 32 * mi + 8 * q + 4 * lk + b, c = wn + 32 * ni + (lr & ~3);
+              store4(out + r * l_pad + c, v);
+            }
+      }
     } else {
       // last step: W <- W - lr (kappa O + wd W), or O = kappa X_K (NS hook).
       // O is X_K, transposed back for tall matrices. The fp32 O tile goes
