@@ -379,11 +379,16 @@ class Bench:
         self.specs = [(t.rows, t.cols, t.lion_only) for t in wl.tensors]
         self.stream = torch.cuda.current_stream()
 
-    def close(self):
+    def close(self, release=True):
+        """Free the device state; with `release`, also the library's plans
+        and workspaces and torch's cached blocks (the next call rebuilds its
+        plan; both take host-side waits during which the GPU idles)."""
         del self.lists, self.params, self.moms, self.grad_sets
-        self.lm.lionmuon_release()
+        if release:
+            self.lm.lionmuon_release()
         self.torch.cuda.synchronize()
-        self.torch.cuda.empty_cache()
+        if release:
+            self.torch.cuda.empty_cache()
 
     def run(self, t0, n, P, beta1, beta2, cfg, n_lists=None):
         k_lists = n_lists or len(self.lists)
@@ -600,8 +605,19 @@ def main():
     P = 1 if args.pure_muon else args.P
     beta = (0.9, 0.9) if args.pure_muon else (None, None)
     adaptive = args.adaptive > 0.0
-    log(f"{wl.name} P={P}{' adaptive' if adaptive else ''}")
+    cpu = not args.no_cpu_baseline and not adaptive
     b = Bench(torch, lm, wl, n_grad=max(1, args.grad_sets))
+    configs = None
+    if not args.single and not adaptive:
+        # The other configurations run first and the headline's steps follow
+        # their GPU work at once: after an idle spell (a fresh process, the
+        # host-side set-up of a workload, or the allocation of a new plan's
+        # workspace) the core clock needs ~20 ms of sustained MFMA load to
+        # settle (the first 124M Muon steps take up to ~2.1 ms, the tenth
+        # ~1.7; Lion steps, bound by HBM, do not change), which would
+        # otherwise fall inside the headline's 20 timed steps.
+        configs = other_configs(torch, lm, args, wl.name, P, profile, cpu, log)
+    log(f"{wl.name} P={P}{' adaptive' if adaptive else ''}")
     res = b.measure(P, args.steps, args.warmup, beta[0], beta[1], args.adaptive,
                     args.power_steps, profile)
     info = lm.lionmuon_plan_info(b.specs, 0, 1, lm.config(ns_precision=wl.ns_precision))
@@ -631,12 +647,11 @@ def main():
               "ns_ms_per_muon_step", "split", "lion_gbps", "lion_frac_hbm_peak", "roofline"):
         if k in res:
             out[k] = res[k]
-    cpu = not args.no_cpu_baseline and not adaptive
     if cpu:
         log("cpu baseline")
         out["cpu_baseline"] = cpu_baseline_for(cpu_oracle_times(wl, 10.0), P)
-    if not args.single and not adaptive:
-        out["configs"] = other_configs(torch, lm, args, wl.name, P, profile, cpu, log)
+    if configs is not None:
+        out["configs"] = configs
     print(json.dumps(out), flush=True)
 
 
@@ -699,7 +714,10 @@ def other_configs(torch, lm, args, main_name, main_P, profile, cpu, log):
     for _ in range(2):
         fixed.append(b.measure(main_P, n_addr, args.warmup, profile=False, n_lists=1)["ms_per_step"])
         rot.append(b.measure(main_P, n_addr, args.warmup, profile=False, n_lists=4)["ms_per_step"])
-    b.close()
+    # (the headline set's plans and torch's blocks stay: the headline's steps
+    # then follow this GPU work without an idle spell of plan building or of
+    # returning memory, during which the clock would drop)
+    b.close(release=False)
     out[f"gradient_addresses_{main_name}"] = {
         "fixed_ms_per_step": min(fixed), "rotating4_ms_per_step": min(rot),
         "ratio": round(min(rot) / min(fixed), 4), "steps": n_addr, "regions": {"fixed": fixed,
