@@ -511,14 +511,17 @@ class Bench:
         # dominant kernel: most total time in the timed region
         dom = max((p for p in phases if phases[p]["launches"]), key=lambda p: phases[p]["ms"])
         d = ph[dom]
+        kname = KERNEL_NAMES[dom]
+        if wl.ns_precision != "bf16":
+            kname = kname.replace("<bf16>", "<float>")
         if "tflops" in d:
-            roof = {"kernel": KERNEL_NAMES[dom], "bound": "mfma", "achieved": d["tflops"],
+            roof = {"kernel": kname, "bound": "mfma", "achieved": d["tflops"],
                     "peak": peak_mfma, "unit": "TFLOP/s", "frac": d["frac_mfma_peak"]}
         elif "gbps" in d:
-            roof = {"kernel": KERNEL_NAMES[dom], "bound": "hbm", "achieved": d["gbps"],
+            roof = {"kernel": kname, "bound": "hbm", "achieved": d["gbps"],
                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": d["frac_hbm_peak"]}
         else:
-            roof = {"kernel": KERNEL_NAMES[dom], "bound": "hbm", "achieved": None,
+            roof = {"kernel": kname, "bound": "hbm", "achieved": None,
                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": None}
         roof["avg_launch_ms"] = d["avg_ms"]
         roof["traffic"] = load_traffic(wl.name + ("-adaptive" if adaptive_on else ""), dom)
