@@ -286,6 +286,30 @@ def test_apply_small_tile_round_on_ragged_matrices(last):
         check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_m, wd, "bf16")
 
 
+def test_persistent_apply_tiles_of_different_depth():
+    """528 apply 256-tiles from matrices whose short sides (256, 512, 768)
+    give K loops of 4, 8 and 12 stages: every persistent workgroup runs two
+    tiles, 32 list positions apart in its XCD's segment, so its two tiles
+    come from different matrices, and the next tile's first K stage, issued
+    during the current tile's last stage, lands in the buffer left free by a
+    tile of another depth (the 16 tiles of the last round run as 64-tiles).
+    Every matrix is checked."""
+    shapes = []
+    for r in range(12):
+        shapes += [(256, 4096), (512, 2048) if r % 2 == 0 else (2048, 512), (768, 1024)]
+    info = lm.lionmuon_plan_info([(*sh, False) for sh in shapes], t=0, P=1)
+    assert info["apply_tiles"] == 512 + 16 * 16
+    W0, M0, G = _state(shapes, 91)
+    W, M, Gd = [dev(x) for x in W0], [dev(x) for x in M0], [dev(x) for x in G]
+    lr_m, wd = 0.02, 0.1
+    cfg = lm.config(ns_precision="bf16", lr_muon=lr_m, lr_lion=1e-3)
+    print("persistent apply, tiles of 4, 8 and 12 K stages", flush=True)
+    lm.lionmuon_step_ex(W, Gd, M, 0, 1, 0.9, 0.99, wd, cfg)
+    sync()
+    for i in range(len(shapes)):
+        check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_m, wd, "bf16")
+
+
 def test_many_small_tensors_in_one_call():
     """2000 tensors of random small shapes (1-D, tall, wide, square, some
     empty) in one call: the multi-tensor Lion grid, the per-matrix
