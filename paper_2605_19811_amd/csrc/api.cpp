@@ -617,16 +617,14 @@ lm_status enqueue(const DevicePlan& dp, const lm::StepConsts& k, const lm_config
         gl.max_count = sp.max_count;
         gl.fp32 = pr;
         gl.tile = p.tile[pr][st3];
+        // the apply's last round as smaller tiles, in the same launch
+        const bool tail = st3 == 2 && p.apply_tail_split[pr].max_count > 0;
+        gl.tail_tasks = tail ? dp.d_tasks[pr][3] : nullptr;
+        gl.tail_split = tail ? dp.d_splits + pr * 4 + 3 : nullptr;
+        gl.tail_max_count = tail ? p.apply_tail_split[pr].max_count : 0;
+        gl.tail_tile = tail ? p.tail_tile[pr] : 0;
         e = lm::launch_gemm(modes[st3], gl, stream);
         if (e != hipSuccess) return hip_fail(e, "Newton-Schulz kernel launch");
-        if (st3 == 2 && p.apply_tail_split[pr].max_count > 0) {   // the last round, as smaller tiles
-          gl.tasks = dp.d_tasks[pr][3];
-          gl.split = dp.d_splits + pr * 4 + 3;
-          gl.max_count = p.apply_tail_split[pr].max_count;
-          gl.tile = p.tail_tile[pr];
-          e = lm::launch_gemm(modes[st3], gl, stream);
-          if (e != hipSuccess) return hip_fail(e, "Newton-Schulz kernel launch");
-        }
       }
       t.done();
     }

@@ -66,6 +66,12 @@ struct GemmLaunch {
   int32_t fp32;                  // element type of the matrices in `tasks`
   int32_t tile;                  // output tile edge of `tasks`: 128 or 256
   const int32_t* decide;         // adaptive: tiles of matrices with decision 0 exit
+  // apply on bf16 256-tiles only: the last round's smaller tiles (64 or 128),
+  // run by extra workgroups of the same launch; none when tail_max_count is 0
+  const GemmTask* tail_tasks = nullptr;   // device, grouped by XCD segment
+  const XcdSplit* tail_split = nullptr;   // device
+  int32_t tail_max_count = 0;             // largest segment (host copy)
+  int32_t tail_tile = 0;
 };
 hipError_t launch_gemm(GemmMode mode, const GemmLaunch& a, hipStream_t stream);
 

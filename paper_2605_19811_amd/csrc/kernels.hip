@@ -1046,11 +1046,29 @@ struct GemmArgs {
   float a, b, c, lr, wd;
 };
 
+// LDS of one product tile: kNBuf operand stages during the K loop, then the
+// output tile (the kernel declares it; the tile body takes a pointer).
+template <typename T, int MODE, int BT>
+struct GemmLds {
+  static constexpr int kLd = Mfma<T>::kBK;      // LDS row: 128 bytes
+  static constexpr int kStR = BT + 16;          // row-major staging row stride
+  // Two stages, except for the bf16 apply on 128- or 64-tiles (a nearly
+  // empty last round of 256-tiles, one or two such workgroups per CU and too
+  // few of them to hide load latency with other workgroups): four, three of
+  // them in flight while one feeds the MFMAs.
+  static constexpr int kNBuf = (MODE == kApply && BT <= 128 && sizeof(T) == 2) ? 4 : 2;
+  static constexpr int kOperand = kNBuf * 2 * BT * kLd, kStage = BT * kStR;
+  static constexpr int kElems = kOperand > kStage ? kOperand : kStage;
+  static constexpr int kBytes = kElems * int(sizeof(T));
+};
+
 // LAST (apply only): the last Newton-Schulz step, whose epilogue updates W
 // (its own instantiation: that epilogue's registers would otherwise weigh
-// on every other apply step).
+// on every other apply step). `smem` is the kernel's LDS block (at least
+// GemmLds<T, MODE, BT>::kBytes); the workgroup is number `bid` of the `nblk`
+// that run this task list (workgroup i on XCD i mod xcds).
 template <typename T, int MODE, int BT, bool LAST = false>
-__device__ __forceinline__ void gemm_body(const GemmArgs& g) {
+__device__ __forceinline__ void gemm_body(const GemmArgs& g, T* smem, int bid, int nblk) {
   using M = Mfma<T>;
   using Geo = TileGeom<BT>;
   constexpr int kBK = M::kBK;
@@ -1058,19 +1076,13 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   constexpr int kLd = kBK;                       // LDS row: 128 bytes, chunks XOR-swizzled
   constexpr int kNT = Geo::kThreads;
   constexpr int kMI = Geo::kMI, kNI = Geo::kNI;
-  // One LDS block: kNBuf operand stages during the K loop, then the output
-  // tile. Two stages, except for the bf16 apply on 128- or 64-tiles (a nearly
-  // empty last round of 256-tiles, one or two such workgroups per CU and too
-  // few of them to hide load latency with other workgroups): four, three of
-  // them in flight while one feeds the MFMAs.
   // Output staging row strides: kStR for row-major staging (16-byte-aligned
   // rows, 8 or 16 dwords apart modulo the 64 banks, so a quad of lanes
   // writing 4 consecutive rows never collides), kStC for transposed staging
   // (4 dwords apart, so 16 lanes writing 16 consecutive rows never collide).
-  constexpr int kStR = BT + 16, kStC = BT + kEpc;
-  constexpr int kNBuf = (MODE == kApply && BT <= 128 && sizeof(T) == 2) ? 4 : 2;
-  constexpr int kOperand = kNBuf * 2 * BT * kLd, kStage = BT * kStR;
-  __shared__ __attribute__((aligned(16))) T smem[kOperand > kStage ? kOperand : kStage];
+  using L = GemmLds<T, MODE, BT>;
+  constexpr int kStR = L::kStR, kStC = BT + kEpc;
+  constexpr int kNBuf = L::kNBuf;
   T (*sA)[BT][kLd] = reinterpret_cast<T (*)[BT][kLd]>(smem);
   T (*sB)[BT][kLd] = reinterpret_cast<T (*)[BT][kLd]>(smem + kNBuf * BT * kLd);
   // apply: the B operand (X, K = s along its rows) is staged k-major as
@@ -1087,10 +1099,10 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // workgroup, so a finished workgroup's successor starts at once.
   constexpr bool kPersistent = MODE == kApply && !LAST;
   const int xcds = g.xcds;
-  const int xcd = int(blockIdx.x) % xcds;
+  const int xcd = bid % xcds;
   const int count = kconst(g.split)->count[xcd];
   const auto* tasks = kconst(g.tasks) + kconst(g.split)->start[xcd];
-  const int step = int(gridDim.x) / xcds;
+  const int step = nblk / xcds;
   auto live = [&](int s) {
     while (s < count && g.decide && kconst(g.decide)[tasks[s].mat] == 0) s += step;
     return s;
@@ -1103,7 +1115,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   constexpr int kDirect = Geo::kMI * Geo::kNI * 4;
   bool prefetched = false;
   int base = 0;                                  // LDS buffer of the tile's first K stage
-  for (int slot = live(int(blockIdx.x) / xcds); slot < count;) {
+  for (int slot = live(bid / xcds); slot < count;) {
   // Lane-derived values are recomputed for every tile (the empty asm keeps
   // the compiler from hoisting them out of the tile loop, where they would
   // stay live, in registers, through the epilogue).
@@ -1189,6 +1201,8 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
   // per-lane addresses and moved M0 from vector registers for every copy
   // (apply 2-5%, polynomial 5% slower). The compiler neither counts these
   // copies nor waits for them: every wait for them is explicit (wait_stage).
+  // M0 is reserved to the compiler, which does not track the clobber; no
+  // other code in these kernels uses M0.
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   auto copy16 = [&](const T* src, uint32_t off, const T* dst) {
     const uint32_t d = uint32_t(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const T*)(dst)));
@@ -1697,19 +1711,44 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g) {
 // One entry point per Newton-Schulz product, so profiles name each stage.
 template <typename T, int BT>
 __global__ __launch_bounds__(TileGeom<BT>::kThreads) void ns_gram_kernel(GemmArgs g) {
-  gemm_body<T, kGram, BT>(g);
+  __shared__ __attribute__((aligned(16))) char lds[GemmLds<T, kGram, BT>::kBytes];
+  gemm_body<T, kGram, BT>(g, reinterpret_cast<T*>(lds), int(blockIdx.x), int(gridDim.x));
 }
 template <typename T, int BT>
 __global__ __launch_bounds__(TileGeom<BT>::kThreads) void ns_poly_kernel(GemmArgs g) {
-  gemm_body<T, kPoly, BT>(g);
+  __shared__ __attribute__((aligned(16))) char lds[GemmLds<T, kPoly, BT>::kBytes];
+  gemm_body<T, kPoly, BT>(g, reinterpret_cast<T*>(lds), int(blockIdx.x), int(gridDim.x));
 }
 template <typename T, int BT>
 __global__ __launch_bounds__(TileGeom<BT>::kThreads) void ns_apply_kernel(GemmArgs g) {
-  gemm_body<T, kApply, BT>(g);
+  __shared__ __attribute__((aligned(16))) char lds[GemmLds<T, kApply, BT>::kBytes];
+  gemm_body<T, kApply, BT>(g, reinterpret_cast<T*>(lds), int(blockIdx.x), int(gridDim.x));
 }
 template <typename T, int BT>
 __global__ __launch_bounds__(TileGeom<BT>::kThreads) void ns_apply_last_kernel(GemmArgs g) {
-  gemm_body<T, kApply, BT, true>(g);
+  __shared__ __attribute__((aligned(16))) char lds[GemmLds<T, kApply, BT>::kBytes];
+  gemm_body<T, kApply, BT, true>(g, reinterpret_cast<T*>(lds), int(blockIdx.x), int(gridDim.x));
+}
+// An apply step's 256-tiles and the small tiles of its last round in one
+// launch: the first `main_grid` workgroups run the 256-tiles, the rest the
+// small tiles, so that each small tile starts as soon as a CU frees up
+// rather than after the whole 256-tile launch (and one launch gap less).
+// The waves a small tile does not use exit at once; a barrier waits only for
+// the waves still running. main_grid is a multiple of the XCD count, so a
+// small tile's workgroup number keeps its XCD.
+template <typename T, int BT, int TT, bool LAST>
+__global__ __launch_bounds__(TileGeom<BT>::kThreads) void ns_apply_pair_kernel(GemmArgs g, GemmArgs tail,
+                                                                                int32_t main_grid) {
+  static_assert(TileGeom<TT>::kThreads <= TileGeom<BT>::kThreads, "small tiles use fewer waves");
+  constexpr int kBytes = GemmLds<T, kApply, BT>::kBytes > GemmLds<T, kApply, TT>::kBytes
+                             ? GemmLds<T, kApply, BT>::kBytes : GemmLds<T, kApply, TT>::kBytes;
+  __shared__ __attribute__((aligned(16))) char lds[kBytes];
+  const int b = int(blockIdx.x);
+  if (b < main_grid) {
+    gemm_body<T, kApply, BT, LAST>(g, reinterpret_cast<T*>(lds), b, main_grid);
+  } else if (int(threadIdx.x) < TileGeom<TT>::kThreads) {
+    gemm_body<T, kApply, TT, LAST>(tail, reinterpret_cast<T*>(lds), b - main_grid, int(gridDim.x) - main_grid);
+  }
 }
 
 }  // namespace
@@ -1773,6 +1812,7 @@ hipError_t launch_norm(const PrepLaunch& l, hipStream_t stream) {
 
 hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
   if (l.max_count == 0) return hipSuccess;
+  if (l.tail_max_count > 0 && (mode != kApply || l.fp32 || l.tile != 256)) return hipErrorInvalidValue;
   GemmArgs a;
   a.mats = l.mats;
   a.bind = l.bind;
@@ -1813,7 +1853,32 @@ hipError_t launch_gemm(GemmMode mode, const GemmLaunch& l, hipStream_t stream) {
     else if (l.tile == 128) LM_LAUNCH_MODE(float, 128);
     else return hipErrorInvalidValue;
   } else if (l.tile == 256) {
-    LM_LAUNCH_MODE(bf16, 256);
+    if (mode == kApply && l.tail_max_count > 0) {
+      // with the last round's small tiles: one workgroup per CU at a time
+      // (the launch's LDS is the 256-tile's), persistent unless last
+      GemmArgs at = a;
+      at.tasks = l.tail_tasks;
+      at.split = l.tail_split;
+      const int t_xcd = l.last ? l.tail_max_count
+                               : (l.tail_max_count < l.chip.cus / l.chip.xcds ? l.tail_max_count
+                                                                              : l.chip.cus / l.chip.xcds);
+      const dim3 pair(grid.x + unsigned(t_xcd) * unsigned(l.chip.xcds));
+      const int32_t main_grid = int32_t(grid.x);
+#define LM_LAUNCH_PAIR(TT, LAST_) \
+  hipLaunchKernelGGL((ns_apply_pair_kernel<bf16, 256, TT, LAST_>), pair, dim3(TileGeom<256>::kThreads), 0, stream, a, at, main_grid)
+      if (l.tail_tile == 64) {
+        if (!l.last) LM_LAUNCH_PAIR(64, false);
+        else LM_LAUNCH_PAIR(64, true);
+      } else if (l.tail_tile == 128) {
+        if (!l.last) LM_LAUNCH_PAIR(128, false);
+        else LM_LAUNCH_PAIR(128, true);
+      } else {
+        return hipErrorInvalidValue;
+      }
+#undef LM_LAUNCH_PAIR
+    } else {
+      LM_LAUNCH_MODE(bf16, 256);
+    }
   } else if (l.tile == 128) {
     LM_LAUNCH_MODE(bf16, 128);
   } else {
