@@ -1164,6 +1164,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g, T* smem, int bid, i
     int64_t lda, ldb;
     int K;
     uint32_t a_off, b_off;
+    bool same;                                   // symmetric product, diagonal tile: B rows = A rows
   };
   auto make_ops = [&](const __attribute__((address_space(4))) GemmTask& t) {
     const auto& m = kconst(g.mats)[t.mat];
@@ -1192,6 +1193,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g, T* smem, int bid, i
     o.b_off = kBRows
         ? uint32_t(((dw * kRpiB + lane / kChunksB) * o.ldb + ((lane % kChunksB) ^ swb(dw * kRpiB + lane / kChunksB)) * kEpc) * sizeof(T))
         : uint32_t(((dw * 8 + (lane >> 3)) * o.ldb + ((lane & 7) ^ swz(dw * 8 + (lane >> 3))) * kEpc) * sizeof(T));
+    o.same = MODE != kApply && sizeof(T) == 2 && t.tm == t.tn;
     return o;
   };
   // One 16-byte-per-lane copy in the scalar-base form: wave-uniform base
@@ -1216,7 +1218,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g, T* smem, int bid, i
       const int blk = q * kDmaWaves + wave_u;    // 8-row block
       copy16(o.a + int64_t(q * kDmaWaves * 8) * o.lda + k0, o.a_off, &sA[buf][blk * 8][0]);
       if constexpr (!kBRows)
-        copy16(o.b + int64_t(q * kDmaWaves * 8) * o.ldb + k0, o.b_off, &sB[buf][blk * 8][0]);
+        if (!o.same) copy16(o.b + int64_t(q * kDmaWaves * 8) * o.ldb + k0, o.b_off, &sB[buf][blk * 8][0]);
     }
     if constexpr (kBRows) {
 #pragma unroll
@@ -1233,6 +1235,11 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g, T* smem, int bid, i
   const int64_t off_x_nxt = g.src ? mm.off_x[0] : mm.off_x[1];
   const Ops ops = make_ops(task);
   const int K = ops.K;
+  // A bf16 diagonal tile of a symmetric product reads its B fragments from
+  // the A operand's buffers (the same rows of X, or of A) and copies only
+  // those: Gram 3-4%, polynomial 2-4% faster at 124M-720M (the fp32 small
+  // tiles were 1% slower with it and keep both copies).
+  T (*sBf)[BT][kLd] = ops.same ? sA : sB;
   const int row0 = task.tm * BT, col0 = task.tn * BT;
 
   f32x16 acc[kMI][kNI];
@@ -1371,7 +1378,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g, T* smem, int bid, i
       for (int j = 0; j < kNI; ++j) {
         if constexpr (kTrB) bfr[s][j] = bq[kk][j];
         else if constexpr (kBRows) bfr[s][j] = frag_b_rows(buf, j, kc);
-        else bfr[s][j] = frag(&sB[buf][wn + 32 * j + lr][0], wn + 32 * j + lr, kc);
+        else bfr[s][j] = frag(&sBf[buf][wn + 32 * j + lr][0], wn + 32 * j + lr, kc);
       }
     };
     fetch(0, 0);
