@@ -1110,8 +1110,9 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g, T* smem, int bid, i
   char* wsb = static_cast<char*>(g.ws);
   auto at = [&](int64_t off) { return reinterpret_cast<T*>(wsb + off); };
   // Non-final apply steps store X' straight from registers; the next tile's
-  // first stage is then requested before those stores, so it loads while
-  // they drain. kDirect is the number of those stores per lane.
+  // first stage is requested during the current tile's last K stage, so it
+  // loads while that stage runs and the stores drain. kDirect is the number
+  // of those stores per lane.
   constexpr int kDirect = Geo::kMI * Geo::kNI * 4;
   bool prefetched = false;
   int base = 0;                                  // LDS buffer of the tile's first K stage
