@@ -1138,8 +1138,10 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g, T* smem, int bid, i
   // Waves that issue the operand copies: on 256-tiles only the first four
   // (one per SIMD), so that the other wave of each SIMD keeps the matrix core
   // busy while the issuing wave stalls on a full memory pipeline (measured:
-  // apply 0.5-0.9%, Gram 1-4%, polynomial 0-2.5% faster at 124M-720M).
-  constexpr int kDmaWaves = (BT == 256) ? kWaves / 2 : kWaves;
+  // apply 0.5-0.9%, Gram 1-4%, polynomial 0-2.5% faster at 124M-720M); on
+  // the 128-tiles of the Gram and polynomial products the first two
+  // (polynomial 2.5% faster at 124M).
+  constexpr int kDmaWaves = (BT == 256 || (BT == 128 && MODE != kApply)) ? kWaves / 2 : kWaves;
   constexpr int kInst = BT / 8 / kDmaWaves;      // wave instructions per operand per stage
   // k-major B rows (apply): kChunksB 16-byte chunks per row, each wave
   // instruction fills kRpiB rows; chunks are XOR-swizzled by swb(k) so that
