@@ -74,8 +74,9 @@ struct Plan {
   std::vector<GemmTask> gram[2], poly[2], apply[2];
   XcdSplit gram_split[2]{}, poly_split[2]{}, apply_split[2]{};
   // bf16 apply tiles past the last full round of 256-tiles (one per CU),
-  // when they fill at most half a round, each split into four 128-tiles
-  // (a second launch after `apply`)
+  // when they fill at most half a round, each split into sixteen 64-tiles
+  // (when those fit one round) or four 128-tiles, run by extra workgroups of
+  // the same launch as `apply`
   std::vector<GemmTask> apply_tail[2];
   XcdSplit apply_tail_split[2]{};
   int32_t tile[2][3] = {{kTileBig, kTileBig, kTileBig}, {kTileSmall, kTileSmall, kTileSmall}};

@@ -1,9 +1,13 @@
 """The host planner under AddressSanitizer and UndefinedBehaviorSanitizer.
 
 ``tests/planner_sanitizer_driver.cpp`` builds plans (tile lists, XCD splits,
-workspace layout, stable-rank tables) for the benchmark sets and for edge-case
-lists; this test compiles it with ``plan.cpp`` by g++ with both sanitizers and
-fails on any sanitizer report or rejected plan. Host code only: no HIP call.
+workspace layout, stable-rank tables) for the benchmark sets, for edge-case
+lists and for 60 seeded random lists, and checks each plan's work lists: every
+XCD split partitions its list, the symmetric products hold each lower-triangle
+tile once, and the apply's two lists cover each padded output exactly once.
+This test compiles it with ``plan.cpp`` by g++ with both sanitizers and fails on
+any sanitizer report, rejected plan or violated invariant. Host code only: no
+HIP call.
 """
 import os
 import shutil
