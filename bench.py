@@ -232,15 +232,20 @@ def sq_summary(wl_name, sq_csvs, command):
 
 def launch_gaps(trace_csv):
     """Idle time between consecutive library kernels in a rocprofv3 kernel
-    trace: gaps shorter than 50 us (back-to-back launches of one step; longer
-    ones are host-side pauses between timed regions)."""
+    trace, over gaps shorter than 50 us (longer ones are host-side pauses
+    between timed regions). Gaps under 0.5 us are counted apart: inside one
+    call without per-launch events the next kernel's start stamp is the
+    previous one's end (the dispatch cost falls inside the kernel durations);
+    the others follow the event records of the library (at the end of every
+    call, and around every launch while per-launch profiling is on)."""
     import csv
     ev = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
                 for r in csv.DictReader(open(trace_csv)) if phase_of(r["Kernel_Name"]))
     gaps = [b[0] - a[1] for a, b in zip(ev, ev[1:]) if 0 <= b[0] - a[1] < 50000]
+    rest = [x for x in gaps if x >= 500]
     busy = sum(e - s for s, e in ev)
-    return {"launches": len(ev), "gaps": len(gaps),
-            "mean_gap_us": sum(gaps) / len(gaps) / 1e3 if gaps else 0.0,
+    return {"launches": len(ev), "gaps": len(gaps), "zero": len(gaps) - len(rest),
+            "rest": len(rest), "mean_rest_us": sum(rest) / len(rest) / 1e3 if rest else 0.0,
             "gap_share": sum(gaps) / (sum(gaps) + busy) if ev else 0.0}
 
 
@@ -279,8 +284,11 @@ def trace_summary(wl_name, stats_csv, command, trace_csv=None):
     if trace_csv:
         g = launch_gaps(trace_csv)
         lines += ["", f"Between consecutive library kernels (per-dispatch timestamps, {g['launches']} "
-                  f"dispatches): mean idle gap {g['mean_gap_us']:.2f} us over {g['gaps']} "
-                  f"back-to-back pairs, {100 * g['gap_share']:.1f}% of the kernels' timeline."]
+                  f"dispatches, {g['gaps']} back-to-back pairs): {g['zero']} pairs with no idle "
+                  f"time (within a call, per-launch events off), {g['rest']} pairs with a mean gap of "
+                  f"{g['mean_rest_us']:.2f} us (after the end-of-call event records, and around "
+                  f"every launch while per-launch events are on); all gaps together "
+                  f"{100 * g['gap_share']:.1f}% of the kernels' timeline."]
     path = os.path.join(TRAFFIC_DIR, f"kernel_trace_{wl_name}.md")
     with open(path, "w") as f:
         f.write("\n".join(lines) + "\n")
