@@ -1412,6 +1412,9 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g, T* smem, int bid, i
       else wait_vmcnt<0>();
     } else {
       static_assert(kNBuf == 4, "stage waits written out for 2 or 4 buffers");
+      // the counts assume kOps copies per stage: a diagonal tile of a
+      // symmetric product copies one operand only
+      static_assert(MODE == kApply, "four stages only for the apply");
       const int n = later < kNBuf - 2 ? later : kNBuf - 2;
       if (stores) {
         if (n >= 2) wait_vmcnt<kDirect + 2 * kOps>();
