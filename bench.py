@@ -249,7 +249,39 @@ def launch_gaps(trace_csv):
             "gap_share": sum(gaps) / (sum(gaps) + busy) if ev else 0.0}
 
 
-def trace_summary(wl_name, stats_csv, command, trace_csv=None):
+# order of the phases within one call: a dispatch whose phase comes earlier
+# than the previous dispatch's (or repeats a phase launched once per call)
+# starts the next call
+_CALL_ORDER = {"srank": 0, "lion": 1, "prep": 2, "norm": 3, "gram": 4, "poly": 4, "apply": 4}
+
+
+def profiled_dispatches(trace_csv, warmup, steps, trailing):
+    """Library dispatches of the profiled steps of one bench run, read from
+    its rocprofv3 kernel trace: the run makes `warmup` calls, `steps` timed
+    calls with per-launch events off, `steps` with them on (the profiled
+    ones) and `trailing` more. Returns [(kernel name, duration ns)], or None
+    when the trace does not split into that many calls."""
+    import csv
+    ev = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"])
+                for r in csv.DictReader(open(trace_csv)) if phase_of(r["Kernel_Name"]))
+    # A Muon call starts with the Lion kernel when the list has Lion-branch
+    # tensors, else with the preparation kernel: try the second reading when
+    # the first does not give the run's number of calls.
+    for prep_starts in (False, True):
+        calls, prev = [], None
+        for s, e, name in ev:
+            rank = _CALL_ORDER[phase_of(name)]
+            if (prev is None or rank < prev or (rank == prev and rank in (1, 2, 3))
+                    or (prep_starts and rank == 2)):
+                calls.append([])
+            calls[-1].append((name, e - s))
+            prev = rank
+        if len(calls) == warmup + 2 * steps + trailing:
+            return [d for c in calls[warmup + steps:warmup + 2 * steps] for d in c]
+    return None
+
+
+def trace_summary(wl_name, stats_csv, command, trace_csv=None, calls=None):
     """Text summary of a rocprofv3 --kernel-trace --stats run."""
     import csv
     rows = list(csv.DictReader(open(stats_csv)))
@@ -275,12 +307,32 @@ def trace_summary(wl_name, stats_csv, command, trace_csv=None):
             t["n_256"] += int(r["Calls"])
         if "srank_decide" in r["Name"]:
             t["n_decide"] += int(r["Calls"])
-    lines += ["", "Per phase launch (all of a phase's kernels; launches = its 256-tile dispatches "
-              "where there are any, the decide dispatches for srank):", "",
-              "| phase | launches | avg us per launch |", "|---|---|---|"]
-    for ph, t in sorted(tot.items(), key=lambda kv: -kv[1]["ns"]):
+    # the same over the profiled steps only (per-launch events on: the
+    # region whose per-launch times bench.py reports), after the clock under
+    # load has settled; the whole run includes the first, slower steps
+    prof = {}
+    for name, ns in ((profiled_dispatches(trace_csv, *calls) if trace_csv and calls else None)
+                     or []):
+        t = prof.setdefault(phase_of(name), {"ns": 0.0, "n_all": 0, "n_256": 0, "n_decide": 0})
+        t["ns"] += ns
+        t["n_all"] += 1
+        t["n_256"] += "Li256" in name
+        t["n_decide"] += "srank_decide" in name
+
+    def per_launch(ph, t):
         n = t["n_decide"] if ph == "srank" else (t["n_256"] or t["n_all"])
-        lines.append(f"| {ph} | {n} | {t['ns'] / n / 1e3:.1f} |")
+        return n, t["ns"] / n / 1e3
+
+    lines += ["", "Per phase launch (all of a phase's kernels; launches = its 256-tile dispatches "
+              "where there are any, the decide dispatches for srank), over the whole run and "
+              "over the profiled steps (the last timed region, per-launch events on, the one "
+              "whose per-launch times bench.py reports):", "",
+              "| phase | launches | avg us per launch | profiled launches | avg us per launch, "
+              "profiled steps |", "|---|---|---|---|---|"]
+    for ph, t in sorted(tot.items(), key=lambda kv: -kv[1]["ns"]):
+        n, avg = per_launch(ph, t)
+        pn, pavg = per_launch(ph, prof[ph]) if ph in prof else (0, float("nan"))
+        lines.append(f"| {ph} | {n} | {avg:.1f} | {pn} | {pavg:.1f} |")
     if trace_csv:
         g = launch_gaps(trace_csv)
         lines += ["", f"Between consecutive library kernels (per-dispatch timestamps, {g['launches']} "
@@ -583,8 +635,14 @@ def main():
         return
     if args.trace_summary:
         trace_csv = args.trace_summary.replace("kernel_stats.csv", "kernel_trace.csv")
+        # the profiled run's calls: warm-up, timed, profiled (whole periods)
+        # and, for the adaptive variant, one more step that reads decisions
+        steps = args.steps
+        if args.P > 1 and steps % args.P and args.adaptive <= 0.0:
+            steps += args.P - steps % args.P
+        calls = (args.warmup, steps, 1 if args.adaptive > 0.0 else 0)
         print(trace_summary(prof_name, args.trace_summary, args.command,
-                            trace_csv if os.path.exists(trace_csv) else None))
+                            trace_csv if os.path.exists(trace_csv) else None, calls))
         return
     if args.sq_summary:
         print(sq_summary(prof_name, args.sq_summary, args.command))
