@@ -352,6 +352,91 @@ def test_many_small_tensors_in_one_call():
         check_lion(W1[i], G[i], M1[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_l, wd)
 
 
+def _placed(x, offset):
+    """Device copy of x inside a zeroed buffer with one guard element on each
+    side; offset 1 puts it 4 bytes past a 16-byte boundary."""
+    n = x.size
+    buf = torch.zeros(n + 8, device=DEV)
+    view = buf[offset:offset + n].view(x.shape)
+    view.copy_(dev(x))
+    return buf, view
+
+
+def _random_list(seed, big):
+    """Seeded random list: `big` lists hold 12-30 tensors with short sides
+    200-1100 (several rounds of 256-tiles), the others 3-8 tensors with short
+    sides 2-1100; long sides up to 2600, either orientation."""
+    rng = np.random.default_rng([101, seed])
+    p_vec = 0.05 if big else 0.15
+    shapes, lion_only, offsets = [], [], []
+    for _ in range(int(rng.integers(12, 31)) if big else int(rng.integers(3, 9))):
+        if rng.random() < p_vec:
+            shapes.append((1, int(rng.integers(1, 5000))))
+        else:
+            s = int(rng.integers(200 if big else 2, 1101))
+            l = int(rng.integers(s, 2601))
+            shapes.append((s, l) if rng.random() < 0.5 else (l, s))
+        lion_only.append(bool(rng.random() < p_vec))
+        offsets.append(int(rng.random() < 0.3))
+    return shapes, lion_only, offsets
+
+
+# (seed, big, edge of the apply's last-round tiles): the big lists' seeds are
+# chosen so that their bf16 apply lists end in a full last round (6), a last
+# round run as 128-tiles (7, 8, 9; 8 at the largest such round, 128 tiles)
+# or as 64-tiles (22, 33)
+RANDOM_LISTS = [(s, False, None) for s in range(6)] + [
+    (6, True, None), (7, True, 128), (8, True, 128), (9, True, 128), (22, True, 64),
+    (33, True, 64)]
+
+
+@pytest.mark.parametrize("seed,big,tail", RANDOM_LISTS)
+def test_random_lists_match_oracle(seed, big, tail):
+    """Seeded random tensor lists: matrices of random shape and orientation
+    (so the Newton-Schulz work lists take random mixes of tile depths, last
+    rounds and fp32 small matrices), some flagged Lion-only, some 1-D, some 4
+    bytes past a 16-byte boundary; NS in bf16 or fp32, kappa 1 or
+    0.2 sqrt(max(m, n)). A Muon step (t = 0), then a Lion step (t = 1) on the
+    state it leaves; every tensor checked against the oracle, and guard
+    elements around every buffer untouched."""
+    shapes, lion_only, offsets = _random_list(seed, big)
+    precision = "fp32" if seed % 3 == 2 and not big else "bf16"
+    scale = "rms02" if seed % 2 else "none"
+    W0, M0, G = _state(shapes, [102, seed])
+    placed = [[_placed(x[i], offsets[i]) for i in range(len(shapes))] for x in (W0, M0, G)]
+    W, M, Gd = ([v for _, v in p] for p in placed)
+    lr_m, lr_l, wd = 0.02, 1e-3, 0.1
+    cfg = lm.config(ns_precision=precision, ns_scale=scale, lr_muon=lr_m, lr_lion=lr_l)
+    info = lm.lionmuon_plan_info([(*sh, lo) for sh, lo in zip(shapes, lion_only)], t=0, P=2,
+                                 cfg=cfg)
+    print(f"random list {seed}: {precision} {scale} {list(zip(shapes, lion_only, offsets))} "
+          f"apply tiles {info['apply_tiles']}", flush=True)
+    if big:
+        n = sum(-(-min(sh) // 256) * -(-max(sh) // 256)
+                for sh, lo in zip(shapes, lion_only) if not lo and min(sh) > 1)
+        split = {None: 1, 128: 2, 64: 4}[tail]
+        assert n > 256 and info["apply_tiles"] == n - n % 256 + (n % 256) * split * split
+    lm.lionmuon_step_ex(W, Gd, M, 0, 2, 0.9, 0.99, wd, cfg, lion_only=lion_only)
+    sync()
+    W1, M1 = [host(x) for x in W], [host(x) for x in M]
+    for i, s in enumerate(shapes):
+        if lion_only[i] or min(s) == 1:
+            check_lion(W0[i], G[i], M0[i], W1[i], M1[i], 0.9, 0.99, lr_l, wd)
+        else:
+            kappa = 0.2 * np.sqrt(max(s)) if scale == "rms02" else 1.0
+            prec = "bf16" if precision == "bf16" and min(s) >= 64 else "fp32"
+            check_muon(W0[i], G[i], M0[i], W1[i], M1[i], 0.9, 0.99, lr_m, wd, prec, kappa=kappa)
+    print(f"random list {seed}: Lion step", flush=True)
+    lm.lionmuon_step_ex(W, Gd, M, 1, 2, 0.9, 0.99, wd, cfg, lion_only=lion_only)
+    sync()
+    for i in range(len(shapes)):
+        check_lion(W1[i], G[i], M1[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_l, wd)
+    for p in placed:
+        for (buf, _), off, sh in zip(p, offsets, shapes):
+            n = sh[0] * sh[1]
+            assert torch.all(buf[:off] == 0) and torch.all(buf[off + n:] == 0)
+
+
 @pytest.mark.parametrize("t,P", [(0, 2), (1, 2), (5, 0)])
 def test_adamw_tensors_in_mixed_list(t, P):
     """1-D tensors (and a matrix) flagged AdamW take AdamW every step
