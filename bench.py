@@ -255,33 +255,47 @@ def launch_gaps(trace_csv):
 _CALL_ORDER = {"srank": 0, "lion": 1, "prep": 2, "norm": 3, "gram": 4, "poly": 4, "apply": 4}
 
 
-def profiled_dispatches(trace_csv, warmup, steps, trailing):
+def _split_calls(ev, prep_starts):
+    calls, prev = [], None
+    for s, e, name in ev:
+        rank = _CALL_ORDER[phase_of(name)]
+        if (prev is None or rank < prev or (rank == prev and rank in (1, 2, 3))
+                or (prep_starts and rank == 2)):
+            calls.append([])
+        calls[-1].append((name, e - s))
+        prev = rank
+    return calls
+
+
+def profiled_dispatches(trace_csv, warmup, steps, trailing, lion_in_muon=None):
     """Library dispatches of the profiled steps of one bench run, read from
-    its rocprofv3 kernel trace: the run makes `warmup` calls, `steps` timed
-    calls with per-launch events off, `steps` with them on (the profiled
-    ones) and `trailing` more. Returns [(kernel name, duration ns)], or None
-    when the trace does not split into that many calls."""
+    its rocprofv3 kernel trace. A `--single` run makes `warmup` calls, `steps`
+    timed calls with per-launch events off, `steps` with them on (the
+    profiled ones) and `trailing` more. With `warmup` None the run is the
+    default one (every configuration, the headline last): its profiled steps
+    are its last `steps` calls, and `lion_in_muon` tells whether the headline
+    set's Muon calls start with the Lion kernel (a set with Lion-branch
+    tensors) or with the preparation kernel. Returns [(kernel name, duration
+    ns)], or None when the trace does not split into that many calls."""
     import csv
     ev = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"])
                 for r in csv.DictReader(open(trace_csv)) if phase_of(r["Kernel_Name"]))
+    if warmup is None:
+        calls = _split_calls(ev, prep_starts=not lion_in_muon)
+        if len(calls) < steps + trailing:
+            return None
+        return [d for c in calls[len(calls) - trailing - steps:len(calls) - trailing] for d in c]
     # A Muon call starts with the Lion kernel when the list has Lion-branch
     # tensors, else with the preparation kernel: try the second reading when
     # the first does not give the run's number of calls.
     for prep_starts in (False, True):
-        calls, prev = [], None
-        for s, e, name in ev:
-            rank = _CALL_ORDER[phase_of(name)]
-            if (prev is None or rank < prev or (rank == prev and rank in (1, 2, 3))
-                    or (prep_starts and rank == 2)):
-                calls.append([])
-            calls[-1].append((name, e - s))
-            prev = rank
+        calls = _split_calls(ev, prep_starts)
         if len(calls) == warmup + 2 * steps + trailing:
             return [d for c in calls[warmup + steps:warmup + 2 * steps] for d in c]
     return None
 
 
-def trace_summary(wl_name, stats_csv, command, trace_csv=None, calls=None):
+def trace_summary(wl_name, stats_csv, command, trace_csv=None, calls=None, file_tag=None):
     """Text summary of a rocprofv3 --kernel-trace --stats run."""
     import csv
     rows = list(csv.DictReader(open(stats_csv)))
@@ -323,10 +337,14 @@ def trace_summary(wl_name, stats_csv, command, trace_csv=None, calls=None):
         n = t["n_decide"] if ph == "srank" else (t["n_256"] or t["n_all"])
         return n, t["ns"] / n / 1e3
 
+    scope = ("over the whole run (every configuration of the default run, so the first "
+             "columns mix the sets) and over the headline's profiled steps (its last timed "
+             "region, per-launch events on, whose per-launch times the bench line reports)"
+             if file_tag == "default_run" else
+             "over the whole run and over the profiled steps (the last timed region, "
+             "per-launch events on, the one whose per-launch times bench.py reports)")
     lines += ["", "Per phase launch (all of a phase's kernels; launches = its 256-tile dispatches "
-              "where there are any, the decide dispatches for srank), over the whole run and "
-              "over the profiled steps (the last timed region, per-launch events on, the one "
-              "whose per-launch times bench.py reports):", "",
+              f"where there are any, the decide dispatches for srank), {scope}:", "",
               "| phase | launches | avg us per launch | profiled launches | avg us per launch, "
               "profiled steps |", "|---|---|---|---|---|"]
     for ph, t in sorted(tot.items(), key=lambda kv: -kv[1]["ns"]):
@@ -341,7 +359,7 @@ def trace_summary(wl_name, stats_csv, command, trace_csv=None, calls=None):
                   f"{g['mean_rest_us']:.2f} us (after the end-of-call event records, and around "
                   f"every launch while per-launch events are on); all gaps together "
                   f"{100 * g['gap_share']:.1f}% of the kernels' timeline."]
-    path = os.path.join(TRAFFIC_DIR, f"kernel_trace_{wl_name}.md")
+    path = os.path.join(TRAFFIC_DIR, f"kernel_trace_{file_tag or wl_name}.md")
     with open(path, "w") as f:
         f.write("\n".join(lines) + "\n")
     return path
@@ -641,8 +659,15 @@ def main():
         if args.P > 1 and steps % args.P and args.adaptive <= 0.0:
             steps += args.P - steps % args.P
         calls = (args.warmup, steps, 1 if args.adaptive > 0.0 else 0)
+        tag = None
+        if not args.single and args.adaptive <= 0.0:
+            # the default command: the headline's profiled steps end the run
+            wl = workloads.get(args.workload)
+            lion_in_muon = any(t.lion_only or t.rows == 1 for t in wl.tensors)
+            calls = (None, steps, 0, lion_in_muon)
+            tag = "default_run"
         print(trace_summary(prof_name, args.trace_summary, args.command,
-                            trace_csv if os.path.exists(trace_csv) else None, calls))
+                            trace_csv if os.path.exists(trace_csv) else None, calls, tag))
         return
     if args.sq_summary:
         print(sq_summary(prof_name, args.sq_summary, args.command))

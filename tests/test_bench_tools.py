@@ -69,6 +69,22 @@ def test_profiled_steps_of_a_periodic_run(tmp_path, lion_first):
     assert got == want
 
 
+@pytest.mark.parametrize("lion_first", [False, True])
+def test_profiled_steps_of_the_default_run(tmp_path, lion_first):
+    # the default run measures the other sets first (Muon calls starting
+    # with the preparation kernel, with the Lion kernel, pure Lion calls) and
+    # the headline set last; its profiled steps are the run's last 20 calls
+    others = (period_calls(45, 1, 2, False) + period_calls(45, 1, 2, True) + [[LION]] * 45
+              + period_calls(45, 1, 1, False))
+    head = period_calls(45, 1, 2, lion_first)
+    calls = others + head
+    path = str(tmp_path / "trace.csv")
+    write_trace(path, calls, len(calls) - 20, len(calls), foreign_every=11)
+    got = bench.profiled_dispatches(path, None, 20, 0, lion_in_muon=lion_first)
+    assert got == [(name, 1000 + ci) for ci in range(len(calls) - 20, len(calls))
+                   for name in calls[ci]]
+
+
 def test_profiled_steps_of_an_adaptive_run(tmp_path):
     warmup, steps = 5, 20
     call = SRANK[:2] * 6 + SRANK[2:] + muon_call(True)
