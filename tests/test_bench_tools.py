@@ -126,3 +126,62 @@ def test_launch_gaps_count_back_to_back_pairs_apart(tmp_path):
     # 8 us after every call but the last, 7.7 us between the kernels of a profiled call
     assert g["mean_rest_us"] == pytest.approx(
         (8.0 * (len(calls) - 1) + 7.7 * inside_evented) / g["rest"])
+
+
+# --------------------------------------------------------------------------
+# Algorithmic units of the bench line's rates and rooflines
+# --------------------------------------------------------------------------
+# The matrix sets written out from their definitions (per layer: qkv, attention
+# projection, MLP in, MLP out), independent of the workload tables.
+SETS = {"gpt2-124m": (12, 768), "gpt2-355m": (24, 1024), "gpt2-720m": (36, 1280)}
+
+
+def _closed_form_ns_flops(layers, d, K=5):
+    shapes = [(d, 3 * d), (d, d), (d, 4 * d), (4 * d, d)]
+    total = 0
+    for m, n in shapes:
+        s, l = min(m, n), max(m, n)
+        total += s * (s + 1) * l + s * s * (s + 1) + 2 * s * s * l   # Gram, polynomial, apply
+    return K * layers * total
+
+
+@pytest.mark.parametrize("name", sorted(SETS))
+def test_ns_flop_counts_agree(name):
+    """bench.py's per-launch flops (the roofline's numerator), the planner's
+    count and the closed form over the set's shapes are one number; the 124M,
+    355M and 720M totals are 1.088, 5.156 and 15.104 TFLOP per Muon step."""
+    import workloads
+    from paper_2605_19811_amd import lionmuon as lm
+    wl = workloads.get(name)
+    per_launch = bench.ns_flops_per_launch(wl)
+    ours = 5 * sum(per_launch.values())
+    closed = _closed_form_ns_flops(*SETS[name])
+    specs = [(t.rows, t.cols, t.lion_only) for t in wl.tensors]
+    planner = lm.lionmuon_plan_info(specs, t=0, P=1)["ns_flops"]
+    assert ours == closed == planner
+    assert closed / 1e12 == pytest.approx({"gpt2-124m": 1.088, "gpt2-355m": 5.156,
+                                           "gpt2-720m": 15.104}[name], abs=5e-4)
+
+
+@pytest.mark.parametrize("name,gb", [("gpt2-124m", 1.699), ("gpt2-355m", 6.040),
+                                     ("gpt2-720m", 15.454)])
+def test_lion_bytes_per_step(name, gb):
+    """20 bytes per element on a Lion step (read W, G, M; write W, M), over
+    every tensor including the 720M set's Lion-only embedding and vectors."""
+    import workloads
+    from paper_2605_19811_amd import lionmuon as lm
+    wl = workloads.get(name)
+    specs = [(t.rows, t.cols, t.lion_only) for t in wl.tensors]
+    info = lm.lionmuon_plan_info(specs, t=1, P=2)
+    assert info["lion_bytes"] == 20.0 * sum(t.numel for t in wl.tensors)
+    assert info["lion_bytes"] / 1e9 == pytest.approx(gb, abs=5e-4)
+
+
+def test_cpu_baseline_amortisation():
+    times = (0.5, 3.5, 16, "sample")
+    assert bench.cpu_baseline_for(times, 0)["value"] == 500.0
+    assert bench.cpu_baseline_for(times, 1)["value"] == 3500.0
+    assert bench.cpu_baseline_for(times, 2)["value"] == 2000.0
+    assert bench.cpu_baseline_for(times, 4)["value"] == 1250.0
+    b = bench.cpu_baseline_for(times, 2)
+    assert b["kind"] == "oracle" and b["cores"] == 16 and b["unit"] == "ms/step"
