@@ -77,6 +77,34 @@ def test_noalloc_matches_step_ex_on_consecutive_calls():
     _check(small, [False, False], 84, 3, 3, "fp32")
 
 
+def test_noalloc_matches_step_ex_on_random_lists():
+    """Twelve seeded random lists in a row (3-8 tensors of random shape and
+    orientation, some 1-D or Lion-only; both precisions; Muon and Lion
+    steps): every call rewrites the scratch's tables, and each result is
+    bitwise that of lionmuon_step_ex and checked against the oracle."""
+    rng = np.random.default_rng(86)
+    done = 0
+    for k in range(12):
+        shapes, lion_only = [], []
+        for _ in range(int(rng.integers(3, 9))):
+            if rng.random() < 0.2:
+                shapes.append((1, int(rng.integers(1, 3000))))
+            else:
+                s = int(rng.integers(2, 700))
+                l = int(rng.integers(s, 1800))
+                shapes.append((s, l) if rng.random() < 0.5 else (l, s))
+            lion_only.append(bool(rng.random() < 0.15))
+        precision = "fp32" if k % 4 == 3 else "bf16"
+        t, P = (0, 2) if k % 3 else (1, 2)
+        cfg = lm.config(ns_precision=precision)
+        need = lm.lionmuon_workspace_bytes([(*sh, lo) for sh, lo in zip(shapes, lion_only)], cfg)
+        if need > lm.NOALLOC_SCRATCH_BYTES - (4 << 20):    # room for the tables
+            continue
+        _check(shapes, lion_only, [87, k], t, P, precision)
+        done += 1
+    assert done >= 10
+
+
 def test_noalloc_rejects_a_list_beyond_its_scratch():
     """A Muon step whose workspace exceeds the scratch is refused before
     anything is enqueued; a Lion step on the same list (no workspace) runs."""
