@@ -351,3 +351,64 @@ def test_adaptive_caller_workspace_on_misaligned_tensors():
             check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 0.02, 0.1, "fp32")
         else:
             check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, 1e-3, 0.1)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_adaptive_random_lists(seed):
+    """Seeded random lists (4-10 tensors of random shape and orientation,
+    short sides 2-900, some 1-D or Lion-only, some 4 bytes past a 16-byte
+    boundary so that their passes take the generic path), momenta of low
+    stable rank (rank 1-4 plus noise) or Gaussian, random alpha, power-step
+    count and NS precision: estimates and decisions against the oracle, every
+    tensor's update against the branch it took, guard elements untouched."""
+    rng = np.random.default_rng([93, seed])
+    shapes, lion_only, offsets, low = [], [], [], []
+    for _ in range(int(rng.integers(4, 11))):
+        if rng.random() < 0.15:
+            shapes.append((1, int(rng.integers(1, 3000))))
+        else:
+            s = int(rng.integers(2, 901))
+            l = int(rng.integers(s, 2101))
+            shapes.append((s, l) if rng.random() < 0.5 else (l, s))
+        lion_only.append(bool(rng.random() < 0.1))
+        offsets.append(int(rng.random() < 0.3))
+        low.append(bool(rng.random() < 0.5))
+    alpha = float(rng.choice([0.01, 0.05, 0.1]))
+    k = int(rng.choice([2, 5]))
+    precision = "fp32" if seed % 2 else "bf16"
+    W0 = [(rng.standard_normal(s) * 0.02).astype(np.float32) for s in shapes]
+    G = [(rng.standard_normal(s) * 1e-2).astype(np.float32) for s in shapes]
+    M0 = [low_rank_momentum([93, seed, i], s, 1 + i % 4, 1e-3) if low[i] and min(s) > 1 else
+          (rng.standard_normal(s) * 1e-2).astype(np.float32) for i, s in enumerate(shapes)]
+    bufs, views = [], []
+    for x in (W0, M0, G):
+        b = [torch.zeros(a.size + 8, device=DEV) for a in x]
+        v = [bb[o:o + a.size].view(a.shape) for bb, o, a in zip(b, offsets, x)]
+        for vv, a in zip(v, x):
+            vv.copy_(dev(a))
+        bufs.append(b)
+        views.append(v)
+    W, M, Gd = views
+    cands = {i for i, s in enumerate(shapes) if min(s) > 1 and not lion_only[i]}
+    dec = torch.full((len(shapes),), 7, dtype=torch.int32, device=DEV)
+    sr = torch.full((len(shapes),), 7.0, dtype=torch.float64, device=DEV)
+    lr_m, lr_l, wd = 0.02, 1e-3, 0.1
+    cfg = lm.config(ns_precision=precision, lr_muon=lr_m, lr_lion=lr_l, adaptive_alpha=alpha,
+                    adaptive_power_steps=k)
+    print(f"adaptive random list {seed}: alpha={alpha} k={k} {precision} "
+          f"{list(zip(shapes, lion_only, offsets, low))}", flush=True)
+    lm.lionmuon_step_adaptive(W, Gd, M, 3, 0.9, 0.99, wd, cfg, lion_only=lion_only,
+                              decisions=dec, stable_rank=sr)
+    torch.cuda.synchronize()
+    dec, sr = dec.cpu().numpy(), sr.cpu().numpy()
+    check_decisions(M0, cands, dec, sr, alpha, k)
+    assert 0 < sum(dec[i] for i in cands) < len(cands)     # both branches taken
+    for i, s in enumerate(shapes):
+        if dec[i]:
+            prec = "bf16" if precision == "bf16" and min(s) >= 64 else "fp32"
+            check_muon(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_m, wd, prec)
+        else:
+            check_lion(W0[i], G[i], M0[i], host(W[i]), host(M[i]), 0.9, 0.99, lr_l, wd)
+    for b, x in zip(bufs, (W0, M0, G)):
+        for bb, o, a in zip(b, offsets, x):
+            assert torch.all(bb[:o] == 0) and torch.all(bb[o + a.size:] == 0)
